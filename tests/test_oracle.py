@@ -1,0 +1,240 @@
+"""Pins for the CPU oracle (runs without a GPU).
+
+Each check ties the oracle to something other than itself: library routines
+(scipy's 2-D convolution, torch float64 autograd), a hand-derived worked
+example, closed forms, invariants of the layer (adjoint identity, linearity,
+shift behaviour), exact finite differences of a bilinear form, and the
+explicit-DFT route of the convolution theorem. Shapes are asymmetric and
+random so that a transposed operand, a missing flip, a wrong offset or a
+dropped term fails at least one of them.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.signal
+import torch
+
+import oracle
+from oracle import oaa
+from tests.conftest import relerr
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+SHAPES = [  # (B, C, K, N, n): partial blocks, n = 1, N = n, n even / odd
+    (1, 3, 4, 32, 5),
+    (2, 2, 3, 13, 4),
+    (1, 1, 1, 9, 3),
+    (2, 3, 2, 11, 1),
+    (1, 2, 2, 7, 7),
+    (1, 1, 2, 10, 6),
+    (3, 2, 3, 17, 8),
+]
+
+
+def _rand(shape, seed):
+    rng = np.random.default_rng(seed)
+    B, C, K, N, n = shape
+    M = N - n + 1
+    return (rng.uniform(-1, 1, (B, C, N, N)), rng.standard_normal((K, C, n, n)),
+            rng.uniform(-1, 1, (B, K, M, M)))
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_forward_matches_scipy_convolve2d(shape):
+    x, w, _ = _rand(shape, 1)
+    B, C, K, N, n = shape
+    ref = np.zeros((B, K, N - n + 1, N - n + 1))
+    for b in range(B):
+        for k in range(K):
+            for c in range(C):
+                ref[b, k] += scipy.signal.convolve2d(x[b, c], w[k, c], mode="valid")
+    assert relerr(oracle.conv_forward(x, w), ref) < 1e-13
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_three_passes_match_torch_float64_autograd(shape):
+    x, w, g = _rand(shape, 2)
+    xt = torch.tensor(x, requires_grad=True)
+    wf = torch.tensor(w[:, :, ::-1, ::-1].copy(), requires_grad=True)  # conv2d correlates
+    y = torch.nn.functional.conv2d(xt, wf)
+    (y * torch.tensor(g)).sum().backward()
+    assert relerr(oracle.conv_forward(x, w), y.detach().numpy()) < 1e-13
+    assert relerr(oracle.conv_backward_data(g, w, shape[3]), xt.grad.numpy()) < 1e-13
+    assert relerr(oracle.conv_backward_filter(x, g, shape[4]),
+                  wf.grad.numpy()[:, :, ::-1, ::-1]) < 1e-13
+
+
+def test_hand_derived_worked_example():
+    d = json.load(open(os.path.join(GOLD, "worked_4x4_2x2.json")))
+    x = np.array(d["x"], float)[None, None]
+    w = np.array(d["w"], float)[None, None]
+    g = np.array(d["g"], float)[None, None]
+    np.testing.assert_array_equal(oracle.conv_forward(x, w)[0, 0], np.array(d["y"]))
+    np.testing.assert_array_equal(oracle.conv_backward_data(g, w, 4)[0, 0], np.array(d["dx"]))
+    np.testing.assert_array_equal(oracle.conv_backward_filter(x, g, 2)[0, 0], np.array(d["dw"]))
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 3, 8, 3), (2, 1, 2, 12, 5), (1, 3, 1, 6, 1), (1, 1, 1, 5, 5)])
+def test_forward_matches_explicit_dft(shape):
+    x, w, _ = _rand(shape, 3)
+    assert relerr(oracle.conv_forward(x, w), oracle.dft_conv_forward(x, w)) < 1e-12
+    # any transform size past N+n-1 gives the same linear convolution
+    N, n = shape[3], shape[4]
+    assert relerr(oracle.conv_forward(x, w), oracle.dft_conv_forward(x, w, Lc=N + n + 4)) < 1e-12
+
+
+def test_explicit_dft_detects_aliasing():
+    # a transform shorter than N+n-1 must be refused, not silently wrap around
+    x, w, _ = _rand((1, 1, 1, 8, 3), 4)
+    with pytest.raises(ValueError):
+        oracle.dft_conv_forward(x, w, Lc=9)
+
+
+@pytest.mark.parametrize("n,N", [(3, 9), (4, 10), (1, 5), (5, 5)])
+def test_delta_kernels(n, N):
+    rng = np.random.default_rng(5)
+    x = rng.uniform(-1, 1, (2, 1, N, N))
+    M = N - n + 1
+    w = np.zeros((1, 1, n, n))
+    w[0, 0, 0, 0] = 1.0   # true convolution: y[i,j] = x[i+n-1, j+n-1]
+    np.testing.assert_array_equal(oracle.conv_forward(x, w)[:, 0], x[:, 0, n - 1:, n - 1:])
+    w[0, 0, 0, 0] = 0.0
+    w[0, 0, n - 1, n - 1] = 1.0   # y = x[:M, :M]
+    np.testing.assert_array_equal(oracle.conv_forward(x, w)[:, 0], x[:, 0, :M, :M])
+    w[0, 0, n - 1, n - 1] = 0.0
+    w[0, 0, 0, n - 1] = 1.0       # rows shifted, columns not: y = x[n-1:, :M]
+    np.testing.assert_array_equal(oracle.conv_forward(x, w)[:, 0], x[:, 0, n - 1:, :M])
+
+
+@pytest.mark.parametrize("shape", [(2, 3, 4, 9, 3), (1, 2, 3, 10, 4), (3, 1, 2, 7, 7), (1, 1, 1, 6, 1)])
+def test_all_ones_closed_forms(shape):
+    B, C, K, N, n = shape
+    M = N - n + 1
+    x = np.ones((B, C, N, N))
+    w = np.ones((K, C, n, n))
+    g = np.ones((B, K, M, M))
+    np.testing.assert_array_equal(oracle.conv_forward(x, w), np.full((B, K, M, M), C * n * n))
+    # dx[p,q] = K * cnt(p) * cnt(q), cnt(p) = #{u < n : 0 <= p-n+1+u < M}
+    cnt = np.array([min(p, M - 1) - max(0, p - n + 1) + 1 for p in range(N)], float)
+    np.testing.assert_array_equal(oracle.conv_backward_data(g, w, N),
+                                  np.broadcast_to(K * np.outer(cnt, cnt), (B, C, N, N)))
+    np.testing.assert_array_equal(oracle.conv_backward_filter(x, g, n),
+                                  np.full((K, C, n, n), B * M * M))
+
+
+def test_separable_kernel_is_row_then_column_1d_convolution():
+    rng = np.random.default_rng(6)
+    N, n = 15, 4
+    x = rng.uniform(-1, 1, (1, 1, N, N))
+    a, bvec = rng.standard_normal(n), rng.standard_normal(n)
+    w = np.outer(a, bvec)[None, None]
+    rows = np.stack([np.convolve(r, bvec, mode="valid") for r in x[0, 0]])
+    ref = np.stack([np.convolve(col, a, mode="valid") for col in rows.T]).T
+    assert relerr(oracle.conv_forward(x, w)[0, 0], ref) < 1e-13
+
+
+def test_shift_equivariance():
+    rng = np.random.default_rng(7)
+    x = rng.uniform(-1, 1, (1, 2, 16, 16))
+    w = rng.standard_normal((3, 2, 4, 4))
+    y = oracle.conv_forward(x, w)
+    ys = oracle.conv_forward(x[:, :, 2:14, 3:15], w)      # 12x12 window, shifted by (2, 3)
+    np.testing.assert_allclose(ys, y[:, :, 2:11, 3:12], rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_adjoint_identity_and_linearity(shape):
+    x, w, g = _rand(shape, 8)
+    N, n = shape[3], shape[4]
+    y = oracle.conv_forward(x, w)
+    dx = oracle.conv_backward_data(g, w, N)
+    dw = oracle.conv_backward_filter(x, g, n)
+    a, b, c = np.vdot(y, g), np.vdot(x, dx), np.vdot(w, dw)
+    scale = np.sum(np.abs(y) * np.abs(g))
+    assert abs(a - b) < 1e-13 * scale and abs(a - c) < 1e-13 * scale
+    x2, w2, _ = _rand(shape, 9)
+    assert relerr(oracle.conv_forward(2.5 * x - x2, w),
+                  2.5 * y - oracle.conv_forward(x2, w)) < 1e-13
+    assert relerr(oracle.conv_forward(x, w + 3 * w2),
+                  y + 3 * oracle.conv_forward(x, w2)) < 1e-13
+
+
+def test_finite_differences_of_bilinear_loss():
+    # L(x, w) = <fwd(x, w), g> is linear in each argument, so a central
+    # difference with a unit step is exact up to rounding.
+    shape = (2, 2, 3, 9, 4)
+    x, w, g = _rand(shape, 10)
+    N, n = shape[3], shape[4]
+    loss = lambda xx, ww: np.vdot(oracle.conv_forward(xx, ww), g)  # noqa: E731
+    dx = oracle.conv_backward_data(g, w, N)
+    dw = oracle.conv_backward_filter(x, g, n)
+    rng = np.random.default_rng(11)
+    for _ in range(12):
+        idx = tuple(int(rng.integers(0, s)) for s in x.shape)
+        e = np.zeros_like(x)
+        e[idx] = 1.0
+        fd = (loss(x + e, w) - loss(x - e, w)) / 2
+        assert abs(fd - dx[idx]) < 1e-12 * max(1.0, abs(dx[idx]))
+        idw = tuple(int(rng.integers(0, s)) for s in w.shape)
+        e = np.zeros_like(w)
+        e[idw] = 1.0
+        fd = (loss(x, w + e) - loss(x, w - e)) / 2
+        assert abs(fd - dw[idw]) < 1e-12 * max(1.0, abs(dw[idw]))
+
+
+def test_sampled_elements_match_whole_arrays():
+    shape = (2, 3, 4, 12, 5)
+    x, w, g = _rand(shape, 12)
+    B, C, K, N, n = shape
+    M = N - n + 1
+    y = oracle.conv_forward(x, w)
+    dx = oracle.conv_backward_data(g, w, N)
+    dw = oracle.conv_backward_filter(x, g, n)
+    rng = np.random.default_rng(13)
+    i = [rng.integers(0, s, 20) for s in (B, K, M, M)]
+    np.testing.assert_allclose(oracle.conv_forward_at(x, w, *i), y[tuple(i)], rtol=1e-13, atol=1e-13)
+    i = [rng.integers(0, s, 20) for s in (B, C, N, N)]
+    np.testing.assert_allclose(oracle.conv_backward_data_at(g, w, N, *i), dx[tuple(i)], rtol=1e-13, atol=1e-13)
+    i = [rng.integers(0, s, 20) for s in (K, C, n, n)]
+    np.testing.assert_allclose(oracle.conv_backward_filter_at(x, g, n, *i), dw[tuple(i)], rtol=1e-13, atol=1e-13)
+
+
+# ---- the step-by-step OaA oracle (Section 2) against the pinned definition --
+
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("Lmode", ["pow2", "2n-1", "big"])
+def test_oaa_steps_equal_direct_definition(shape, Lmode):
+    x, w, g = _rand(shape, 14)
+    N, n = shape[3], shape[4]
+    L = {"pow2": oaa.fft_size(n), "2n-1": max(2 * n - 1, 1), "big": oaa.fft_size(n) * 2}[Lmode]
+    if L < 2:
+        L = 2
+    assert relerr(oaa.forward(x, w, L), oracle.conv_forward(x, w)) < 1e-12
+    assert relerr(oaa.backward_data(g, w, N, L), oracle.conv_backward_data(g, w, N)) < 1e-12
+    assert relerr(oaa.backward_filter(x, g, n, L), oracle.conv_backward_filter(x, g, n)) < 1e-12
+
+
+def test_oaa_fft_size_and_block_grid():
+    assert [oaa.fft_size(n) for n in (1, 2, 3, 5, 7, 8, 9, 16, 17, 32)] == \
+        [2, 4, 8, 16, 16, 16, 32, 32, 64, 64]
+    assert [oaa.block_grid(N, n) for N, n in ((32, 5), (224, 3), (224, 7), (56, 3), (128, 16))] == \
+        [7, 75, 32, 19, 8]
+    # every power-of-two size satisfies L >= 2n, so a block fills at most half a tile
+    assert all(oaa.fft_size(n) >= 2 * n for n in range(1, 33))
+
+
+def test_oaa_spectra_are_explicit_dft_sums():
+    rng = np.random.default_rng(15)
+    x = rng.uniform(-1, 1, (1, 1, 6, 6))
+    n, L = 3, 8
+    Xh = oaa.block_spectra(x, n, L)            # [1,1,2,2,L,L/2+1]
+    P, Q = 1, 0
+    blk = x[0, 0, P * n:P * n + n, Q * n:Q * n + n]
+    for u in range(L):
+        for v in range(L // 2 + 1):
+            ref = sum(blk[r, s] * np.exp(-2j * np.pi * (u * r + v * s) / L)
+                      for r in range(n) for s in range(n))
+            assert abs(Xh[0, 0, P, Q, u, v] - ref) < 1e-12

@@ -1,0 +1,256 @@
+"""Benchmark of the OaA FFT convolution layer on one MI355X.
+
+One step = one training step of one layer through the C ABI: forward (kernel
+spectra, input block spectra, per-bin contraction over C, inverse transform +
+overlap-add + crop), backward-data (gradient window spectra, contraction over
+K with the kernel spectra of the same step, inverse + block crop) and
+backward-filter (contraction over the batch and all blocks with the block and
+window spectra of the same step, inverse + crop). Inputs are seeded synthetic
+arrays already resident in HBM when the timed region starts.
+
+Prints ONE JSON line. value = direct-convolution-equivalent TFLOP/s of the
+whole step, 3 * 2*B*K*C*M^2*n^2 / (ms per step). A "roofline" object gives
+the dominant kernel's achieved rate from HIP events recorded around each of
+its launches inside the timed region, and "cpu_baseline" the fp64 oracle
+timed on a bounded sample of the same layer on the host cores.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def stage_work(ly, geo):
+    """Algorithmic bytes (HBM) and flops per launch of each stage."""
+    B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
+    F, P, S = geo["F"], geo["P"], geo["split"]
+    BP = B * P
+    cplx = 8
+    prod_flops = 8.0 * BP * C * K * F
+    return {
+        "w_spectrum": dict(bytes=K * C * n * n * 4 + F * C * K * cplx),
+        "x_spectrum": dict(bytes=B * C * N * N * 4 + F * C * BP * cplx),
+        "g_spectrum": dict(bytes=B * K * M * M * 4 + F * K * BP * cplx),
+        "fwd_product": dict(flops=prod_flops, bytes=(F * C * K + F * C * BP + F * K * BP) * cplx),
+        "fwd_inverse": dict(bytes=F * K * BP * cplx + B * K * M * M * 4),
+        "bwd_data_product": dict(flops=prod_flops, bytes=(F * C * K + F * K * BP + F * C * BP) * cplx),
+        "bwd_data_inverse": dict(bytes=F * C * BP * cplx + B * C * N * N * 4),
+        "bwd_filter_product": dict(flops=prod_flops, bytes=(F * C * BP + F * K * BP + S * F * C * K) * cplx),
+        "bwd_filter_inverse": dict(bytes=S * F * C * K * cplx + K * C * n * n * 4),
+    }
+
+
+KERNEL_SOURCE = {
+    "w_spectrum": "k_tile_fft.hip", "x_spectrum": "k_tile_fft.hip", "g_spectrum": "k_tile_fft.hip",
+    "fwd_inverse": "k_tile_fft.hip", "bwd_data_inverse": "k_tile_fft.hip", "bwd_filter_inverse": "k_tile_fft.hip",
+    "fwd_product": "k_cgemm.hip", "bwd_data_product": "k_cgemm.hip", "bwd_filter_product": "k_cgemm.hip",
+}
+
+
+def source_digest(fname):
+    path = os.path.join(ROOT, "paper_1601_06815_amd", "csrc", fname)
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload, stage):
+    """HBM bytes per launch from committed rocprofv3 counter runs, or None if
+    absent or taken on a different version of the kernel's source."""
+    path = os.path.join(PROFILE_DIR, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(f"{workload}/{stage}")
+    except (ValueError, OSError):
+        return None
+    if not rec or rec.get("source_sha256") != source_digest(KERNEL_SOURCE[stage]):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(ly, x, w, g, budget_s=20.0):
+    """The fp64 oracle on the host on a sample of whole images (all channels,
+    all kernels, all three passes), grown until about budget_s of work."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    b, spent, flops = 0, 0.0, 0.0
+    per_img = 3 * ly.direct_flops() / ly.B
+    while b < ly.B and spent < budget_s:
+        xs, gs = np.asarray(x[b:b + 1], np.float64), np.asarray(g[b:b + 1], np.float64)
+        t0 = time.perf_counter()
+        oracle.conv_forward(xs, w)
+        oracle.conv_backward_data(gs, w, ly.N)
+        oracle.conv_backward_filter(xs, gs, ly.n)
+        spent += time.perf_counter() - t0
+        flops += per_img
+        b += 1
+        if spent * (ly.B / b) < budget_s * 0.5 and b == ly.B:
+            break
+    return {"value": flops / spent / 1e12, "unit": "TFLOP/s (direct-conv equivalent, fp64)",
+            "cores": int(cores), "kind": "oracle",
+            "sample": f"{b} of {ly.B} images, all {ly.C} channels and {ly.K} kernels, forward + "
+                      f"backward_data + backward_filter, {spent:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--layer", default="large128")
+    ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--stages-out", default=None, help="also write per-stage timings as JSON here")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (for counter calibration) and exit")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the layer would shard along the batch, with one all-reduce of dw).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1601_06815_amd import binding
+    from paper_1601_06815_amd.workloads import LAYERS, make_inputs
+
+    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            torch.mul(a, 1.0, out=b)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_each_way": n * 4, "launches": 5}))
+        return
+
+    ly = LAYERS[args.layer]
+    t0 = time.perf_counter()
+    x, w, g = make_inputs(ly, seed=0)
+    print(f"[bench] inputs for {ly.name} drawn in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+    which = {"auto": binding.CONTRACTION_AUTO, "valu": binding.CONTRACTION_VALU,
+             "mfma": binding.CONTRACTION_MFMA}[args.contraction]
+    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which)
+    geo = plan.geometry
+    xd, wd, gd = (torch.from_numpy(a).to(dev) for a in (x, w, g))
+    y = torch.empty((ly.B, ly.K, ly.M, ly.M), dtype=torch.float32, device=dev)
+    dx = torch.empty_like(xd)
+    dw = torch.empty_like(wd)
+
+    def step():
+        plan.forward(xd, wd, y)
+        plan.backward_data(gd, None, dx)
+        plan.backward_filter(None, None, dw)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    plan.set_timing(True)
+    plan.stage_times()  # clear
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    stages = plan.stage_times()
+    plan.set_timing(False)
+    ms_step = ms_total / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    direct = 3 * ly.direct_flops()
+    value = direct / (ms_step * 1e-3) / 1e12
+    work = stage_work(ly, geo)
+    per_stage = {}
+    for name, (ms, cnt) in stages.items():
+        if cnt:
+            per_stage[name] = {"ms_per_launch": ms / cnt, "launches": cnt}
+    dom = max(per_stage, key=lambda k: per_stage[k]["ms_per_launch"] * per_stage[k]["launches"])
+    avg_s = per_stage[dom]["ms_per_launch"] * 1e-3
+    wk = work[dom]
+    if "flops" in wk:
+        achieved = wk["flops"] / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / FP32_MFMA_PEAK_TFLOPS}
+    else:
+        achieved = wk["bytes"] / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    roof["traffic"] = measured_traffic(ly.name, dom)
+    roof["kernel"] = dom
+    roof["ms_per_launch"] = per_stage[dom]["ms_per_launch"]
+    for name, st in per_stage.items():
+        wk = work[name]
+        s = st["ms_per_launch"] * 1e-3
+        st["gbs_algorithmic"] = wk["bytes"] / s / 1e9
+        if "flops" in wk:
+            st["tflops"] = wk["flops"] / s / 1e12
+
+    # sampled parity of the timed outputs against the oracle
+    import oracle
+    rng = np.random.default_rng(0)
+    iy = [rng.integers(0, s, 16) for s in (ly.B, ly.K, ly.M, ly.M)]
+    iw = [rng.integers(0, s, 16) for s in (ly.K, ly.C, ly.n, ly.n)]
+    yh, dwh = y.cpu().numpy(), dw.cpu().numpy()
+    ry = oracle.conv_forward_at(x, w, *iy)
+    rw = oracle.conv_backward_filter_at(x, g, ly.n, *iw)
+    err = max(float(np.max(np.abs(yh[tuple(iy)] - ry)) / np.max(np.abs(ry))),
+              float(np.max(np.abs(dwh[tuple(iw)] - rw)) / np.max(np.abs(rw))))
+
+    out = {
+        "metric": "OaA conv fwd+bwd direct-equivalent TFLOP/s",
+        "value": value,
+        "unit": "TFLOP/s (direct-conv equivalent)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded numpy draws, resident in HBM)",
+        "config": {"workload": f"{ly.name}: x[{ly.B},{ly.C},{ly.N},{ly.N}] w[{ly.K},{ly.C},{ly.n},{ly.n}] "
+                               f"valid stride 1, forward + backward_data + backward_filter",
+                   "B": ly.B, "C": ly.C, "K": ly.K, "N": ly.N, "n": ly.n,
+                   "L": geo["L"], "T": geo["T"], "split": geo["split"],
+                   "contraction": args.contraction},
+        "roofline": roof,
+        "stages": per_stage,
+        "sampled_rel_err": err,
+    }
+    if args.stages_out:
+        with open(args.stages_out, "w") as f:
+            json.dump(per_stage, f, indent=1)
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(ly, x, w, g, args.cpu_budget)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

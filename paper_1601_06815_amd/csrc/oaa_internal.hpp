@@ -1,0 +1,81 @@
+// Kernel parameter blocks and launchers shared by the host plan code and the
+// HIP kernels. Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+
+namespace oaa {
+
+// Spectrum layout used by every kernel: complex64 [F][n_ch][n_img * P],
+// bin f = u * (L/2+1) + v, tile index within an image = P_row * T + Q_col.
+
+// Zero-padded windows of a stack of square planes -> spectra.
+// Window (P, Q) of plane (img, ch) has element (r, s), r, s < R, equal to
+// plane[P*pitch + r - off][Q*pitch + s - off] (0 outside the plane); it is
+// placed at [0,R)^2 of an L x L tile and transformed.
+struct TileFwdParams {
+  const float* src;  // [n_img][n_ch][H][H]
+  float2* dst;       // [F][n_ch][n_img * T * T]
+  int n_img, n_ch;
+  int H;             // plane side
+  int pitch;         // block pitch (the kernel side n)
+  int off;           // window origin offset in the padded frame
+  int R;             // window side
+  int T;             // blocks per side
+  int TQ;            // tiles per workgroup chunk along a block row
+  int nchunk;        // ceil(T / TQ)
+};
+
+// Output spectra -> inverse transform -> overlap-add (pitch n, tile support
+// 2n-1) -> valid crop of side M into dst[n_img][n_ch][M][M].
+struct OverlapAddParams {
+  const float2* src;  // [F][n_ch][n_img * T * T]
+  float* dst;         // [n_img][n_ch][M][M]
+  int n_img, n_ch;
+  int M, n, T;
+  int TQ, nchunk;     // tiles per column-pass chunk
+  int SPW, ngroups;   // block rows per workgroup, ceil(T / SPW)
+};
+
+// Spectra (optionally the sum of `nsplit` partial spectra spaced
+// `split_stride` elements apart) -> inverse transform -> top-left n x n of
+// each tile written to block (P, Q) of dst[n_img][n_ch][H][H], clipped to H.
+struct CropParams {
+  const float2* src;  // [nsplit][F][n_ch][n_img * T * T]
+  int nsplit;
+  size_t split_stride;
+  float* dst;         // [n_img][n_ch][H][H]
+  int n_img, n_ch;
+  int H, n, T;
+  int TQ, nchunk;
+};
+
+// Batched complex matrix product, one problem per frequency bin f:
+//   Cmat[f] (M x N) = op(A[f]) (M x Kr) * op(B[f]) (Kr x N)
+// A element (m, kk) is at A + f*a_fstride + (a_trans ? kk*lda + m : m*lda + kk),
+// conjugated when a_conj; likewise B element (kk, n) at
+// B + f*b_fstride + (b_trans ? n*ldb + kk : kk*ldb + n). With nsplit > 1 the
+// reduction is split into ranges of kchunk and split s writes its partial
+// product to Cmat + s*c_sstride.
+struct GemmParams {
+  const float2* A;
+  const float2* B;
+  float2* C;
+  int M, N, Kr;
+  long lda, ldb, ldc;
+  size_t a_fstride, b_fstride, c_fstride;
+  int nsplit, kchunk;
+  size_t c_sstride;
+  int F;
+  bool a_trans, a_conj, b_trans, b_conj;
+};
+
+hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
+hipError_t launch_irfft2_overlap_add(int L, const OverlapAddParams& p, hipStream_t s);
+hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
+hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s);
+hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s);
+
+}  // namespace oaa

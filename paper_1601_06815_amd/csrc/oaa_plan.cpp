@@ -1,0 +1,446 @@
+// Host side of the C ABI declared in include/oaa.h: plan geometry, argument
+// validation, workspace layout, and the order of kernel launches for each
+// pass of the overlap-and-add convolution (arXiv:1601.06815, Section 2 for
+// the forward pass, Section 3.2 for the two backward convolutions).
+#include "oaa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "oaa_internal.hpp"
+
+struct oaa_plan_s {
+  int B, C, K, N, n;
+  int M, T, P, L, F;
+  int split, kchunk;
+  size_t off[4];
+  size_t size[4];
+  size_t ws_bytes;
+  char* ws;
+  size_t ws_bound;
+  bool w_valid, x_valid, g_valid;
+  oaa_contraction_t contraction;
+  // per-stage timing: event pairs recorded around launches
+  bool timing;
+  std::vector<hipEvent_t> event_pool;
+  struct Rec {
+    int stage;
+    hipEvent_t start, stop;
+  };
+  std::vector<Rec> records;
+};
+
+namespace {
+
+thread_local std::string g_detail;
+
+oaa_status_t fail(oaa_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+oaa_status_t fail(oaa_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_detail = buf;
+  return st;
+}
+
+constexpr size_t kAlign = 256;
+constexpr unsigned long long kMaxElems = 1ull << 60;
+constexpr long long kMaxInt = 0x7fffffffll;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int pow2_at_least(int v) {
+  int L = 2;
+  while (L < v) L *= 2;
+  return L;
+}
+
+oaa_status_t check_plan(oaa_plan_t plan, bool need_ws) {
+  if (!plan) return fail(OAA_ERR_INVALID_ARG, "plan is NULL");
+  if (need_ws && !plan->ws)
+    return fail(OAA_ERR_NO_WORKSPACE, "no workspace bound (need %zu bytes)", plan->ws_bytes);
+  return OAA_OK;
+}
+
+oaa_status_t hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return OAA_OK;
+  return fail(OAA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+float2* region(oaa_plan_t p, int r) { return reinterpret_cast<float2*>(p->ws + p->off[r]); }
+
+hipError_t take_event(oaa_plan_t p, hipEvent_t* ev) {
+  if (!p->event_pool.empty()) {
+    *ev = p->event_pool.back();
+    p->event_pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(ev);
+}
+
+// Run one launch; when timing is on, bracket it with events on stream s.
+template <class Fn>
+oaa_status_t timed(oaa_plan_t p, oaa_stage_t stage, hipStream_t s, const char* what, Fn&& launch) {
+  if (!p->timing) return hip_status(launch(), what);
+  hipEvent_t a = nullptr, b = nullptr;
+  hipError_t e = take_event(p, &a);
+  if (e == hipSuccess) e = take_event(p, &b);
+  if (e == hipSuccess) e = hipEventRecord(a, s);
+  if (e != hipSuccess) {
+    if (a) p->event_pool.push_back(a);
+    if (b) p->event_pool.push_back(b);
+    return hip_status(e, "timing event");
+  }
+  e = launch();
+  if (e == hipSuccess) e = hipEventRecord(b, s);
+  if (e != hipSuccess) {
+    p->event_pool.push_back(a);
+    p->event_pool.push_back(b);
+    return hip_status(e, what);
+  }
+  p->records.push_back({int(stage), a, b});
+  return OAA_OK;
+}
+
+oaa_status_t run_filter_fft(oaa_plan_t p, const float* w, hipStream_t s) {
+  oaa::TileFwdParams t{};
+  t.src = w;
+  t.dst = region(p, OAA_REGION_W_SPECTRUM);
+  t.n_img = p->K;   // w[k][c] plane; spectra [F][C][K]
+  t.n_ch = p->C;
+  t.H = p->n;
+  t.pitch = p->n;
+  t.off = 0;
+  t.R = p->n;
+  t.T = 1;
+  oaa_status_t st = timed(p, OAA_STAGE_W_SPECTRUM, s, "kernel spectra",
+                          [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+  if (st == OAA_OK) p->w_valid = true;
+  return st;
+}
+
+oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
+  oaa::TileFwdParams t{};
+  t.src = x;
+  t.dst = region(p, OAA_REGION_X_SPECTRUM);
+  t.n_img = p->B;
+  t.n_ch = p->C;
+  t.H = p->N;
+  t.pitch = p->n;
+  t.off = 0;
+  t.R = p->n;
+  t.T = p->T;
+  oaa_status_t st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
+                          [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+  if (st == OAA_OK) p->x_valid = true;
+  return st;
+}
+
+oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
+  // window (P,Q) of the zero-framed gradient: g[P*n + r - (n-1)][Q*n + s - (n-1)]
+  oaa::TileFwdParams t{};
+  t.src = g;
+  t.dst = region(p, OAA_REGION_G_SPECTRUM);
+  t.n_img = p->B;
+  t.n_ch = p->K;
+  t.H = p->M;
+  t.pitch = p->n;
+  t.off = p->n - 1;
+  t.R = 2 * p->n - 1;
+  t.T = p->T;
+  oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient window spectra",
+                          [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+  if (st == OAA_OK) p->g_valid = true;
+  return st;
+}
+
+oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipStream_t s, const char* what) {
+  g.F = p->F;
+  return timed(p, stage, s, what, [&] {
+    return p->contraction == OAA_CONTRACTION_MFMA ? oaa::launch_cgemm_mfma(g, s) : oaa::launch_cgemm_valu(g, s);
+  });
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* oaa_status_string(oaa_status_t status) {
+  switch (status) {
+    case OAA_OK: return "OAA_OK";
+    case OAA_ERR_INVALID_ARG: return "OAA_ERR_INVALID_ARG";
+    case OAA_ERR_UNSUPPORTED: return "OAA_ERR_UNSUPPORTED";
+    case OAA_ERR_NO_WORKSPACE: return "OAA_ERR_NO_WORKSPACE";
+    case OAA_ERR_NO_CACHE: return "OAA_ERR_NO_CACHE";
+    case OAA_ERR_HIP: return "OAA_ERR_HIP";
+  }
+  return "OAA_ERR_UNKNOWN";
+}
+
+const char* oaa_last_error_detail(void) { return g_detail.c_str(); }
+
+oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n) {
+  if (!out) return fail(OAA_ERR_INVALID_ARG, "plan output pointer is NULL");
+  *out = nullptr;
+  if (B < 1 || C < 1 || K < 1 || N < 1 || n < 1)
+    return fail(OAA_ERR_INVALID_ARG, "dimensions must be positive (B=%d C=%d K=%d N=%d n=%d)", B, C, K, N, n);
+  if (n > N) return fail(OAA_ERR_INVALID_ARG, "kernel side n=%d exceeds input side N=%d", n, N);
+  if (n > 32) return fail(OAA_ERR_UNSUPPORTED, "kernel side n=%d > 32 (transform side would exceed 64)", n);
+
+  const int M = N - n + 1;
+  const int T = (N + n - 1) / n;
+  const long long P = (long long)T * T;
+  const int L = pow2_at_least(2 * n - 1);
+  const int F = L * (L / 2 + 1);
+  const long long BP = (long long)B * P;
+  // index ranges the kernels keep in 32-bit integers
+  if (BP > kMaxInt || (long long)N * N > kMaxInt || (long long)B * C > kMaxInt || (long long)B * K > kMaxInt ||
+      (long long)K * C > kMaxInt)
+    return fail(OAA_ERR_UNSUPPORTED, "layer too large for 32-bit tile and plane indices");
+  // the overlap-add keeps one block row of output (2n-1 rows) in LDS
+  {
+    const long long acc = (long long)(2 * n - 1) * ((long long)T * n + n - 1) * 4;
+    const long long tile = (long long)(2 * n - 1) * (L / 2 + 1) * 8;
+    if (acc + tile > 160 * 1024)
+      return fail(OAA_ERR_UNSUPPORTED, "one block row of output (%lld bytes) exceeds the 160 KiB LDS", acc + tile);
+  }
+  const unsigned long long eW = (unsigned long long)F * C * K;
+  const unsigned long long eX = (unsigned long long)F * C * BP;
+  const unsigned long long eG = (unsigned long long)F * K * BP;
+  if (eX > kMaxElems || eG > kMaxElems || eW > kMaxElems)
+    return fail(OAA_ERR_UNSUPPORTED, "spectra exceed the addressable workspace");
+
+  // split of the weight-gradient reduction over B*P so that the contraction
+  // has enough workgroups to fill the device
+  const long long tiles = (long long)((C + 63) / 64) * ((K + 63) / 64) * F;
+  long long split = tiles >= 2048 ? 1 : (2048 + tiles - 1) / tiles;
+  const long long max_split = (BP + 63) / 64;
+  if (split > max_split) split = max_split;
+  if (split < 1) split = 1;
+  long long kchunk = (BP + split - 1) / split;
+  kchunk = (kchunk + 15) / 16 * 16;
+  split = (BP + kchunk - 1) / kchunk;
+
+  oaa_plan_s* p = new (std::nothrow) oaa_plan_s();
+  if (!p) return fail(OAA_ERR_INVALID_ARG, "out of host memory");
+  p->B = B; p->C = C; p->K = K; p->N = N; p->n = n;
+  p->M = M; p->T = T; p->P = (int)P; p->L = L; p->F = F;
+  p->split = (int)split;
+  p->kchunk = (int)kchunk;
+  unsigned long long eProd = eG > eX ? eG : eX;
+  if ((unsigned long long)split * eW > eProd) eProd = (unsigned long long)split * eW;
+  p->size[OAA_REGION_W_SPECTRUM] = size_t(eW) * 8;
+  p->size[OAA_REGION_X_SPECTRUM] = size_t(eX) * 8;
+  p->size[OAA_REGION_G_SPECTRUM] = size_t(eG) * 8;
+  p->size[OAA_REGION_PRODUCT] = size_t(eProd) * 8;
+  size_t off = 0;
+  for (int r = 0; r < 4; ++r) {
+    p->off[r] = off;
+    off = align_up(off + p->size[r]);
+  }
+  p->ws_bytes = off;
+  p->ws = nullptr;
+  p->ws_bound = 0;
+  p->w_valid = p->x_valid = p->g_valid = false;
+  p->contraction = OAA_CONTRACTION_AUTO;
+  p->timing = false;
+  *out = p;
+  return OAA_OK;
+}
+
+oaa_status_t oaa_plan_destroy(oaa_plan_t plan) {
+  if (!plan) return OAA_OK;
+  for (auto& r : plan->records) {
+    (void)hipEventSynchronize(r.stop);
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  for (hipEvent_t e : plan->event_pool) (void)hipEventDestroy(e);
+  delete plan;
+  return OAA_OK;
+}
+
+oaa_status_t oaa_plan_set_timing(oaa_plan_t plan, int enable) {
+  if (oaa_status_t st = check_plan(plan, false)) return st;
+  plan->timing = enable != 0;
+  return OAA_OK;
+}
+
+oaa_status_t oaa_plan_stage_times(oaa_plan_t plan, double* total_ms, int* launches, int count) {
+  if (oaa_status_t st = check_plan(plan, false)) return st;
+  if (count < 0) return fail(OAA_ERR_INVALID_ARG, "negative count");
+  for (int i = 0; i < count; ++i) {
+    if (total_ms) total_ms[i] = 0.0;
+    if (launches) launches[i] = 0;
+  }
+  oaa_status_t result = OAA_OK;
+  for (auto& r : plan->records) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess && result == OAA_OK) result = hip_status(e, "timing event");
+    if (e == hipSuccess && r.stage < count) {
+      if (total_ms) total_ms[r.stage] += ms;
+      if (launches) launches[r.stage] += 1;
+    }
+    plan->event_pool.push_back(r.start);
+    plan->event_pool.push_back(r.stop);
+  }
+  plan->records.clear();
+  return result;
+}
+
+oaa_status_t oaa_plan_geometry(oaa_plan_t plan, oaa_geometry_t* out) {
+  if (oaa_status_t st = check_plan(plan, false)) return st;
+  if (!out) return fail(OAA_ERR_INVALID_ARG, "geometry output pointer is NULL");
+  out->B = plan->B; out->C = plan->C; out->K = plan->K; out->N = plan->N; out->n = plan->n;
+  out->M = plan->M; out->T = plan->T; out->P = plan->P; out->L = plan->L; out->F = plan->F;
+  out->split = plan->split;
+  return OAA_OK;
+}
+
+size_t oaa_plan_workspace_bytes(oaa_plan_t plan) { return plan ? plan->ws_bytes : 0; }
+
+oaa_status_t oaa_plan_region(oaa_plan_t plan, oaa_region_t r, size_t* offset, size_t* bytes) {
+  if (oaa_status_t st = check_plan(plan, false)) return st;
+  if ((int)r < 0 || (int)r > 3) return fail(OAA_ERR_INVALID_ARG, "unknown region %d", (int)r);
+  if (offset) *offset = plan->off[r];
+  if (bytes) *bytes = plan->size[r];
+  return OAA_OK;
+}
+
+oaa_status_t oaa_plan_bind_workspace(oaa_plan_t plan, void* dev_ptr, size_t bytes) {
+  if (oaa_status_t st = check_plan(plan, false)) return st;
+  plan->w_valid = plan->x_valid = plan->g_valid = false;
+  plan->ws = nullptr;
+  plan->ws_bound = 0;
+  if (!dev_ptr) return fail(OAA_ERR_INVALID_ARG, "workspace pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(dev_ptr) % kAlign)
+    return fail(OAA_ERR_INVALID_ARG, "workspace pointer is not %zu-byte aligned", kAlign);
+  if (bytes < plan->ws_bytes)
+    return fail(OAA_ERR_NO_WORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", bytes, plan->ws_bytes);
+  plan->ws = static_cast<char*>(dev_ptr);
+  plan->ws_bound = bytes;
+  return OAA_OK;
+}
+
+oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which) {
+  if (oaa_status_t st = check_plan(plan, false)) return st;
+  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA)
+    return fail(OAA_ERR_INVALID_ARG, "unknown contraction %d", (int)which);
+  plan->contraction = which;
+  return OAA_OK;
+}
+
+oaa_status_t oaa_conv_forward(oaa_plan_t p, const float* x, const float* w, float* y, void* stream) {
+  if (oaa_status_t st = check_plan(p, true)) return st;
+  if (!x || !y) return fail(OAA_ERR_INVALID_ARG, "x and y must be non-NULL");
+  if (!w && !p->w_valid) return fail(OAA_ERR_NO_CACHE, "w is NULL and no kernel spectra are cached");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  oaa_status_t st;
+  if (w && (st = run_filter_fft(p, w, s))) return st;
+  if ((st = run_input_fft(p, x, s))) return st;
+  // Yhat[f] (K x BP) = What[f]^T (K x C) * Xhat[f] (C x BP)
+  const long BP = (long)p->B * p->P;
+  oaa::GemmParams g{};
+  g.A = region(p, OAA_REGION_W_SPECTRUM);
+  g.B = region(p, OAA_REGION_X_SPECTRUM);
+  g.C = region(p, OAA_REGION_PRODUCT);
+  g.M = p->K; g.N = (int)BP; g.Kr = p->C;
+  g.lda = p->K; g.ldb = BP; g.ldc = BP;
+  g.a_fstride = (size_t)p->C * p->K;
+  g.b_fstride = (size_t)p->C * BP;
+  g.c_fstride = (size_t)p->K * BP;
+  g.nsplit = 1; g.kchunk = p->C; g.c_sstride = 0;
+  g.a_trans = true; g.a_conj = false; g.b_trans = false; g.b_conj = false;
+  if ((st = run_gemm(p, g, OAA_STAGE_FWD_PRODUCT, s, "forward contraction"))) return st;
+  oaa::OverlapAddParams o{};
+  o.src = region(p, OAA_REGION_PRODUCT);
+  o.dst = y;
+  o.n_img = p->B; o.n_ch = p->K;
+  o.M = p->M; o.n = p->n; o.T = p->T;
+  return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
+               [&] { return oaa::launch_irfft2_overlap_add(p->L, o, s); });
+}
+
+oaa_status_t oaa_conv_backward_data(oaa_plan_t p, const float* g, const float* w, float* dx, void* stream) {
+  if (oaa_status_t st = check_plan(p, true)) return st;
+  if (!g || !dx) return fail(OAA_ERR_INVALID_ARG, "g and dx must be non-NULL");
+  if (!w && !p->w_valid) return fail(OAA_ERR_NO_CACHE, "w is NULL and no kernel spectra are cached");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  oaa_status_t st;
+  if (w && (st = run_filter_fft(p, w, s))) return st;
+  if ((st = run_grad_fft(p, g, s))) return st;
+  // dXhat[f] (C x BP) = conj(What[f]) (C x K) * Ghat[f] (K x BP)
+  const long BP = (long)p->B * p->P;
+  oaa::GemmParams gm{};
+  gm.A = region(p, OAA_REGION_W_SPECTRUM);
+  gm.B = region(p, OAA_REGION_G_SPECTRUM);
+  gm.C = region(p, OAA_REGION_PRODUCT);
+  gm.M = p->C; gm.N = (int)BP; gm.Kr = p->K;
+  gm.lda = p->K; gm.ldb = BP; gm.ldc = BP;
+  gm.a_fstride = (size_t)p->C * p->K;
+  gm.b_fstride = (size_t)p->K * BP;
+  gm.c_fstride = (size_t)p->C * BP;
+  gm.nsplit = 1; gm.kchunk = p->K; gm.c_sstride = 0;
+  gm.a_trans = false; gm.a_conj = true; gm.b_trans = false; gm.b_conj = false;
+  if ((st = run_gemm(p, gm, OAA_STAGE_BWD_DATA_PRODUCT, s, "backward-data contraction"))) return st;
+  oaa::CropParams c{};
+  c.src = region(p, OAA_REGION_PRODUCT);
+  c.nsplit = 1; c.split_stride = 0;
+  c.dst = dx;
+  c.n_img = p->B; c.n_ch = p->C;
+  c.H = p->N; c.n = p->n; c.T = p->T;
+  return timed(p, OAA_STAGE_BWD_DATA_INVERSE, s, "inverse transform + block crop",
+               [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+}
+
+oaa_status_t oaa_conv_backward_filter(oaa_plan_t p, const float* x, const float* g, float* dw, void* stream) {
+  if (oaa_status_t st = check_plan(p, true)) return st;
+  if (!dw) return fail(OAA_ERR_INVALID_ARG, "dw must be non-NULL");
+  if (!x && !p->x_valid) return fail(OAA_ERR_NO_CACHE, "x is NULL and no input block spectra are cached");
+  if (!g && !p->g_valid) return fail(OAA_ERR_NO_CACHE, "g is NULL and no gradient window spectra are cached");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  oaa_status_t st;
+  if (x && (st = run_input_fft(p, x, s))) return st;
+  if (g && (st = run_grad_fft(p, g, s))) return st;
+  // dWhat^T[f] (C x K) = conj(Xhat[f]) (C x BP) * Ghat[f]^T (BP x K), split over BP
+  const long BP = (long)p->B * p->P;
+  oaa::GemmParams gm{};
+  gm.A = region(p, OAA_REGION_X_SPECTRUM);
+  gm.B = region(p, OAA_REGION_G_SPECTRUM);
+  gm.C = region(p, OAA_REGION_PRODUCT);
+  gm.M = p->C; gm.N = p->K; gm.Kr = (int)BP;
+  gm.lda = BP; gm.ldb = BP; gm.ldc = p->K;
+  gm.a_fstride = (size_t)p->C * BP;
+  gm.b_fstride = (size_t)p->K * BP;
+  gm.c_fstride = (size_t)p->C * p->K;
+  gm.nsplit = p->split; gm.kchunk = p->kchunk;
+  gm.c_sstride = (size_t)p->F * p->C * p->K;
+  gm.a_trans = false; gm.a_conj = true; gm.b_trans = true; gm.b_conj = false;
+  if ((st = run_gemm(p, gm, OAA_STAGE_BWD_FILTER_PRODUCT, s, "backward-filter contraction"))) return st;
+  oaa::CropParams c{};
+  c.src = region(p, OAA_REGION_PRODUCT);
+  c.nsplit = p->split;
+  c.split_stride = (size_t)p->F * p->C * p->K;
+  c.dst = dw;
+  c.n_img = p->K; c.n_ch = p->C;   // spectra [F][C][K], output planes dw[k][c]
+  c.H = p->n; c.n = p->n; c.T = 1;
+  return timed(p, OAA_STAGE_BWD_FILTER_INVERSE, s, "inverse transform of weight gradient",
+               [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+}
+
+}  // extern "C"

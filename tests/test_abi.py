@@ -1,0 +1,172 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library is loaded (it is built first if absent), every function that
+include/oaa.h declares must be exported, and plan creation, geometry,
+workspace layout and argument validation are exercised. Only calls that fail
+validation before any launch are made here, so no device is touched.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1601_06815_amd import binding, build
+from paper_1601_06815_amd.workloads import LAYERS
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "oaa.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(build.LIB_PATH):
+        build.build()
+    return binding.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(oaa_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in oaa.h but not exported"
+    assert set(names) == set(binding.SIGNATURES), "binding and header disagree"
+
+
+def test_status_strings(lib):
+    for code, name in binding.STATUS.items():
+        assert binding.oaa_status_string(code) == name
+    assert binding.oaa_status_string(99) == "OAA_ERR_UNKNOWN"
+
+
+@pytest.mark.parametrize("name,expect", [
+    ("tiny", dict(M=28, T=7, P=49, L=16, F=144)),
+    ("plane224_n3", dict(M=222, T=75, P=5625, L=8, F=40)),
+    ("plane224_n5", dict(M=220, T=45, P=2025, L=16, F=144)),
+    ("plane224_n8", dict(M=217, T=28, P=784, L=16, F=144)),
+    ("first224", dict(M=218, T=32, P=1024, L=16, F=144)),
+    ("mid56", dict(M=54, T=19, P=361, L=8, F=40)),
+    ("large128", dict(M=113, T=8, P=64, L=32, F=544)),
+])
+def test_geometry_of_named_layers(lib, name, expect):
+    ly = LAYERS[name]
+    h = binding.oaa_plan_create(ly.B, ly.C, ly.K, ly.N, ly.n)
+    try:
+        g = binding.oaa_plan_geometry(h)
+        for k, v in expect.items():
+            assert g[k] == v, (k, g[k], v)
+        BP = ly.B * g["P"]
+        F = g["F"]
+        sizes = {}
+        offs = []
+        for r, elems in [(binding.REGION_W_SPECTRUM, F * ly.C * ly.K),
+                         (binding.REGION_X_SPECTRUM, F * ly.C * BP),
+                         (binding.REGION_G_SPECTRUM, F * ly.K * BP)]:
+            off, size = binding.oaa_plan_region(h, r)
+            assert size == 8 * elems and off % 256 == 0
+            sizes[r] = size
+            offs.append((off, size))
+        off, size = binding.oaa_plan_region(h, binding.REGION_PRODUCT)
+        assert size == 8 * max(F * ly.K * BP, F * ly.C * BP, g["split"] * F * ly.C * ly.K)
+        offs.append((off, size))
+        offs.sort()
+        for (o1, s1), (o2, _) in zip(offs, offs[1:]):
+            assert o1 + s1 <= o2, "regions overlap"
+        assert offs[-1][0] + offs[-1][1] <= binding.oaa_plan_workspace_bytes(h)
+        assert g["split"] >= 1
+    finally:
+        binding.oaa_plan_destroy(h)
+
+
+@pytest.mark.parametrize("dims,status", [
+    ((0, 1, 1, 8, 3), 1), ((1, 0, 1, 8, 3), 1), ((1, 1, 0, 8, 3), 1), ((1, 1, 1, 0, 1), 1),
+    ((1, 1, 1, 8, 0), 1), ((1, 1, 1, 4, 5), 1), ((1, 1, 1, 64, 33), 2), ((1, 1, 1, 64, 32), 0),
+    ((1, 1, 1, 1, 1), 0), ((1 << 20, 1, 1, 4096, 2), 2),
+])
+def test_plan_create_validation(lib, dims, status):
+    h = ctypes.c_void_p(12345)
+    st = lib.oaa_plan_create(ctypes.byref(h), *dims)
+    assert st == status, (dims, st, binding.oaa_last_error_detail())
+    if status == 0:
+        assert h.value
+        lib.oaa_plan_destroy(h)
+    else:
+        assert h.value is None
+        assert binding.oaa_last_error_detail()
+
+
+def test_null_and_workspace_validation(lib):
+    assert lib.oaa_plan_create(None, 1, 1, 1, 8, 3) == 1
+    assert lib.oaa_plan_destroy(None) == 0
+    assert lib.oaa_plan_workspace_bytes(None) == 0
+    assert lib.oaa_conv_forward(None, 256, 256, 256, None) == 1
+    h = binding.oaa_plan_create(2, 3, 4, 16, 5)
+    try:
+        fake = 1 << 40   # never dereferenced: every call below fails validation first
+        assert lib.oaa_conv_forward(h, fake, fake, fake, None) == 3        # no workspace
+        assert lib.oaa_conv_backward_data(h, fake, fake, fake, None) == 3
+        assert lib.oaa_conv_backward_filter(h, fake, fake, fake, None) == 3
+        need = binding.oaa_plan_workspace_bytes(h)
+        assert lib.oaa_plan_bind_workspace(h, fake, need - 1) == 3        # too small
+        assert lib.oaa_plan_bind_workspace(h, fake + 8, need) == 1        # misaligned
+        assert lib.oaa_plan_bind_workspace(h, None, need) == 1
+        assert lib.oaa_plan_bind_workspace(h, fake, need) == 0
+        assert lib.oaa_conv_forward(h, None, fake, fake, None) == 1       # x NULL
+        assert lib.oaa_conv_forward(h, fake, fake, None, None) == 1       # y NULL
+        assert lib.oaa_conv_forward(h, fake, None, fake, None) == 4       # no cached kernel spectra
+        assert lib.oaa_conv_backward_data(h, fake, None, fake, None) == 4
+        assert lib.oaa_conv_backward_data(h, None, fake, fake, None) == 1
+        assert lib.oaa_conv_backward_filter(h, None, fake, fake, None) == 4   # no cached block spectra
+        assert lib.oaa_conv_backward_filter(h, fake, None, fake, None) == 4   # no cached window spectra
+        assert lib.oaa_conv_backward_filter(h, fake, fake, None, None) == 1
+        assert lib.oaa_plan_set_contraction(h, 7) == 1
+        assert lib.oaa_plan_set_contraction(h, 1) == 0
+        assert lib.oaa_plan_region(h, 4, None, None) == 1
+        g = binding.Geometry()
+        assert lib.oaa_plan_geometry(h, None) == 1
+        assert lib.oaa_plan_geometry(h, ctypes.byref(g)) == 0 and g.L == 16 and g.T == 4
+    finally:
+        binding.oaa_plan_destroy(h)
+
+
+def test_binding_raises_with_detail(lib):
+    with pytest.raises(binding.OaaError) as e:
+        binding.oaa_plan_create(1, 1, 1, 8, 9)
+    assert "exceeds" in str(e.value)
+
+
+def test_twiddle_table_matches_libm(tmp_path):
+    """The compile-time twiddles (csrc/twiddle.hpp, plain C++) against the C
+    library's cos/sin in double, rounded to float."""
+    import shutil
+    import subprocess
+    import numpy as np
+    cxx = shutil.which("g++")
+    if cxx is None:
+        pytest.skip("no host C++ compiler")
+    src = tmp_path / "tw.cpp"
+    src.write_text('#include "twiddle.hpp"\n#include <cstdio>\n'
+                   'template <int L> void dump() { for (int k = 0; k < L; ++k) '
+                   'std::printf("%d %d %.9e %.9e\\n", L, k, (double)oaa::tw::kTable<L>.c[k], '
+                   '(double)oaa::tw::kTable<L>.s[k]); }\n'
+                   'int main() { dump<2>(); dump<4>(); dump<8>(); dump<16>(); dump<32>(); dump<64>(); }\n')
+    exe = tmp_path / "tw"
+    csrc = os.path.join(os.path.dirname(build.LIB_PATH), "csrc")
+    subprocess.run([cxx, "-std=c++17", "-O1", "-I", csrc, str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    worst = 0
+    for line in filter(None, out):
+        L, k, c, s = line.split()
+        L, k = int(L), int(k)
+        ang = 2 * np.pi * k / L
+        rc, rs = np.float32(np.cos(ang)), np.float32(np.sin(ang))
+        for got, ref in ((np.float32(float(c)), rc), (np.float32(float(s)), rs)):
+            ulp = np.spacing(np.float32(max(abs(ref), 1e-30)))
+            worst = max(worst, abs(float(got) - float(ref)) / float(ulp) if abs(ref) > 1e-7 else abs(float(got)) * 1e7)
+    assert worst <= 1.0

@@ -1,0 +1,210 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar: max|gpu - oracle| / max|oracle| <= 2e-5 per output tensor and pass, for
+float32 data. Whole arrays are compared wherever the oracle finishes in
+seconds; the full-size layers are compared on sampled outputs that the
+oracle evaluates one by one, in the same launch configuration bench.py times.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import oaa as oaa_oracle
+from paper_1601_06815_amd import binding
+from paper_1601_06815_amd.workloads import LAYERS, Layer, make_inputs
+from tests.conftest import relerr
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-5
+DEV = "cuda:0"
+
+SMALL = [  # (B, C, K, N, n): every transform size, ragged block rows, n = 1, N = n
+    (1, 3, 4, 32, 5),
+    (2, 2, 3, 13, 4),
+    (1, 1, 1, 9, 3),
+    (2, 3, 2, 11, 1),
+    (1, 2, 2, 7, 7),
+    (1, 1, 2, 10, 6),
+    (3, 2, 3, 17, 8),
+    (1, 1, 1, 2, 2),
+    (2, 2, 3, 40, 16),
+    (1, 2, 2, 40, 17),
+    (1, 1, 2, 33, 32),
+    (2, 70, 66, 12, 2),
+    (1, 5, 130, 20, 3),
+    (4, 9, 7, 61, 9),
+]
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO):
+    B, C, N, _ = x.shape
+    K, _, n, _ = w.shape
+    plan = binding.Plan(B, C, K, N, n, device=DEV, contraction=contraction)
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    y = plan.forward(xd, wd)
+    dx = plan.backward_data(gd, wd)
+    dw = plan.backward_filter(xd, gd)
+    torch.cuda.synchronize()
+    return plan, y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
+
+
+def check_whole(x, w, g, contraction=binding.CONTRACTION_AUTO):
+    _, y, dx, dw = run_layer(x, w, g, contraction)
+    N, n = x.shape[-1], w.shape[-1]
+    e = (relerr(y, oracle.conv_forward(x, w)),
+         relerr(dx, oracle.conv_backward_data(g, w, N)),
+         relerr(dw, oracle.conv_backward_filter(x, g, n)))
+    print(f"shape x{x.shape} w{w.shape}: rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e} bwd_filter {e[2]:.2e}",
+          flush=True)
+    assert max(e) <= TOL, e
+    return e
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+def test_small_layers_all_passes(gpu_lib, shape):
+    B, C, K, N, n = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=sum(shape))
+    check_whole(x, w, g)
+
+
+@pytest.mark.parametrize("name", ["tiny", "plane224_n3", "plane224_n5", "plane224_n8"])
+def test_named_small_layers(gpu_lib, name):
+    ly = LAYERS[name]
+    x, w, g = make_inputs(ly, seed=0)   # g is drawn for every layer; unused passes still checked
+    check_whole(x, w, g)
+
+
+@pytest.mark.parametrize("name,batch,C,K", [("first224", 2, None, None), ("mid56", 2, None, None),
+                                            ("large128", 1, 16, 32)])
+def test_reduced_large_layers_whole(gpu_lib, name, batch, C, K):
+    ly = LAYERS[name]
+    ly = Layer(ly.name, batch, C or ly.C, K or ly.K, ly.N, ly.n, ly.x_dist, ly.w_var, ly.g_dist)
+    x, w, g = make_inputs(ly, seed=0)
+    check_whole(x, w, g)
+
+
+@pytest.mark.parametrize("name", ["first224", "mid56", "large128"])
+def test_full_size_layers_sampled(gpu_lib, name):
+    ly = LAYERS[name]
+    x, w, g = make_inputs(ly, seed=0)
+    _, y, dx, dw = run_layer(x, w, g)
+    rng = np.random.default_rng(1)
+    S = 48
+    B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
+    # include the corners (ragged last block row and column) among the samples
+    iy = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, K, M, M)]
+    ix = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, C, N, N)]
+    iw = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (K, C, n, n)]
+    e = (relerr(y[tuple(iy)], oracle.conv_forward_at(x, w, *iy)),
+         relerr(dx[tuple(ix)], oracle.conv_backward_data_at(g, w, N, *ix)),
+         relerr(dw[tuple(iw)], oracle.conv_backward_filter_at(x, g, n, *iw)))
+    print(f"{name} sampled rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e} bwd_filter {e[2]:.2e}", flush=True)
+    assert max(e) <= TOL, e
+    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dw).all()
+
+
+def test_stage_spectra_match_oracle_steps(gpu_lib):
+    """Workspace spectra (kernel, input blocks, gradient windows, products)
+    against the OaA steps of the oracle, in the layouts oaa.h documents."""
+    B, C, K, N, n = 2, 3, 4, 23, 5
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=3)
+    plan = binding.Plan(B, C, K, N, n, device=DEV)
+    geo = plan.geometry
+    L, T, F = geo["L"], geo["T"], geo["F"]
+    V = L // 2 + 1
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    plan.forward(xd, wd)
+    torch.cuda.synchronize()
+    Wh = plan.region(binding.REGION_W_SPECTRUM).cpu().numpy().reshape(L, V, C, K)
+    Xh = plan.region(binding.REGION_X_SPECTRUM).cpu().numpy().reshape(L, V, C, B, T, T)
+    Yh = plan.region(binding.REGION_PRODUCT).cpu().numpy()[:F * K * B * T * T].reshape(L, V, K, B, T, T)
+    Wo = oaa_oracle.filter_spectra(w, L)                    # [K,C,L,V]
+    Xo = oaa_oracle.block_spectra(x, n, L)                  # [B,C,T,T,L,V]
+    Yo = oaa_oracle.forward_product(Xo, Wo)                 # [B,K,T,T,L,V]
+    assert relerr(Wh.transpose(3, 2, 0, 1), Wo) < TOL
+    assert relerr(Xh.transpose(3, 2, 4, 5, 0, 1), Xo) < TOL
+    assert relerr(Yh.transpose(3, 2, 4, 5, 0, 1), Yo) < TOL
+    plan.backward_data(gd, None)
+    torch.cuda.synchronize()
+    Gh = plan.region(binding.REGION_G_SPECTRUM).cpu().numpy().reshape(L, V, K, B, T, T)
+    dXh = plan.region(binding.REGION_PRODUCT).cpu().numpy()[:F * C * B * T * T].reshape(L, V, C, B, T, T)
+    Go = oaa_oracle.window_spectra(g, n, N, L)
+    assert relerr(Gh.transpose(3, 2, 4, 5, 0, 1), Go) < TOL
+    assert relerr(dXh.transpose(3, 2, 4, 5, 0, 1), oaa_oracle.backward_data_product(Go, Wo)) < TOL
+    plan.backward_filter(None, None)
+    torch.cuda.synchronize()
+    S = geo["split"]
+    part = plan.region(binding.REGION_PRODUCT).cpu().numpy()[:S * F * C * K].reshape(S, L, V, C, K)
+    dWh = part.astype(np.complex128).sum(0)
+    assert relerr(dWh.transpose(3, 2, 0, 1), oaa_oracle.backward_filter_product(Go, Xo)) < TOL
+
+
+def test_cached_spectra_reuse_matches_explicit_inputs(gpu_lib):
+    B, C, K, N, n = 2, 5, 6, 30, 7
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=5)
+    plan = binding.Plan(B, C, K, N, n, device=DEV)
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    y1 = plan.forward(xd, wd).clone()
+    y2 = plan.forward(xd, None).clone()           # cached kernel spectra
+    dx1 = plan.backward_data(gd, wd).clone()
+    dx2 = plan.backward_data(gd, None).clone()
+    dw1 = plan.backward_filter(xd, gd).clone()
+    plan.forward(xd, wd)
+    plan.backward_data(gd, None)
+    dw2 = plan.backward_filter(None, None).clone()  # cached block and window spectra
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2) and torch.equal(dx1, dx2) and torch.equal(dw1, dw2)
+    assert relerr(dw1.cpu().numpy(), oracle.conv_backward_filter(x, g, n)) <= TOL
+
+
+def test_bitwise_deterministic(gpu_lib):
+    B, C, K, N, n = 2, 66, 70, 24, 3
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=6)
+    _, y1, dx1, dw1 = run_layer(x, w, g)
+    _, y2, dx2, dw2 = run_layer(x, w, g)
+    assert np.array_equal(y1, y2) and np.array_equal(dx1, dx2) and np.array_equal(dw1, dw2)
+
+
+def test_outputs_overwritten_not_accumulated(gpu_lib):
+    B, C, K, N, n = 1, 2, 3, 14, 4
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=7)
+    plan = binding.Plan(B, C, K, N, n, device=DEV)
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    M = N - n + 1
+    y = torch.full((B, K, M, M), 1e6, device=DEV)
+    dx = torch.full((B, C, N, N), -1e6, device=DEV)
+    dw = torch.full((K, C, n, n), 3e5, device=DEV)
+    plan.forward(xd, wd, y)
+    plan.backward_data(gd, wd, dx)
+    plan.backward_filter(xd, gd, dw)
+    torch.cuda.synchronize()
+    assert relerr(y.cpu().numpy(), oracle.conv_forward(x, w)) <= TOL
+    assert relerr(dx.cpu().numpy(), oracle.conv_backward_data(g, w, N)) <= TOL
+    assert relerr(dw.cpu().numpy(), oracle.conv_backward_filter(x, g, n)) <= TOL
+
+
+def test_zero_inputs_give_exact_zeros(gpu_lib):
+    B, C, K, N, n = 1, 3, 2, 19, 6
+    z = np.zeros((B, C, N, N), np.float32)
+    w = np.ones((K, C, n, n), np.float32)
+    g = np.zeros((B, K, N - n + 1, N - n + 1), np.float32)
+    _, y, dx, dw = run_layer(z, w, g)
+    assert not y.any() and not dx.any() and not dw.any()
+
+
+def test_named_stream_is_used(gpu_lib):
+    B, C, K, N, n = 2, 3, 4, 32, 5
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=8)
+    s = torch.cuda.Stream(device=DEV)
+    with torch.cuda.stream(s):
+        plan = binding.Plan(B, C, K, N, n, device=DEV)
+        xd, wd = to_dev(x), to_dev(w)
+        y = plan.forward(xd, wd)
+    s.synchronize()
+    assert relerr(y.cpu().numpy(), oracle.conv_forward(x, w)) <= TOL

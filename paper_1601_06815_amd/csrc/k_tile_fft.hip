@@ -2,13 +2,19 @@
 // inverse transforms with overlap-add or crop (arXiv:1601.06815, Section 2:
 // block division, padding, per-block transforms, overlap by n-1 and add).
 //
-// One workgroup handles a run of consecutive tiles along one block row of one
-// plane. Forward: the rows of the plane that the run covers are staged in LDS
-// with coalesced loads; pass 1 (one lane per pair of tile rows) transforms
-// rows, pass 2 (one lane per tile column) transforms columns and writes the
-// spectra bin-major with consecutive tiles in consecutive addresses. Inverse:
-// the same two passes in the opposite order; the overlap-add accumulates
-// whole block rows in LDS and writes each finished output row once.
+// Forward: one workgroup handles a run of consecutive tiles along one block
+// row of one plane. The plane rows that the run covers are staged in LDS with
+// coalesced loads; pass 1 (one lane per pair of tile rows) transforms rows,
+// pass 2 (one lane per tile column) transforms columns and writes the spectra
+// bin-major with consecutive tiles at consecutive addresses.
+// Inverse: the same two passes in the opposite order. The overlap-add keeps a
+// ring of 2n output rows per plane in LDS: every tile adds its own n columns
+// directly, parks its n-1 overhanging columns, and a second step adds the
+// overhangs, so every output pixel is summed in a fixed order and written once.
+//
+// LDS intermediates are stored tile-major with an odd per-tile stride (in
+// complex elements), so every index inside a tile is a compile-time offset
+// and consecutive tiles fall in different banks.
 #include <algorithm>
 
 #include "fft_core.hpp"
@@ -26,65 +32,119 @@ inline int pick_threads(int tasks) {
   return t < 64 ? 64 : (t > kMaxThreads ? kMaxThreads : t);
 }
 
+__host__ __device__ inline int odd_at_least(int v) { return v | 1; }
 __host__ __device__ inline size_t even_floats(size_t n) { return (n + 1) & ~size_t(1); }
+
+// Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2.
+// Renumber them so that logically consecutive workgroups (neighbouring tiles,
+// which share cache lines of their inputs and outputs) run on the same XCD at
+// about the same time.
+__device__ __forceinline__ unsigned xcd_local_order(unsigned w, unsigned nwg) {
+  const unsigned q = nwg / 8, r = nwg % 8, x = w % 8, j = w / 8;
+  return x * q + min(x, r) + j;
+}
+
+// Copy rows [row0, row0+R) x columns [col0, col0+W) of an H x H plane into
+// LDS rows of stride Wp (zero outside the plane). Lanes are laid out along
+// the columns; each lane issues up to kUnroll independent loads (clamped to a
+// valid address when out of range) before storing any of them.
+constexpr int kUnroll = 8;
+
+__device__ __forceinline__ void stage_rows(float* dst, int Wp, const float* src, int H, int row0, int col0,
+                                           int R, int W) {
+  const int nthr = blockDim.x, tid = threadIdx.x;
+  const int Wt = W < nthr ? W : nthr;
+  const int rstep = nthr / Wt;
+  const int cl = tid % Wt, rl = tid / Wt;
+  if (rl >= rstep) return;
+  for (int c = cl; c < W; c += Wt) {
+    const int gc = col0 + c;
+    const bool col_ok = gc >= 0 && gc < H;
+    for (int rb = rl; rb < R; rb += kUnroll * rstep) {
+      float v[kUnroll];
+#pragma unroll
+      for (int j = 0; j < kUnroll; ++j) {
+        const int r = rb + j * rstep;
+        const int gr = row0 + r;
+        const bool ok = col_ok && r < R && gr >= 0 && gr < H;
+        const float t = src[ok ? size_t(gr) * H + gc : 0];
+        v[j] = ok ? t : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kUnroll; ++j) {
+        const int r = rb + j * rstep;
+        if (r < R) dst[r * Wp + c] = v[j];
+      }
+    }
+  }
+}
 
 // ---------------------------------------------------------------------------
 // Forward: windows -> spectra
+//
+// LDS: img [R + 1][Wp] floats (row R stays zero), then zbuf [TQ][TS] float2,
+// TS >= ROWS * V (rounded up to whole row pairs) odd, ROWS = L/2 when
+// windows fill at most half a tile (ZH), else L. Row r of tile q's row transform is at zbuf[q * TS + r * V + v].
 template <int L, bool ZH>
 __global__ void __launch_bounds__(kMaxThreads) tile_rfft2_kernel(TileFwdParams p) {
   constexpr int V = L / 2 + 1;
+  constexpr int ROWS = ZH ? L / 2 : L;
+  constexpr int S = ZH ? L / 2 : L;         // row entries that may be nonzero
+  constexpr int PAIRS = (ROWS + 1) / 2;     // row pairs covering rows [0, ROWS)
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
-  const long wg = blockIdx.x;
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
-  const long rest = wg / p.nchunk;
+  const unsigned rest = wg / p.nchunk;
   const int strip = int(rest % p.T);
-  const long plane = rest / p.T;
+  const unsigned plane = rest / p.T;
   const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
   const int q0 = chunk * p.TQ;
   const int nq = min(p.TQ, p.T - q0);
   const int R = p.R, pitch = p.pitch;
   const int W = (nq - 1) * pitch + R;
-  float* img_s = smem;                                                      // [R][W]
-  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R) * W));  // [R][V][TQ]
+  const int Wp = (p.TQ - 1) * pitch + R + L;  // row stride: reads past W stay inside the row
+  const int TS = odd_at_least(2 * PAIRS * V);
+  float* img_s = smem;                                                                 // [R+1][Wp]
+  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R + 1) * Wp));  // [TQ][TS]
 
   const float* src = p.src + size_t(plane) * p.H * p.H;
-  const int row0 = strip * pitch - p.off, col0 = q0 * pitch - p.off;
-  for (int idx = tid; idx < R * W; idx += nthr) {
-    const int r = idx / W, c = idx - r * W;
-    const int gr = row0 + r, gc = col0 + c;
-    float val = 0.f;
-    if (gr >= 0 && gr < p.H && gc >= 0 && gc < p.H) val = src[size_t(gr) * p.H + gc];
-    img_s[idx] = val;
-  }
+  stage_rows(img_s, Wp, src, p.H, strip * pitch - p.off, q0 * pitch - p.off, R, W);
+  for (int c = tid; c < Wp; c += nthr) img_s[R * Wp + c] = 0.f;
   __syncthreads();
 
-  // pass 1: real rows, two per lane
-  const int npair = (R + 1) >> 1;
-  for (int task = tid; task < npair * nq; task += nthr) {
+  // pass 1: real rows, two per lane (row R is the zero row); pairs past the
+  // window write zero rows, so pass 2 reads every row unconditionally
+  for (int task = tid; task < PAIRS * nq; task += nthr) {
     const int q = task % nq, pr = task / nq;
-    const int r0 = 2 * pr, r1 = r0 + 1;
-    const bool has1 = r1 < R;
-    const float* row_a = img_s + r0 * W + q * pitch;
-    const float* row_b = row_a + W;
+    const int r0 = 2 * pr;
+    float2* zt = zbuf + q * TS + r0 * V;
+    if (r0 >= R) {
+#pragma unroll
+      for (int v = 0; v < 2 * V; ++v) zt[v] = make_float2(0.f, 0.f);
+      continue;
+    }
+    const float* row_a = img_s + r0 * Wp + q * pitch;
+    const float* row_b = row_a + Wp;
     float zr[L], zi[L];
 #pragma unroll
     for (int s = 0; s < L; ++s) {
-      if (ZH && s >= L / 2) {
+      if (s < S) {
+        const float a = row_a[s], b = row_b[s];
+        const bool in = s < R;
+        zr[s] = in ? a : 0.f;
+        zi[s] = in ? b : 0.f;
+      } else {
         zr[s] = 0.f;
         zi[s] = 0.f;
-      } else {
-        const bool in = s < R;
-        zr[s] = in ? row_a[s] : 0.f;
-        zi[s] = (in && has1) ? row_b[s] : 0.f;
       }
     }
     float2 X0[V], X1[V];
     rfft_pair<L, ZH>(zr, zi, X0, X1);
 #pragma unroll
     for (int v = 0; v < V; ++v) {
-      zbuf[(r0 * V + v) * p.TQ + q] = X0[v];
-      if (has1) zbuf[(r1 * V + v) * p.TQ + q] = X1[v];
+      zt[v] = X0[v];
+      zt[V + v] = X1[v];
     }
   }
   __syncthreads();
@@ -92,74 +152,93 @@ __global__ void __launch_bounds__(kMaxThreads) tile_rfft2_kernel(TileFwdParams p
   // pass 2: complex columns, bin-major stores
   const size_t tiles_per_ch = size_t(p.n_img) * p.T * p.T;
   const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
+  const size_t ustride = size_t(V) * fstride;
   float2* out = p.dst + size_t(ch) * tiles_per_ch + size_t(img) * p.T * p.T + size_t(strip) * p.T + q0;
   for (int task = tid; task < V * nq; task += nthr) {
     const int q = task % nq, v = task / nq;
+    const float2* zt = zbuf + q * TS + v;
     float re[L], im[L];
 #pragma unroll
     for (int r = 0; r < L; ++r) {
-      float2 z = make_float2(0.f, 0.f);
-      if (!(ZH && r >= L / 2) && r < R) z = zbuf[(r * V + v) * p.TQ + q];
-      re[r] = z.x;
-      im[r] = z.y;
+      if (r < ROWS) {
+        const float2 z = zt[r * V];
+        re[r] = z.x;
+        im[r] = z.y;
+      } else {
+        re[r] = 0.f;
+        im[r] = 0.f;
+      }
     }
     fft_dif<L, -1, ZH>(re, im);
+    float2* o = out + size_t(v) * fstride + q;
 #pragma unroll
     for (int u = 0; u < L; ++u) {
       const int pos = bitrev(u, L);
-      out[size_t(u * V + v) * fstride + q] = make_float2(re[pos], im[pos]);
+      o[u * ustride] = make_float2(re[pos], im[pos]);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// Inverse column pass shared by the two inverse kernels: spectra of tiles
-// [q0, q0+nq) of block row `strip` -> zbuf rows [0, R).
-template <int L>
+// Inverse column pass shared by the inverse kernels: for the tiles at
+// in[q], q < nq (bin f at in[q + f * fstride], plus nsplit - 1 partial sums
+// spaced split_stride apart), transform every column v and keep rows
+// [0, ROWS) at zbuf[q * TS + r * V + v].
+template <int L, int ROWS>
 __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride, int nsplit,
-                                                size_t split_stride, int nq, int TQ, int R,
-                                                float2* zbuf) {
+                                                size_t split_stride, int nq, int TS, float2* zbuf) {
   constexpr int V = L / 2 + 1;
+  const size_t ustride = size_t(V) * fstride;
   for (int task = threadIdx.x; task < V * nq; task += blockDim.x) {
     const int q = task % nq, v = task / nq;
-    const float2* col = in + q;
+    const float2* col = in + q + size_t(v) * fstride;
     float re[L], im[L];
 #pragma unroll
     for (int u = 0; u < L; ++u) {
-      float2 z = col[size_t(u * V + v) * fstride];
-      for (int s = 1; s < nsplit; ++s) {
-        const float2 t = col[s * split_stride + size_t(u * V + v) * fstride];
-        z.x += t.x;
-        z.y += t.y;
-      }
+      const float2 z = col[u * ustride];
       re[u] = z.x;
       im[u] = z.y;
     }
-    fft_dif<L, +1, false>(re, im);
+    for (int s = 1; s < nsplit; ++s) {
+      const float2* cs = col + s * split_stride;
 #pragma unroll
-    for (int r = 0; r < L; ++r) {
-      if (r < R) {
-        const int pos = bitrev(r, L);
-        zbuf[(r * V + v) * TQ + q] = make_float2(re[pos], im[pos]);
+      for (int u = 0; u < L; ++u) {
+        const float2 z = cs[u * ustride];
+        re[u] += z.x;
+        im[u] += z.y;
       }
+    }
+    fft_dif<L, +1, false>(re, im);
+    float2* zt = zbuf + q * TS + v;
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+      const int pos = bitrev(r, L);
+      zt[r * V] = make_float2(re[pos], im[pos]);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
 // Inverse + overlap-add + valid crop
+//
+// LDS: ring [2n][Wacc] floats (absolute output row a lives in ring row
+// a mod 2n), then zbuf [TQ][TS] float2, TS >= L * V odd, holding the column
+// transforms of rows [0, L-1) (>= 2n-1 rows); after the row pass a tile's row
+// r area holds the n-1 columns of that row which overhang the next tile.
 template <int L>
 __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_add_kernel(OverlapAddParams p) {
   constexpr int V = L / 2 + 1;
+  constexpr int RT = L - 1;
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
-  const int n = p.n, T = p.T, M = p.M, R = 2 * n - 1;
+  const int n = p.n, T = p.T, M = p.M, R = 2 * n - 1, RING = 2 * n;
   const int Wacc = T * n + n - 1;
-  float* acc = smem;                                                          // [R][Wacc]
-  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R) * Wacc));  // [R][V][TQ]
-  const long wg = blockIdx.x;
+  const int TS = odd_at_least(L * V);
+  float* ring = smem;                                                                  // [2n][Wacc]
+  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(RING) * Wacc));  // [TQ][TS]
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int grp = int(wg % p.ngroups);
-  const long plane = wg / p.ngroups;
+  const unsigned plane = wg / p.ngroups;
   const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
   const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
   const size_t tiles_per_ch = size_t(p.n_img) * T * T;
@@ -168,107 +247,138 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_add_kernel(Overlap
   float* out = p.dst + size_t(plane) * M * M;
   const float scale = 1.0f / float(L * L);
 
-  for (int i = tid; i < R * Wacc; i += nthr) acc[i] = 0.f;
+  for (int i = tid; i < RING * Wacc; i += nthr) ring[i] = 0.f;
   __syncthreads();
 
   // block row pb-1 is recomputed (not written) to supply the rows that
   // overlap into block row pb
   for (int strip = (pb > 0 ? pb - 1 : 0); strip < pe; ++strip) {
+    const int a0 = strip * n;           // first absolute output row of this block row
+    const int slot0 = a0 % RING;        // its ring row
     for (int q0 = 0; q0 < T; q0 += p.TQ) {
       const int nq = min(p.TQ, T - q0);
-      inverse_columns<L>(in + size_t(strip) * T + q0, fstride, 1, 0, nq, p.TQ, R, zbuf);
+      inverse_columns<L, RT>(in + size_t(strip) * T + q0, fstride, 1, 0, nq, TS, zbuf);
       __syncthreads();
-      // rows, in two passes over tiles of even and odd block column so that
-      // the overlapping tiles of one pass never touch the same pixel
-      for (int parity = 0; parity < 2; ++parity) {
-        const int first = (parity - q0) & 1;
-        const int cnt = nq > first ? (nq - first + 1) / 2 : 0;
-        for (int task = tid; task < n * cnt; task += nthr) {
-          const int j = task % cnt, pr = task / cnt;
-          const int q = first + 2 * j;
-          const int r0 = 2 * pr, r1 = r0 + 1;
-          const bool has1 = r1 < R;
-          float2 A[V], Bv[V];
+      // rows: own n columns straight into the ring, overhang parked in zbuf
+      for (int task = tid; task < n * nq; task += nthr) {
+        const int q = task % nq, pr = task / nq;
+        const int r0 = 2 * pr;
+        float2* zt = zbuf + q * TS + r0 * V;
+        float2 A[V], Bv[V];
 #pragma unroll
-          for (int v = 0; v < V; ++v) {
-            A[v] = zbuf[(r0 * V + v) * p.TQ + q];
-            Bv[v] = has1 ? zbuf[(r1 * V + v) * p.TQ + q] : make_float2(0.f, 0.f);
-          }
-          float zr[L], zi[L];
-          irfft_pair<L>(A, Bv, zr, zi);
-          float* d0 = acc + r0 * Wacc + (q0 + q) * n;
+        for (int v = 0; v < V; ++v) {
+          A[v] = zt[v];
+          Bv[v] = zt[V + v];  // row 2n-1 (when r0 + 1 == 2n-1) is read but discarded
+        }
+        float zr[L], zi[L];
+        irfft_pair<L>(A, Bv, zr, zi);
+        const bool has1 = r0 + 1 < R;
+        int s0 = slot0 + r0;
+        if (s0 >= RING) s0 -= RING;
+        int s1 = s0 + 1;
+        if (s1 >= RING) s1 -= RING;
+        float* d0 = ring + s0 * Wacc + (q0 + q) * n;
+        float* d1 = ring + s1 * Wacc + (q0 + q) * n;
+        float* o0 = reinterpret_cast<float*>(zt);      // overhang of row r0
+        float* o1 = reinterpret_cast<float*>(zt + V);  // overhang of row r0 + 1
 #pragma unroll
-          for (int s = 0; s < L; ++s) {
-            if (s < R) {
-              const int pos = bitrev(s, L);
-              d0[s] += zr[pos] * scale;
-              if (has1) d0[Wacc + s] += zi[pos] * scale;
-            }
+        for (int s = 0; s < L; ++s) {
+          const int pos = bitrev(s, L);
+          const float t0 = zr[pos] * scale, t1 = zi[pos] * scale;
+          if (s < n) {
+            d0[s] += t0;
+            if (has1) d1[s] += t1;
+          } else if (s < R) {
+            o0[s - n] = t0;
+            if (has1) o1[s - n] = t1;
           }
         }
-        __syncthreads();
       }
+      __syncthreads();
+      // overhangs: tile q's columns [n, 2n-1) land on columns [(q+1)n, (q+1)n + n-1)
+      const int ov = nq * (n - 1);
+      for (int c = tid; c < ov; c += nthr) {
+        const int q = c / (n - 1), s = c - q * (n - 1);
+        const float* o = reinterpret_cast<const float*>(zbuf + q * TS) + s;
+        float* dcol = ring + (q0 + q + 1) * n + s;
+        int slot = slot0;
+        for (int r = 0; r < R; ++r) {
+          dcol[slot * Wacc] += o[r * 2 * V];
+          if (++slot == RING) slot = 0;
+        }
+      }
+      __syncthreads();
     }
-    if (strip >= pb) {
-      for (int idx = tid; idx < n * M; idx += nthr) {
-        const int r = idx / M, j = idx - r * M;
-        const int i = strip * n + r - (n - 1);
-        if (i >= 0 && i < M) out[size_t(i) * M + j] = acc[r * Wacc + j + n - 1];
+    // rows [a0, a0 + n) are complete: write the valid part, then clear them
+    int slot = slot0;
+    for (int r = 0; r < n; ++r) {
+      const float* row = ring + slot * Wacc;
+      const int i = a0 + r - (n - 1);
+      if (strip >= pb && i >= 0 && i < M) {
+        for (int j = tid; j < M; j += nthr) out[size_t(i) * M + j] = row[j + n - 1];
       }
+      if (++slot == RING) slot = 0;
     }
     __syncthreads();
-    for (int idx = tid; idx < (n - 1) * Wacc; idx += nthr) acc[idx] = acc[n * Wacc + idx];
-    __syncthreads();
-    for (int idx = tid; idx < n * Wacc; idx += nthr) acc[(n - 1) * Wacc + idx] = 0.f;
+    slot = slot0;
+    for (int r = 0; r < n; ++r) {
+      float* row = ring + slot * Wacc;
+      for (int j = tid; j < Wacc; j += nthr) row[j] = 0.f;
+      if (++slot == RING) slot = 0;
+    }
     __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// Inverse + top-left n x n crop, scattered to the blocks of the output planes
+// Inverse + top-left n x n crop, scattered to the blocks of the output planes.
+// A workgroup takes TQ consecutive tiles of one channel (they may span block
+// rows and images), so its spectrum reads are contiguous.
 template <int L>
 __global__ void __launch_bounds__(kMaxThreads) irfft2_crop_kernel(CropParams p) {
   constexpr int V = L / 2 + 1;
+  constexpr int RT = L / 2;  // rows kept from the column transforms (>= n)
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
-  float2* zbuf = reinterpret_cast<float2*>(smem);  // [n][V][TQ]
-  const long wg = blockIdx.x;
+  const int TS = odd_at_least((RT + 1) * V);
+  float2* zbuf = reinterpret_cast<float2*>(smem);  // [TQ][TS]
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
-  const long rest = wg / p.nchunk;
-  const int strip = int(rest % p.T);
-  const long plane = rest / p.T;
-  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
-  const int q0 = chunk * p.TQ;
-  const int nq = min(p.TQ, p.T - q0);
+  const int ch = int(wg / p.nchunk);
+  const int P = p.T * p.T;
+  const int tiles = p.n_img * P;
+  const int t0 = chunk * p.TQ;
+  const int nq = min(p.TQ, tiles - t0);
   const int n = p.n, H = p.H;
-  const size_t tiles_per_ch = size_t(p.n_img) * p.T * p.T;
-  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
-  const float2* in =
-      p.src + size_t(ch) * tiles_per_ch + size_t(img) * p.T * p.T + size_t(strip) * p.T + q0;
-  inverse_columns<L>(in, fstride, p.nsplit, p.split_stride, nq, p.TQ, n, zbuf);
+  const size_t fstride = size_t(p.n_ch) * tiles;
+  inverse_columns<L, RT>(p.src + size_t(ch) * tiles + t0, fstride, p.nsplit, p.split_stride, nq, TS, zbuf);
   __syncthreads();
-  float* out = p.dst + size_t(plane) * H * H;
   const float scale = 1.0f / float(L * L);
   const int npair = (n + 1) >> 1;
   for (int task = tid; task < npair * nq; task += nthr) {
     const int q = task % nq, pr = task / nq;
-    const int r0 = 2 * pr, r1 = r0 + 1;
-    const bool has1 = r1 < n;
+    const int r0 = 2 * pr;
+    const float2* zt = zbuf + q * TS + r0 * V;
     float2 A[V], Bv[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) {
-      A[v] = zbuf[(r0 * V + v) * p.TQ + q];
-      Bv[v] = has1 ? zbuf[(r1 * V + v) * p.TQ + q] : make_float2(0.f, 0.f);
+      A[v] = zt[v];
+      Bv[v] = zt[V + v];  // row n (odd n) is read but discarded
     }
     float zr[L], zi[L];
     irfft_pair<L>(A, Bv, zr, zi);
-    const int gr0 = strip * n + r0, gc0 = (q0 + q) * n;
+    const int t = t0 + q;
+    const int img = t / P, pp = t - img * P;
+    const int prow = pp / p.T, qcol = pp - prow * p.T;
+    const int gr0 = prow * n + r0, gc0 = qcol * n;
+    float* o = p.dst + (size_t(img) * p.n_ch + ch) * H * H;
+    const bool w0 = gr0 < H, w1 = r0 + 1 < n && gr0 + 1 < H;
 #pragma unroll
-    for (int s = 0; s < L; ++s) {
+    for (int s = 0; s < L / 2; ++s) {
       if (s < n && gc0 + s < H) {
         const int pos = bitrev(s, L);
-        if (gr0 < H) out[size_t(gr0) * H + gc0 + s] = zr[pos] * scale;
-        if (has1 && gr0 + 1 < H) out[size_t(gr0 + 1) * H + gc0 + s] = zi[pos] * scale;
+        if (w0) o[size_t(gr0) * H + gc0 + s] = zr[pos] * scale;
+        if (w1) o[size_t(gr0 + 1) * H + gc0 + s] = zi[pos] * scale;
       }
     }
   }
@@ -280,9 +390,12 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_crop_kernel(CropParams p) 
 template <int L, bool ZH>
 hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
+  constexpr int ROWS = ZH ? L / 2 : L;
+  constexpr int PAIRS = (ROWS + 1) / 2;
+  const int TS = odd_at_least(2 * PAIRS * V);
   auto lds_for = [&](int tq) {
-    const size_t W = size_t(tq - 1) * p.pitch + p.R;
-    return even_floats(size_t(p.R) * W) * 4 + size_t(p.R) * V * tq * 8;
+    const size_t Wp = size_t(tq - 1) * p.pitch + p.R + L;
+    return even_floats(size_t(p.R + 1) * Wp) * 4 + size_t(TS) * tq * 8;
   };
   int nchunk = 1;
   while (nchunk < p.T && lds_for((p.T + nchunk - 1) / nchunk) > kLdsBudget) ++nchunk;
@@ -290,7 +403,7 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
   p.nchunk = (p.T + p.TQ - 1) / p.TQ;
   const size_t lds = lds_for(p.TQ);
   if (lds > kLdsBudget) return hipErrorInvalidConfiguration;
-  const int tasks = std::max(((p.R + 1) / 2) * p.TQ, V * p.TQ);
+  const int tasks = std::max(PAIRS * p.TQ, V * p.TQ);
   const long nwg = long(p.n_img) * p.n_ch * p.T * p.nchunk;
   hipLaunchKernelGGL((tile_rfft2_kernel<L, ZH>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
@@ -299,13 +412,13 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
 template <int L>
 hipError_t launch_oa_L(OverlapAddParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
-  const int R = 2 * p.n - 1;
-  const size_t acc_bytes = even_floats(size_t(R) * (size_t(p.T) * p.n + p.n - 1)) * 4;
-  const size_t per_tile = size_t(R) * V * 8;
+  const int TS = odd_at_least(L * V);
+  const size_t ring_bytes = even_floats(size_t(2 * p.n) * (size_t(p.T) * p.n + p.n - 1)) * 4;
+  const size_t per_tile = size_t(TS) * 8;
   size_t budget = kLdsBudget;
-  if (acc_bytes + per_tile > budget) budget = 160 * 1024;  // gfx950: 160 KiB per workgroup
-  if (acc_bytes + per_tile > budget) return hipErrorInvalidConfiguration;
-  int tq = int(std::min<size_t>(p.T, (budget - acc_bytes) / per_tile));
+  if (ring_bytes + per_tile > budget) budget = 160 * 1024;  // gfx950: 160 KiB per workgroup
+  if (ring_bytes + per_tile > budget) return hipErrorInvalidConfiguration;
+  int tq = int(std::min<size_t>(p.T, (budget - ring_bytes) / per_tile));
   const int nchunk = (p.T + tq - 1) / tq;
   p.TQ = (p.T + nchunk - 1) / nchunk;
   p.nchunk = nchunk;
@@ -314,13 +427,13 @@ hipError_t launch_oa_L(OverlapAddParams p, hipStream_t s) {
   if (planes < 2048) ngroups = int(std::min<long>(p.T, (2048 + planes - 1) / planes));
   p.SPW = (p.T + ngroups - 1) / ngroups;
   p.ngroups = (p.T + p.SPW - 1) / p.SPW;
-  const size_t lds = acc_bytes + per_tile * p.TQ;
+  const size_t lds = ring_bytes + per_tile * p.TQ;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&irfft2_overlap_add_kernel<L>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
   }
-  const int tasks = std::max(V * p.TQ, p.n * ((p.TQ + 1) / 2));
+  const int tasks = std::max(V * p.TQ, p.n * p.TQ);
   hipLaunchKernelGGL(irfft2_overlap_add_kernel<L>, dim3(unsigned(planes * p.ngroups)),
                      dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
@@ -329,14 +442,18 @@ hipError_t launch_oa_L(OverlapAddParams p, hipStream_t s) {
 template <int L>
 hipError_t launch_crop_L(CropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
-  const size_t per_tile = size_t(p.n) * V * 8;
-  int tq = int(std::min<size_t>(p.T, kLdsBudget / per_tile));
-  const int nchunk = (p.T + tq - 1) / tq;
-  p.TQ = (p.T + nchunk - 1) / nchunk;
-  p.nchunk = nchunk;
+  const int TS = odd_at_least((L / 2 + 1) * V);
+  const size_t per_tile = size_t(TS) * 8;
+  const long tiles = long(p.n_img) * p.T * p.T;
+  // enough consecutive tiles for 128-byte reads, as LDS allows
+  long tq = std::min<long>(long(kLdsBudget / per_tile), 64);
+  if (tq > tiles) tq = tiles;
+  const long nchunk = (tiles + tq - 1) / tq;
+  p.TQ = int((tiles + nchunk - 1) / nchunk);
+  p.nchunk = int(nchunk);
   const size_t lds = per_tile * p.TQ;
   const int tasks = std::max(V * p.TQ, ((p.n + 1) / 2) * p.TQ);
-  const long nwg = long(p.n_img) * p.n_ch * p.T * p.nchunk;
+  const long nwg = long(p.n_ch) * p.nchunk;
   hipLaunchKernelGGL(irfft2_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }

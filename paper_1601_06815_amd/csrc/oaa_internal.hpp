@@ -77,5 +77,8 @@ hipError_t launch_irfft2_overlap_add(int L, const OverlapAddParams& p, hipStream
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
 hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s);
 hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s);
+hipError_t launch_cgemm_mfma3(const GemmParams& p, hipStream_t s);
+// Shape rule of the automatic choice between the two contractions.
+bool mfma_preferred(const GemmParams& p);
 
 }  // namespace oaa

@@ -166,8 +166,14 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
 
 oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipStream_t s, const char* what) {
   g.F = p->F;
+  oaa_contraction_t c = p->contraction;
+  if (c == OAA_CONTRACTION_AUTO) c = oaa::mfma_preferred(g) ? OAA_CONTRACTION_MFMA : OAA_CONTRACTION_VALU;
   return timed(p, stage, s, what, [&] {
-    return p->contraction == OAA_CONTRACTION_MFMA ? oaa::launch_cgemm_mfma(g, s) : oaa::launch_cgemm_valu(g, s);
+    switch (c) {
+      case OAA_CONTRACTION_MFMA: return oaa::launch_cgemm_mfma(g, s);
+      case OAA_CONTRACTION_MFMA3: return oaa::launch_cgemm_mfma3(g, s);
+      default: return oaa::launch_cgemm_valu(g, s);
+    }
   });
 }
 
@@ -221,9 +227,11 @@ oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n)
     return fail(OAA_ERR_UNSUPPORTED, "spectra exceed the addressable workspace");
 
   // split of the weight-gradient reduction over B*P so that the contraction
-  // has enough workgroups to fill the device
-  const long long tiles = (long long)((C + 63) / 64) * ((K + 63) / 64) * F;
-  long long split = tiles >= 2048 ? 1 : (2048 + tiles - 1) / tiles;
+  // (96- or 128-row by 128-column tiles, two workgroups per CU) runs in at
+  // least eight rounds of 512 workgroups
+  const long long rows = ((C + 95) / 96) * 96 - C < ((C + 127) / 128) * 128 - C ? (C + 95) / 96 : (C + 127) / 128;
+  const long long tiles = rows * ((K + 127) / 128) * F;
+  long long split = tiles >= 4096 ? 1 : (4096 + tiles - 1) / tiles;
   const long long max_split = (BP + 63) / 64;
   if (split > max_split) split = max_split;
   if (split < 1) split = 1;
@@ -336,7 +344,8 @@ oaa_status_t oaa_plan_bind_workspace(oaa_plan_t plan, void* dev_ptr, size_t byte
 
 oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which) {
   if (oaa_status_t st = check_plan(plan, false)) return st;
-  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA)
+  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA &&
+      which != OAA_CONTRACTION_MFMA3)
     return fail(OAA_ERR_INVALID_ARG, "unknown contraction %d", (int)which);
   plan->contraction = which;
   return OAA_OK;

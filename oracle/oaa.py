@@ -84,21 +84,26 @@ def filter_spectra(w, L=None):
     return np.fft.rfft2(tiles)
 
 
-def window_spectra(g, n, N, L=None):
+def window_spectra(g, n, N, L=None, side=None):
     """Adjoint of steps 6-7, then 2-3, on the upstream gradient:
-    g[B,K,M,M] -> G_hat[B,K,T,T,L,L//2+1]."""
+    g[B,K,M,M] -> G_hat[B,K,T,T,L,L//2+1]. Windows are side x side
+    (default 2n-1, the padded size of Section 3.2; any side in [2n-1, L]
+    gives the same backward results, since rows and columns past 2n-2 only
+    meet kernel taps beyond n)."""
     g = np.asarray(g, dtype=np.float64)
     B, K, M, _ = g.shape
     L = fft_size(n) if L is None else L
+    side = 2 * n - 1 if side is None else side
+    if not 2 * n - 1 <= side <= L:
+        raise ValueError("window side must lie in [2n-1, L]")
     T = block_grid(N, n)
-    S = T * n + n - 1
+    S = T * n + side
     gfull = np.zeros((B, K, S, S))
     gfull[:, :, n - 1:n - 1 + M, n - 1:n - 1 + M] = g
     tiles = np.zeros((B, K, T, T, L, L))
     for P in range(T):
         for Q in range(T):
-            tiles[:, :, P, Q, :2 * n - 1, :2 * n - 1] = \
-                gfull[:, :, P * n:P * n + 2 * n - 1, Q * n:Q * n + 2 * n - 1]
+            tiles[:, :, P, Q, :side, :side] = gfull[:, :, P * n:P * n + side, Q * n:Q * n + side]
     return np.fft.rfft2(tiles)
 
 
@@ -139,23 +144,23 @@ def forward(x, w, L=None):
     return overlap_add(forward_product(block_spectra(x, n, L), filter_spectra(w, L)), n, N, L)
 
 
-def backward_data(g, w, N, L=None):
+def backward_data(g, w, N, L=None, side=None):
     """OaA error propagation: window spectra times conj(kernel spectra), summed
     over K, inverse, top-left n x n of each tile placed at its block."""
     w = np.asarray(w, dtype=np.float64)
     K, C, n, _ = w.shape
     L = fft_size(n) if L is None else L
-    dXh = backward_data_product(window_spectra(g, n, N, L), filter_spectra(w, L))
+    dXh = backward_data_product(window_spectra(g, n, N, L, side), filter_spectra(w, L))
     blk = np.fft.irfft2(dXh, s=(L, L))[..., :n, :n]                     # [B,C,T,T,n,n]
     B, _, T, _, _, _ = blk.shape
     dx = blk.transpose(0, 1, 2, 4, 3, 5).reshape(B, C, T * n, T * n)
     return np.ascontiguousarray(dx[:, :, :N, :N])
 
 
-def backward_filter(x, g, n, L=None):
+def backward_filter(x, g, n, L=None, side=None):
     """OaA weight gradient: window spectra times conj(block spectra), summed
     over the batch and all blocks, inverse, top-left n x n."""
     N = np.asarray(x).shape[-1]
     L = fft_size(n) if L is None else L
-    dWh = backward_filter_product(window_spectra(g, n, N, L), block_spectra(x, n, L))
+    dWh = backward_filter_product(window_spectra(g, n, N, L, side), block_spectra(x, n, L))
     return np.ascontiguousarray(np.fft.irfft2(dWh, s=(L, L))[..., :n, :n])

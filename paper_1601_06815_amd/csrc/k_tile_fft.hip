@@ -19,65 +19,13 @@
 
 #include "fft_core.hpp"
 #include "oaa_internal.hpp"
+#include "tile_common.hpp"
 
 namespace oaa {
 
 namespace {
 
-constexpr int kMaxThreads = 256;
-constexpr size_t kLdsBudget = 60 * 1024;
-
-inline int pick_threads(int tasks) {
-  int t = ((tasks + 63) / 64) * 64;
-  return t < 64 ? 64 : (t > kMaxThreads ? kMaxThreads : t);
-}
-
-__host__ __device__ inline int odd_at_least(int v) { return v | 1; }
-__host__ __device__ inline size_t even_floats(size_t n) { return (n + 1) & ~size_t(1); }
-
-// Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2.
-// Renumber them so that logically consecutive workgroups (neighbouring tiles,
-// which share cache lines of their inputs and outputs) run on the same XCD at
-// about the same time.
-__device__ __forceinline__ unsigned xcd_local_order(unsigned w, unsigned nwg) {
-  const unsigned q = nwg / 8, r = nwg % 8, x = w % 8, j = w / 8;
-  return x * q + min(x, r) + j;
-}
-
-// Copy rows [row0, row0+R) x columns [col0, col0+W) of an H x H plane into
-// LDS rows of stride Wp (zero outside the plane). Lanes are laid out along
-// the columns; each lane issues up to kUnroll independent loads (clamped to a
-// valid address when out of range) before storing any of them.
-constexpr int kUnroll = 8;
-
-__device__ __forceinline__ void stage_rows(float* dst, int Wp, const float* src, int H, int row0, int col0,
-                                           int R, int W) {
-  const int nthr = blockDim.x, tid = threadIdx.x;
-  const int Wt = W < nthr ? W : nthr;
-  const int rstep = nthr / Wt;
-  const int cl = tid % Wt, rl = tid / Wt;
-  if (rl >= rstep) return;
-  for (int c = cl; c < W; c += Wt) {
-    const int gc = col0 + c;
-    const bool col_ok = gc >= 0 && gc < H;
-    for (int rb = rl; rb < R; rb += kUnroll * rstep) {
-      float v[kUnroll];
-#pragma unroll
-      for (int j = 0; j < kUnroll; ++j) {
-        const int r = rb + j * rstep;
-        const int gr = row0 + r;
-        const bool ok = col_ok && r < R && gr >= 0 && gr < H;
-        const float t = src[ok ? size_t(gr) * H + gc : 0];
-        v[j] = ok ? t : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < kUnroll; ++j) {
-        const int r = rb + j * rstep;
-        if (r < R) dst[r * Wp + c] = v[j];
-      }
-    }
-  }
-}
+using namespace tile;
 
 // ---------------------------------------------------------------------------
 // Forward: windows -> spectra

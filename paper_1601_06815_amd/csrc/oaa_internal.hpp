@@ -52,6 +52,29 @@ struct CropParams {
   int TQ, nchunk;
 };
 
+// Gradient windows through block spectra (overlap by n in the frequency
+// domain): window (P, Q) is the 2n x 2n region of the framed plane starting
+// at (P*pitch - off, Q*pitch - off) of plane coordinates, pitch = n; its
+// spectrum goes to dst like TileFwdParams'.
+struct WindowFoldParams {
+  const float* src;  // [n_img][n_ch][H][H]
+  float2* dst;       // [F][n_ch][n_img * T * T]
+  int n_img, n_ch;
+  int H, n, off, T;
+  int TQ, nchunk;    // window columns per workgroup, ceil(T / TQ)
+  int SPW, ngroups;  // window rows per workgroup, ceil(T / SPW)
+};
+
+// Forward output through folded tile spectra: output block (P, Q) covers
+// rows P*n - off + [0, n) and columns Q*n - off + [0, n) of dst[n_img][n_ch][M][M].
+struct FoldCropParams {
+  const float2* src;  // [F][n_ch][n_img * T * T]
+  float* dst;         // [n_img][n_ch][M][M]
+  int n_img, n_ch;
+  int M, n, off, T;
+  int TQ, nchunk, SPW, ngroups;
+};
+
 // Batched complex matrix product, one problem per frequency bin f:
 //   Cmat[f] (M x N) = op(A[f]) (M x Kr) * op(B[f]) (Kr x N)
 // A element (m, kk) is at A + f*a_fstride + (a_trans ? kk*lda + m : m*lda + kk),
@@ -75,6 +98,8 @@ struct GemmParams {
 hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
 hipError_t launch_irfft2_overlap_add(int L, const OverlapAddParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
+hipError_t launch_window_fold_rfft2(int L, const WindowFoldParams& p, hipStream_t s);
+hipError_t launch_irfft2_fold_crop(int L, const FoldCropParams& p, hipStream_t s);
 hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s);
 hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s);
 hipError_t launch_cgemm_mfma3(const GemmParams& p, hipStream_t s);

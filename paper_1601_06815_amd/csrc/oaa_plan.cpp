@@ -147,19 +147,19 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
 }
 
 oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
-  // window (P,Q) of the zero-framed gradient: g[P*n + r - (n-1)][Q*n + s - (n-1)]
-  oaa::TileFwdParams t{};
+  // window (P,Q) of the zero-framed gradient: g[P*n + r - (n-1)][Q*n + s - (n-1)],
+  // r, s < 2n, formed from n x n block spectra
+  oaa::WindowFoldParams t{};
   t.src = g;
   t.dst = region(p, OAA_REGION_G_SPECTRUM);
   t.n_img = p->B;
   t.n_ch = p->K;
   t.H = p->M;
-  t.pitch = p->n;
+  t.n = p->n;
   t.off = p->n - 1;
-  t.R = 2 * p->n - 1;
   t.T = p->T;
   oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient window spectra",
-                          [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+                          [&] { return oaa::launch_window_fold_rfft2(p->L, t, s); });
   if (st == OAA_OK) p->g_valid = true;
   return st;
 }
@@ -374,13 +374,13 @@ oaa_status_t oaa_conv_forward(oaa_plan_t p, const float* x, const float* w, floa
   g.nsplit = 1; g.kchunk = p->C; g.c_sstride = 0;
   g.a_trans = true; g.a_conj = false; g.b_trans = false; g.b_conj = false;
   if ((st = run_gemm(p, g, OAA_STAGE_FWD_PRODUCT, s, "forward contraction"))) return st;
-  oaa::OverlapAddParams o{};
+  oaa::FoldCropParams o{};
   o.src = region(p, OAA_REGION_PRODUCT);
   o.dst = y;
   o.n_img = p->B; o.n_ch = p->K;
-  o.M = p->M; o.n = p->n; o.T = p->T;
+  o.M = p->M; o.n = p->n; o.off = p->n - 1; o.T = p->T;
   return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
-               [&] { return oaa::launch_irfft2_overlap_add(p->L, o, s); });
+               [&] { return oaa::launch_irfft2_fold_crop(p->L, o, s); });
 }
 
 oaa_status_t oaa_conv_backward_data(oaa_plan_t p, const float* g, const float* w, float* dx, void* stream) {

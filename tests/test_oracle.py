@@ -217,6 +217,22 @@ def test_oaa_steps_equal_direct_definition(shape, Lmode):
     assert relerr(oaa.backward_filter(x, g, n, L), oracle.conv_backward_filter(x, g, n)) < 1e-12
 
 
+@pytest.mark.parametrize("shape", SHAPES)
+def test_oaa_backward_independent_of_window_side(shape):
+    # windows of side 2n (what the GPU path stores) and L give the results of
+    # the 2n-1 windows, which equal the direct definition
+    x, w, g = _rand(shape, 16)
+    N, n = shape[3], shape[4]
+    L = oaa.fft_size(n)
+    for side in (2 * n, L):
+        if side > L:
+            continue
+        assert relerr(oaa.backward_data(g, w, N, L, side), oracle.conv_backward_data(g, w, N)) < 1e-12
+        assert relerr(oaa.backward_filter(x, g, n, L, side), oracle.conv_backward_filter(x, g, n)) < 1e-12
+    with pytest.raises(ValueError):
+        oaa.window_spectra(g, n, N, L, side=2 * n - 2)
+
+
 def test_oaa_fft_size_and_block_grid():
     assert [oaa.fft_size(n) for n in (1, 2, 3, 5, 7, 8, 9, 16, 17, 32)] == \
         [2, 4, 8, 16, 16, 16, 32, 32, 64, 64]

@@ -145,7 +145,7 @@ def test_stage_spectra_match_oracle_steps(gpu_lib):
     torch.cuda.synchronize()
     Gh = plan.region(binding.REGION_G_SPECTRUM).cpu().numpy().reshape(L, V, K, B, T, T)
     dXh = plan.region(binding.REGION_PRODUCT).cpu().numpy()[:F * C * B * T * T].reshape(L, V, C, B, T, T)
-    Go = oaa_oracle.window_spectra(g, n, N, L)
+    Go = oaa_oracle.window_spectra(g, n, N, L, side=2 * n)   # the library stores 2n x 2n windows
     assert relerr(Gh.transpose(3, 2, 4, 5, 0, 1), Go) < TOL
     assert relerr(dXh.transpose(3, 2, 4, 5, 0, 1), oaa_oracle.backward_data_product(Go, Wo)) < TOL
     plan.backward_filter(None, None)

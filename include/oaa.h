@@ -91,9 +91,7 @@ typedef enum {
 typedef enum {
   OAA_CONTRACTION_AUTO = 0,  /* library's choice by shape                        */
   OAA_CONTRACTION_VALU = 1,  /* LDS-tiled FMA on the vector ALUs                 */
-  OAA_CONTRACTION_MFMA = 2,  /* fp32 matrix cores, 4 real products per complex one */
-  OAA_CONTRACTION_MFMA3 = 3  /* fp32 matrix cores, 3 real products per complex one
-                                (Gauss: re = t1 - t2, im = t3 - t1 - t2)        */
+  OAA_CONTRACTION_MFMA = 2   /* fp32 matrix cores                                */
 } oaa_contraction_t;
 
 /* Stages of the three passes, for per-stage timing. */

@@ -176,11 +176,7 @@ __device__ __forceinline__ unsigned xcd_local_order(unsigned w, unsigned nwg) {
 
 // MB x NB blocks of 16 x 16 per wave, waves in a 2 x 2 grid:
 // tile (32*MB) x (32*NB) complex per workgroup.
-// G3: three real products per complex product (Gauss): with
-//   t1 = sum ar*br, t2 = sum ai*bi, t3 = sum (ar+ai)*(br+bi),
-// re = t1 - t2 and im = t3 - t1 - t2; otherwise four (re += ar*br - ai*bi,
-// im += ar*bi + ai*br).
-template <int MB, int NB, bool G3, bool AT, bool AC, bool BT, bool BC>
+template <int MB, int NB, bool AT, bool AC, bool BT, bool BC>
 __global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
   constexpr int TM = 32 * MB, TN = 32 * NB;
   constexpr int LDA = TM + 16, LDB = TN + 16;  // padded LDS row strides (floats)
@@ -205,15 +201,13 @@ __global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
   const float2* A = p.A + size_t(f) * p.a_fstride;
   const float2* B = p.B + size_t(f) * p.b_fstride;
 
-  // 4M: accr = re, acci = im. G3: accr = t1, acci = t2, acc3 = t3.
-  floatx4 accr[MB][NB], acci[MB][NB], acc3[G3 ? MB : 1][G3 ? NB : 1];
+  floatx4 accr[MB][NB], acci[MB][NB];
 #pragma unroll
   for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       accr[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
       acci[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-      if (G3) acc3[G3 ? i : 0][G3 ? j : 0] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
   const int lr = lane & 15;  // operand row (A) / column (B) within a 16-block
@@ -248,29 +242,6 @@ __global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
         br[j] = Bsr[buf][kr][wn + 16 * j + lr];
         bi[j] = Bsi[buf][kr][wn + 16 * j + lr];
       }
-      if (G3) {
-        float as[MB], bs[NB];
-#pragma unroll
-        for (int i = 0; i < MB; ++i) as[i] = ar[i] + ai[i];
-#pragma unroll
-        for (int j = 0; j < NB; ++j) bs[j] = br[j] + bi[j];
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            accr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i], br[j], accr[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ai[i], bi[j], acci[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acc3[G3 ? i : 0][G3 ? j : 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                as[i], bs[j], acc3[G3 ? i : 0][G3 ? j : 0], 0, 0, 0);
-      } else {
         // four independent sweeps, so that dependent accumulations are
         // MB*NB instructions apart
 #pragma unroll
@@ -293,7 +264,6 @@ __global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
 #pragma unroll
           for (int j = 0; j < NB; ++j)
             acci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ai[i], br[j], acci[i][j], 0, 0, 0);
-      }
     }
     if (more) {
       sa.template store<LDA>(Asr[buf ^ 1], Asi[buf ^ 1], AC);
@@ -313,35 +283,26 @@ __global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm + 16 * i + 4 * lk + r;
-        float re = accr[i][j][r], im = acci[i][j][r];
-        if (G3) {
-          const float t1 = re, t2 = im;
-          re = t1 - t2;
-          im = acc3[G3 ? i : 0][G3 ? j : 0][r] - t1 - t2;
-        }
-        if (m < p.M && nn < p.N) Cm[size_t(m) * p.ldc + nn] = make_float2(re, im);
+        if (m < p.M && nn < p.N) Cm[size_t(m) * p.ldc + nn] = make_float2(accr[i][j][r], acci[i][j][r]);
       }
     }
 }
 
-template <int MB, int NB, bool G3, bool AT, bool AC, bool BT, bool BC>
+template <int MB, int NB, bool AT, bool AC, bool BT, bool BC>
 hipError_t launch_mfma_shape(const GemmParams& p, hipStream_t s) {
   const unsigned tiles = unsigned(((p.M + 32 * MB - 1) / (32 * MB)) * ((p.N + 32 * NB - 1) / (32 * NB)));
   const unsigned nwg = tiles * unsigned(p.nsplit) * unsigned(p.F);
-  hipLaunchKernelGGL((cgemm_mfma_kernel<MB, NB, G3, AT, AC, BT, BC>), dim3(nwg), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((cgemm_mfma_kernel<MB, NB, AT, AC, BT, BC>), dim3(nwg), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
 // Row tile of 96 when that wastes less than 128 does (e.g. 96 channels).
-// The three-product form keeps three accumulators, so it uses 12 blocks per
-// wave (96 x 128 or 128 x 96) to stay within two waves per SIMD.
-template <bool G3, bool AT, bool AC, bool BT, bool BC>
+template <bool AT, bool AC, bool BT, bool BC>
 hipError_t launch_mfma(const GemmParams& p, hipStream_t s) {
   const long waste128 = (long)((p.M + 127) / 128) * 128 - p.M;
   const long waste96 = (long)((p.M + 95) / 96) * 96 - p.M;
-  if (waste96 < waste128) return launch_mfma_shape<3, 4, G3, AT, AC, BT, BC>(p, s);
-  if (G3) return launch_mfma_shape<4, 3, G3, AT, AC, BT, BC>(p, s);
-  return launch_mfma_shape<4, 4, G3, AT, AC, BT, BC>(p, s);
+  if (waste96 < waste128) return launch_mfma_shape<3, 4, AT, AC, BT, BC>(p, s);
+  return launch_mfma_shape<4, 4, AT, AC, BT, BC>(p, s);
 }
 
 template <int TM, int TN, class Kern>
@@ -365,18 +326,13 @@ hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-template <bool G3>
-hipError_t launch_mfma_any(const GemmParams& p, hipStream_t s) {
+hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s) {
   if (p.kchunk % kKC != 0 && p.nsplit > 1) return hipErrorInvalidValue;
-  if (p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<G3, true, false, false, false>(p, s);
-  if (!p.a_trans && p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<G3, false, true, false, false>(p, s);
-  if (!p.a_trans && p.a_conj && p.b_trans && !p.b_conj) return launch_mfma<G3, false, true, true, false>(p, s);
+  if (p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<true, false, false, false>(p, s);
+  if (!p.a_trans && p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<false, true, false, false>(p, s);
+  if (!p.a_trans && p.a_conj && p.b_trans && !p.b_conj) return launch_mfma<false, true, true, false>(p, s);
   return hipErrorInvalidValue;
 }
-
-hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s) { return launch_mfma_any<false>(p, s); }
-
-hipError_t launch_cgemm_mfma3(const GemmParams& p, hipStream_t s) { return launch_mfma_any<true>(p, s); }
 
 bool mfma_preferred(const GemmParams& p) { return p.M >= 32 && p.N >= 32 && p.Kr >= 16; }
 

@@ -128,6 +128,139 @@ __global__ void __launch_bounds__(kMaxThreads) tile_rfft2_kernel(TileFwdParams p
 }
 
 // ---------------------------------------------------------------------------
+// Gradient windows: window (P, Q) is the 2n x 2n region of the framed plane
+// (plane rows/cols shifted by -off) starting at (P n, Q n). A workgroup walks
+// down the window rows [pb, pe) of one plane for a run of window columns.
+// Consecutive window rows share n input rows, so the input sits in a ring of
+// 2n rows in LDS (framed row a in ring row a mod 2n) and only the n new rows
+// are loaded per step, prefetched into registers while the current windows
+// are transformed.
+//
+// LDS: ring [2n][Wp] floats, then zbuf [TQ][TS] float2 (row transforms,
+// rows [0, ROWS)).
+template <int L, bool ZH>
+__global__ void __launch_bounds__(kMaxThreads) window_rfft2_kernel(WindowParams p) {
+  constexpr int V = L / 2 + 1;
+  constexpr int ROWS = ZH ? L / 2 : L;
+  constexpr int S = ZH ? L / 2 : L;
+  constexpr int PAIRS = (ROWS + 1) / 2;
+  constexpr int PF = L < 16 ? L : 16;
+  extern __shared__ float smem[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int n = p.n, T = p.T, H = p.H, R = 2 * n;
+  const int TS = odd_at_least(2 * PAIRS * V);
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
+  const int chunk = int(wg % p.nchunk);
+  const unsigned rest = wg / p.nchunk;
+  const int grp = int(rest % p.ngroups);
+  const unsigned plane = rest / p.ngroups;
+  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
+  const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
+  const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
+  const int W = (nq + 1) * n;                  // framed columns [q0 n, q0 n + W)
+  const int Wp = (p.TQ - 1) * n + L;           // row stride: window reads stay inside the row
+  float* ring = smem;                                                               // [2n][Wp]
+  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R) * Wp));  // [TQ][TS]
+  const float* src = p.src + size_t(plane) * H * H;
+  const size_t tiles_per_ch = size_t(p.n_img) * T * T;
+  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
+  const size_t ustride = size_t(V) * fstride;
+  float2* out_base = p.dst + size_t(ch) * tiles_per_ch + size_t(img) * T * T + q0;
+  const int col0 = q0 * n - p.off;
+
+  // ring rows of window row pb: framed rows [pb n, pb n + 2n); clear the padding
+  for (int i = tid; i < R * Wp; i += nthr) ring[i] = 0.f;
+  __syncthreads();
+  {
+    const int a0 = pb * n, s0 = a0 % R;
+    // rows a0 .. a0+2n-1 land in ring rows s0 .. (wrapping at 2n)
+    stage_rows(ring + s0 * Wp, Wp, src, H, a0 - p.off, col0, R - s0, W);
+    if (s0 > 0) stage_rows(ring, Wp, src, H, a0 + (R - s0) - p.off, col0, s0, W);
+  }
+  RowPrefetch<PF> pf;
+  const bool use_pf = OAA_WINDOW_PREFETCH && RowPrefetch<PF>::fits(n, W);
+
+  for (int P = pb; P < pe; ++P) {
+    const int a0 = P * n;
+    const int slot0 = a0 % R;
+    __syncthreads();
+    const bool next = P + 1 < pe;
+    if (next && use_pf) pf.load(src, H, a0 + R - p.off, col0, n, W);
+    // pass 1: window rows two at a time; pairs past the window write zero rows
+    for (int task = tid; task < PAIRS * nq; task += nthr) {
+      const int q = task % nq, pr = task / nq;
+      const int r0 = 2 * pr;
+      float2* zt = zbuf + q * TS + r0 * V;
+      if (r0 >= R) {
+#pragma unroll
+        for (int k = 0; k < 2 * V; ++k) zt[k] = make_float2(0.f, 0.f);
+        continue;
+      }
+      int sa = slot0 + r0;
+      if (sa >= R) sa -= R;
+      int sb = sa + 1;
+      if (sb >= R) sb -= R;
+      const float* row_a = ring + sa * Wp + q * n;
+      const float* row_b = ring + sb * Wp + q * n;
+      float zr[L], zi[L];
+#pragma unroll
+      for (int s = 0; s < L; ++s) {
+        if (s < S) {
+          const float x0 = row_a[s], x1 = row_b[s];
+          const bool in = s < R;
+          zr[s] = in ? x0 : 0.f;
+          zi[s] = in ? x1 : 0.f;
+        } else {
+          zr[s] = 0.f;
+          zi[s] = 0.f;
+        }
+      }
+      float2 X0[V], X1[V];
+      rfft_pair<L, ZH>(zr, zi, X0, X1);
+#pragma unroll
+      for (int k = 0; k < V; ++k) {
+        zt[k] = X0[k];
+        zt[V + k] = X1[k];
+      }
+    }
+    __syncthreads();
+    // the ring rows of framed rows [a0, a0 + n) (ring rows [slot0, slot0 + n),
+    // slot0 being 0 or n) are free now: bring in framed rows [a0 + 2n, a0 + 3n)
+    if (next) {
+      if (use_pf)
+        pf.store(ring + slot0 * Wp, Wp, n, W);
+      else
+        stage_rows(ring + slot0 * Wp, Wp, src, H, a0 + R - p.off, col0, n, W);
+    }
+    // pass 2: complex columns, bin-major stores of window row P
+    float2* out = out_base + size_t(P) * T;
+    for (int task = tid; task < V * nq; task += nthr) {
+      const int q = task % nq, v = task / nq;
+      const float2* zt = zbuf + q * TS + v;
+      float re[L], im[L];
+#pragma unroll
+      for (int r = 0; r < L; ++r) {
+        if (r < ROWS) {
+          const float2 z = zt[r * V];
+          re[r] = z.x;
+          im[r] = z.y;
+        } else {
+          re[r] = 0.f;
+          im[r] = 0.f;
+        }
+      }
+      fft_dif<L, -1, ZH>(re, im);
+      float2* o = out + size_t(v) * fstride + q;
+#pragma unroll
+      for (int u = 0; u < L; ++u) {
+        const int pos = bitrev(u, L);
+        o[u * ustride] = make_float2(re[pos], im[pos]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Inverse column pass shared by the inverse kernels: for the tiles at
 // in[q], q < nq (bin f at in[q + f * fstride], plus nsplit - 1 partial sums
 // spaced split_stride apart), transform every column v and keep rows
@@ -345,7 +478,7 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
     const size_t Wp = size_t(tq - 1) * p.pitch + p.R + L;
     return even_floats(size_t(p.R + 1) * Wp) * 4 + size_t(TS) * tq * 8;
   };
-  int nchunk = 1;
+  int nchunk = (p.T + OAA_FWD_TQ_MAX - 1) / OAA_FWD_TQ_MAX;
   while (nchunk < p.T && lds_for((p.T + nchunk - 1) / nchunk) > kLdsBudget) ++nchunk;
   p.TQ = (p.T + nchunk - 1) / nchunk;
   p.nchunk = (p.T + p.TQ - 1) / p.TQ;
@@ -354,6 +487,33 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
   const int tasks = std::max(PAIRS * p.TQ, V * p.TQ);
   const long nwg = long(p.n_img) * p.n_ch * p.T * p.nchunk;
   hipLaunchKernelGGL((tile_rfft2_kernel<L, ZH>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
+  return hipGetLastError();
+}
+
+template <int L, bool ZH>
+hipError_t launch_window_L(WindowParams p, hipStream_t s) {
+  constexpr int V = L / 2 + 1;
+  constexpr int ROWS = ZH ? L / 2 : L;
+  constexpr int PAIRS = (ROWS + 1) / 2;
+  const int TS = odd_at_least(2 * PAIRS * V);
+  auto lds_for = [&](int tq) {
+    const size_t Wp = size_t(tq - 1) * p.n + L;
+    return even_floats(size_t(2 * p.n) * Wp) * 4 + size_t(TS) * tq * 8;
+  };
+  int nchunk = (p.T + OAA_WINDOW_TQ_MAX - 1) / OAA_WINDOW_TQ_MAX;
+  while (nchunk < p.T && lds_for((p.T + nchunk - 1) / nchunk) > kLdsBudget) ++nchunk;
+  p.TQ = (p.T + nchunk - 1) / nchunk;
+  p.nchunk = (p.T + p.TQ - 1) / p.TQ;
+  const size_t lds = lds_for(p.TQ);
+  if (lds > kLdsBudget) return hipErrorInvalidConfiguration;
+  const long planes = long(p.n_img) * p.n_ch;
+  int ng = 1;
+  if (planes < 2048) ng = int(std::min<long>(p.T, (2048 + planes - 1) / planes));
+  p.SPW = (p.T + ng - 1) / ng;
+  p.ngroups = (p.T + p.SPW - 1) / p.SPW;
+  const int tasks = std::max(PAIRS * p.TQ, V * p.TQ);
+  const long nwg = planes * p.ngroups * p.nchunk;
+  hipLaunchKernelGGL((window_rfft2_kernel<L, ZH>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }
 
@@ -394,7 +554,7 @@ hipError_t launch_crop_L(CropParams p, hipStream_t s) {
   const size_t per_tile = size_t(TS) * 8;
   const long tiles = long(p.n_img) * p.T * p.T;
   // enough consecutive tiles for 128-byte reads, as LDS allows
-  long tq = std::min<long>(long(kLdsBudget / per_tile), 64);
+  long tq = std::min<long>(long(kLdsBudget / per_tile), OAA_CROP_TQ_MAX);
   if (tq > tiles) tq = tiles;
   const long nchunk = (tiles + tq - 1) / tq;
   p.TQ = int((tiles + nchunk - 1) / nchunk);
@@ -417,6 +577,19 @@ hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s) {
     case 16: return zh ? launch_fwd_L<16, true>(p, s) : launch_fwd_L<16, false>(p, s);
     case 32: return zh ? launch_fwd_L<32, true>(p, s) : launch_fwd_L<32, false>(p, s);
     case 64: return zh ? launch_fwd_L<64, true>(p, s) : launch_fwd_L<64, false>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s) {
+  const bool zh = 4 * p.n <= L;
+  switch (L) {
+    case 2: return zh ? launch_window_L<2, true>(p, s) : launch_window_L<2, false>(p, s);
+    case 4: return zh ? launch_window_L<4, true>(p, s) : launch_window_L<4, false>(p, s);
+    case 8: return zh ? launch_window_L<8, true>(p, s) : launch_window_L<8, false>(p, s);
+    case 16: return zh ? launch_window_L<16, true>(p, s) : launch_window_L<16, false>(p, s);
+    case 32: return zh ? launch_window_L<32, true>(p, s) : launch_window_L<32, false>(p, s);
+    case 64: return zh ? launch_window_L<64, true>(p, s) : launch_window_L<64, false>(p, s);
     default: return hipErrorInvalidValue;
   }
 }

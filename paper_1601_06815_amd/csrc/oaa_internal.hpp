@@ -52,11 +52,10 @@ struct CropParams {
   int TQ, nchunk;
 };
 
-// Gradient windows through block spectra (overlap by n in the frequency
-// domain): window (P, Q) is the 2n x 2n region of the framed plane starting
-// at (P*pitch - off, Q*pitch - off) of plane coordinates, pitch = n; its
-// spectrum goes to dst like TileFwdParams'.
-struct WindowFoldParams {
+// Gradient windows: window (P, Q) is the 2n x 2n region of the plane starting
+// at row P*n - off, column Q*n - off (zero outside the plane); its spectrum
+// goes to dst like TileFwdParams'.
+struct WindowParams {
   const float* src;  // [n_img][n_ch][H][H]
   float2* dst;       // [F][n_ch][n_img * T * T]
   int n_img, n_ch;
@@ -98,11 +97,10 @@ struct GemmParams {
 hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
 hipError_t launch_irfft2_overlap_add(int L, const OverlapAddParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
-hipError_t launch_window_fold_rfft2(int L, const WindowFoldParams& p, hipStream_t s);
+hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s);
 hipError_t launch_irfft2_fold_crop(int L, const FoldCropParams& p, hipStream_t s);
 hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s);
 hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s);
-hipError_t launch_cgemm_mfma3(const GemmParams& p, hipStream_t s);
 // Shape rule of the automatic choice between the two contractions.
 bool mfma_preferred(const GemmParams& p);
 

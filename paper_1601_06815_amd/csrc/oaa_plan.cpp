@@ -148,8 +148,8 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
 
 oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
   // window (P,Q) of the zero-framed gradient: g[P*n + r - (n-1)][Q*n + s - (n-1)],
-  // r, s < 2n, formed from n x n block spectra
-  oaa::WindowFoldParams t{};
+  // r, s < 2n
+  oaa::WindowParams t{};
   t.src = g;
   t.dst = region(p, OAA_REGION_G_SPECTRUM);
   t.n_img = p->B;
@@ -159,7 +159,7 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
   t.off = p->n - 1;
   t.T = p->T;
   oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient window spectra",
-                          [&] { return oaa::launch_window_fold_rfft2(p->L, t, s); });
+                          [&] { return oaa::launch_window_rfft2(p->L, t, s); });
   if (st == OAA_OK) p->g_valid = true;
   return st;
 }
@@ -169,11 +169,7 @@ oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipSt
   oaa_contraction_t c = p->contraction;
   if (c == OAA_CONTRACTION_AUTO) c = oaa::mfma_preferred(g) ? OAA_CONTRACTION_MFMA : OAA_CONTRACTION_VALU;
   return timed(p, stage, s, what, [&] {
-    switch (c) {
-      case OAA_CONTRACTION_MFMA: return oaa::launch_cgemm_mfma(g, s);
-      case OAA_CONTRACTION_MFMA3: return oaa::launch_cgemm_mfma3(g, s);
-      default: return oaa::launch_cgemm_valu(g, s);
-    }
+    return c == OAA_CONTRACTION_MFMA ? oaa::launch_cgemm_mfma(g, s) : oaa::launch_cgemm_valu(g, s);
   });
 }
 
@@ -344,8 +340,7 @@ oaa_status_t oaa_plan_bind_workspace(oaa_plan_t plan, void* dev_ptr, size_t byte
 
 oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which) {
   if (oaa_status_t st = check_plan(plan, false)) return st;
-  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA &&
-      which != OAA_CONTRACTION_MFMA3)
+  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA)
     return fail(OAA_ERR_INVALID_ARG, "unknown contraction %d", (int)which);
   plan->contraction = which;
   return OAA_OK;

@@ -5,6 +5,24 @@
 
 #include "fft_core.hpp"
 
+// Launch-shape defaults (tiles per workgroup along a block row, register
+// prefetch of the next rows); overridable at build time for tuning sweeps.
+#ifndef OAA_WINDOW_TQ_MAX
+#define OAA_WINDOW_TQ_MAX 64
+#endif
+#ifndef OAA_WINDOW_PREFETCH
+#define OAA_WINDOW_PREFETCH 1
+#endif
+#ifndef OAA_FOLD_TQ_MAX
+#define OAA_FOLD_TQ_MAX 64
+#endif
+#ifndef OAA_FWD_TQ_MAX
+#define OAA_FWD_TQ_MAX 64
+#endif
+#ifndef OAA_CROP_TQ_MAX
+#define OAA_CROP_TQ_MAX 64
+#endif
+
 namespace oaa {
 namespace tile {
 

@@ -126,7 +126,7 @@ def test_null_and_workspace_validation(lib):
         assert lib.oaa_conv_backward_filter(h, fake, None, fake, None) == 4   # no cached window spectra
         assert lib.oaa_conv_backward_filter(h, fake, fake, None, None) == 1
         assert lib.oaa_plan_set_contraction(h, 7) == 1
-        assert lib.oaa_plan_set_contraction(h, 3) == 0
+        assert lib.oaa_plan_set_contraction(h, 3) == 1
         assert lib.oaa_plan_set_contraction(h, 1) == 0
         assert lib.oaa_plan_region(h, 4, None, None) == 1
         g = binding.Geometry()

@@ -73,8 +73,7 @@ def test_small_layers_all_passes(gpu_lib, shape):
     check_whole(x, w, g)
 
 
-@pytest.mark.parametrize("contraction", [binding.CONTRACTION_VALU, binding.CONTRACTION_MFMA,
-                                         binding.CONTRACTION_MFMA3], ids=["valu", "mfma", "mfma3"])
+@pytest.mark.parametrize("contraction", [binding.CONTRACTION_VALU, binding.CONTRACTION_MFMA], ids=["valu", "mfma"])
 @pytest.mark.parametrize("shape", [(2, 70, 66, 12, 2), (1, 5, 130, 20, 3), (3, 33, 17, 21, 4),
                                    (1, 130, 140, 9, 3), (2, 16, 32, 40, 16), (1, 3, 64, 30, 7)],
                          ids=lambda s: "x".join(map(str, s)))

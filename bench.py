@@ -120,7 +120,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layer", default="large128")
-    ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma"])
+    ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma", "narrow"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--stages-out", default=None, help="also write per-stage timings as JSON here")
@@ -154,7 +154,7 @@ def main():
     x, w, g = make_inputs(ly, seed=0)
     print(f"[bench] inputs for {ly.name} drawn in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
     which = {"auto": binding.CONTRACTION_AUTO, "valu": binding.CONTRACTION_VALU,
-             "mfma": binding.CONTRACTION_MFMA}[args.contraction]
+             "mfma": binding.CONTRACTION_MFMA, "narrow": binding.CONTRACTION_NARROW}[args.contraction]
     plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which)
     geo = plan.geometry
     xd, wd, gd = (torch.from_numpy(a).to(dev) for a in (x, w, g))

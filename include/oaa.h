@@ -91,7 +91,8 @@ typedef enum {
 typedef enum {
   OAA_CONTRACTION_AUTO = 0,  /* library's choice by shape                        */
   OAA_CONTRACTION_VALU = 1,  /* LDS-tiled FMA on the vector ALUs                 */
-  OAA_CONTRACTION_MFMA = 2   /* fp32 matrix cores                                */
+  OAA_CONTRACTION_MFMA = 2,  /* fp32 matrix cores                                */
+  OAA_CONTRACTION_NARROW = 3 /* streaming, for C <= 4 input channels only       */
 } oaa_contraction_t;
 
 /* Stages of the three passes, for per-stage timing. */

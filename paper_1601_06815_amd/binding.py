@@ -16,7 +16,7 @@ OAA_OK = 0
 STATUS = {0: "OAA_OK", 1: "OAA_ERR_INVALID_ARG", 2: "OAA_ERR_UNSUPPORTED",
           3: "OAA_ERR_NO_WORKSPACE", 4: "OAA_ERR_NO_CACHE", 5: "OAA_ERR_HIP"}
 REGION_W_SPECTRUM, REGION_X_SPECTRUM, REGION_G_SPECTRUM, REGION_PRODUCT = 0, 1, 2, 3
-CONTRACTION_AUTO, CONTRACTION_VALU, CONTRACTION_MFMA = 0, 1, 2
+CONTRACTION_AUTO, CONTRACTION_VALU, CONTRACTION_MFMA, CONTRACTION_NARROW = 0, 1, 2, 3
 STAGES = ["w_spectrum", "x_spectrum", "g_spectrum", "fwd_product", "fwd_inverse",
           "bwd_data_product", "bwd_data_inverse", "bwd_filter_product", "bwd_filter_inverse"]
 

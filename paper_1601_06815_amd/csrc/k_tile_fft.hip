@@ -1,16 +1,17 @@
 // Tiling + zero-padding + 2-D real FFT of blocks and windows, and the
-// inverse transforms with overlap-add or crop (arXiv:1601.06815, Section 2:
-// block division, padding, per-block transforms, overlap by n-1 and add).
+// inverse transforms with crop (arXiv:1601.06815, Section 2: block division,
+// padding, per-block transforms; Section 3.2: the two backward convolutions).
 //
 // Forward: one workgroup handles a run of consecutive tiles along one block
 // row of one plane. The plane rows that the run covers are staged in LDS with
 // coalesced loads; pass 1 (one lane per pair of tile rows) transforms rows,
 // pass 2 (one lane per tile column) transforms columns and writes the spectra
 // bin-major with consecutive tiles at consecutive addresses.
-// Inverse: the same two passes in the opposite order. The overlap-add keeps a
-// ring of 2n output rows per plane in LDS: every tile adds its own n columns
-// directly, parks its n-1 overhanging columns, and a second step adds the
-// overhangs, so every output pixel is summed in a fixed order and written once.
+// Gradient windows: one workgroup walks down the block rows of a plane with
+// a ring of 2n input rows in LDS, reading each row of g once.
+// Inverse with crop (error propagation, weight gradient): the two passes in
+// the opposite order, keeping the top-left n x n of every tile. The forward
+// inverse with overlap-add is in k_fold_fft.hip.
 //
 // LDS intermediates are stored tile-major with an odd per-tile stride (in
 // complex elements), so every index inside a tile is a compile-time offset
@@ -300,118 +301,6 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
 }
 
 // ---------------------------------------------------------------------------
-// Inverse + overlap-add + valid crop
-//
-// LDS: ring [2n][Wacc] floats (absolute output row a lives in ring row
-// a mod 2n), then zbuf [TQ][TS] float2, TS >= L * V odd, holding the column
-// transforms of rows [0, L-1) (>= 2n-1 rows); after the row pass a tile's row
-// r area holds the n-1 columns of that row which overhang the next tile.
-template <int L>
-__global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_add_kernel(OverlapAddParams p) {
-  constexpr int V = L / 2 + 1;
-  constexpr int RT = L - 1;
-  extern __shared__ float smem[];
-  const int tid = threadIdx.x, nthr = blockDim.x;
-  const int n = p.n, T = p.T, M = p.M, R = 2 * n - 1, RING = 2 * n;
-  const int Wacc = T * n + n - 1;
-  const int TS = odd_at_least(L * V);
-  float* ring = smem;                                                                  // [2n][Wacc]
-  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(RING) * Wacc));  // [TQ][TS]
-  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
-  const int grp = int(wg % p.ngroups);
-  const unsigned plane = wg / p.ngroups;
-  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
-  const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
-  const size_t tiles_per_ch = size_t(p.n_img) * T * T;
-  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
-  const float2* in = p.src + size_t(ch) * tiles_per_ch + size_t(img) * T * T;
-  float* out = p.dst + size_t(plane) * M * M;
-  const float scale = 1.0f / float(L * L);
-
-  for (int i = tid; i < RING * Wacc; i += nthr) ring[i] = 0.f;
-  __syncthreads();
-
-  // block row pb-1 is recomputed (not written) to supply the rows that
-  // overlap into block row pb
-  for (int strip = (pb > 0 ? pb - 1 : 0); strip < pe; ++strip) {
-    const int a0 = strip * n;           // first absolute output row of this block row
-    const int slot0 = a0 % RING;        // its ring row
-    for (int q0 = 0; q0 < T; q0 += p.TQ) {
-      const int nq = min(p.TQ, T - q0);
-      inverse_columns<L, RT>(in + size_t(strip) * T + q0, fstride, 1, 0, nq, TS, zbuf);
-      __syncthreads();
-      // rows: own n columns straight into the ring, overhang parked in zbuf
-      for (int task = tid; task < n * nq; task += nthr) {
-        const int q = task % nq, pr = task / nq;
-        const int r0 = 2 * pr;
-        float2* zt = zbuf + q * TS + r0 * V;
-        float2 A[V], Bv[V];
-#pragma unroll
-        for (int v = 0; v < V; ++v) {
-          A[v] = zt[v];
-          Bv[v] = zt[V + v];  // row 2n-1 (when r0 + 1 == 2n-1) is read but discarded
-        }
-        float zr[L], zi[L];
-        irfft_pair<L>(A, Bv, zr, zi);
-        const bool has1 = r0 + 1 < R;
-        int s0 = slot0 + r0;
-        if (s0 >= RING) s0 -= RING;
-        int s1 = s0 + 1;
-        if (s1 >= RING) s1 -= RING;
-        float* d0 = ring + s0 * Wacc + (q0 + q) * n;
-        float* d1 = ring + s1 * Wacc + (q0 + q) * n;
-        float* o0 = reinterpret_cast<float*>(zt);      // overhang of row r0
-        float* o1 = reinterpret_cast<float*>(zt + V);  // overhang of row r0 + 1
-#pragma unroll
-        for (int s = 0; s < L; ++s) {
-          const int pos = bitrev(s, L);
-          const float t0 = zr[pos] * scale, t1 = zi[pos] * scale;
-          if (s < n) {
-            d0[s] += t0;
-            if (has1) d1[s] += t1;
-          } else if (s < R) {
-            o0[s - n] = t0;
-            if (has1) o1[s - n] = t1;
-          }
-        }
-      }
-      __syncthreads();
-      // overhangs: tile q's columns [n, 2n-1) land on columns [(q+1)n, (q+1)n + n-1)
-      const int ov = nq * (n - 1);
-      for (int c = tid; c < ov; c += nthr) {
-        const int q = c / (n - 1), s = c - q * (n - 1);
-        const float* o = reinterpret_cast<const float*>(zbuf + q * TS) + s;
-        float* dcol = ring + (q0 + q + 1) * n + s;
-        int slot = slot0;
-        for (int r = 0; r < R; ++r) {
-          dcol[slot * Wacc] += o[r * 2 * V];
-          if (++slot == RING) slot = 0;
-        }
-      }
-      __syncthreads();
-    }
-    // rows [a0, a0 + n) are complete: write the valid part, then clear them
-    int slot = slot0;
-    for (int r = 0; r < n; ++r) {
-      const float* row = ring + slot * Wacc;
-      const int i = a0 + r - (n - 1);
-      if (strip >= pb && i >= 0 && i < M) {
-        for (int j = tid; j < M; j += nthr) out[size_t(i) * M + j] = row[j + n - 1];
-      }
-      if (++slot == RING) slot = 0;
-    }
-    __syncthreads();
-    slot = slot0;
-    for (int r = 0; r < n; ++r) {
-      float* row = ring + slot * Wacc;
-      for (int j = tid; j < Wacc; j += nthr) row[j] = 0.f;
-      if (++slot == RING) slot = 0;
-    }
-    __syncthreads();
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Inverse + top-left n x n crop, scattered to the blocks of the output planes.
 // A workgroup takes TQ consecutive tiles of one channel (they may span block
 // rows and images), so its spectrum reads are contiguous.
@@ -518,43 +407,16 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
 }
 
 template <int L>
-hipError_t launch_oa_L(OverlapAddParams p, hipStream_t s) {
-  constexpr int V = L / 2 + 1;
-  const int TS = odd_at_least(L * V);
-  const size_t ring_bytes = even_floats(size_t(2 * p.n) * (size_t(p.T) * p.n + p.n - 1)) * 4;
-  const size_t per_tile = size_t(TS) * 8;
-  size_t budget = kLdsBudget;
-  if (ring_bytes + per_tile > budget) budget = 160 * 1024;  // gfx950: 160 KiB per workgroup
-  if (ring_bytes + per_tile > budget) return hipErrorInvalidConfiguration;
-  int tq = int(std::min<size_t>(p.T, (budget - ring_bytes) / per_tile));
-  const int nchunk = (p.T + tq - 1) / tq;
-  p.TQ = (p.T + nchunk - 1) / nchunk;
-  p.nchunk = nchunk;
-  const long planes = long(p.n_img) * p.n_ch;
-  int ngroups = 1;
-  if (planes < 2048) ngroups = int(std::min<long>(p.T, (2048 + planes - 1) / planes));
-  p.SPW = (p.T + ngroups - 1) / ngroups;
-  p.ngroups = (p.T + p.SPW - 1) / p.SPW;
-  const size_t lds = ring_bytes + per_tile * p.TQ;
-  if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&irfft2_overlap_add_kernel<L>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-    if (e != hipSuccess) return e;
-  }
-  const int tasks = std::max(V * p.TQ, p.n * p.TQ);
-  hipLaunchKernelGGL(irfft2_overlap_add_kernel<L>, dim3(unsigned(planes * p.ngroups)),
-                     dim3(pick_threads(tasks)), lds, s, p);
-  return hipGetLastError();
-}
-
-template <int L>
 hipError_t launch_crop_L(CropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   const int TS = odd_at_least((L / 2 + 1) * V);
   const size_t per_tile = size_t(TS) * 8;
   const long tiles = long(p.n_img) * p.T * p.T;
-  // enough consecutive tiles for 128-byte reads, as LDS allows
+  // runs of consecutive tiles (128-byte reads) as LDS allows, shortened to
+  // keep about 2048 workgroups when there are few tiles (the weight gradient)
   long tq = std::min<long>(long(kLdsBudget / per_tile), OAA_CROP_TQ_MAX);
+  const long want = (long(p.n_ch) * tiles + 2047) / 2048;
+  if (want < tq) tq = std::max<long>(want, 1);
   if (tq > tiles) tq = tiles;
   const long nchunk = (tiles + tq - 1) / tq;
   p.TQ = int((tiles + nchunk - 1) / nchunk);
@@ -590,18 +452,6 @@ hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s) {
     case 16: return zh ? launch_window_L<16, true>(p, s) : launch_window_L<16, false>(p, s);
     case 32: return zh ? launch_window_L<32, true>(p, s) : launch_window_L<32, false>(p, s);
     case 64: return zh ? launch_window_L<64, true>(p, s) : launch_window_L<64, false>(p, s);
-    default: return hipErrorInvalidValue;
-  }
-}
-
-hipError_t launch_irfft2_overlap_add(int L, const OverlapAddParams& p, hipStream_t s) {
-  switch (L) {
-    case 2: return launch_oa_L<2>(p, s);
-    case 4: return launch_oa_L<4>(p, s);
-    case 8: return launch_oa_L<8>(p, s);
-    case 16: return launch_oa_L<16>(p, s);
-    case 32: return launch_oa_L<32>(p, s);
-    case 64: return launch_oa_L<64>(p, s);
     default: return hipErrorInvalidValue;
   }
 }

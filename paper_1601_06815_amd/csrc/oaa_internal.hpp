@@ -28,17 +28,6 @@ struct TileFwdParams {
   int nchunk;        // ceil(T / TQ)
 };
 
-// Output spectra -> inverse transform -> overlap-add (pitch n, tile support
-// 2n-1) -> valid crop of side M into dst[n_img][n_ch][M][M].
-struct OverlapAddParams {
-  const float2* src;  // [F][n_ch][n_img * T * T]
-  float* dst;         // [n_img][n_ch][M][M]
-  int n_img, n_ch;
-  int M, n, T;
-  int TQ, nchunk;     // tiles per column-pass chunk
-  int SPW, ngroups;   // block rows per workgroup, ceil(T / SPW)
-};
-
 // Spectra (optionally the sum of `nsplit` partial spectra spaced
 // `split_stride` elements apart) -> inverse transform -> top-left n x n of
 // each tile written to block (P, Q) of dst[n_img][n_ch][H][H], clipped to H.
@@ -95,13 +84,18 @@ struct GemmParams {
 };
 
 hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
-hipError_t launch_irfft2_overlap_add(int L, const OverlapAddParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
 hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s);
 hipError_t launch_irfft2_fold_crop(int L, const FoldCropParams& p, hipStream_t s);
 hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s);
 hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s);
-// Shape rule of the automatic choice between the two contractions.
+// Streaming contraction for few input channels (C <= kNarrowMaxC), for the
+// three orientations above; the weight-gradient form writes nsplit partial
+// sums like the tiled kernels.
+constexpr int kNarrowMaxC = 4;
+hipError_t launch_cgemm_narrow(const GemmParams& p, hipStream_t s);
+bool narrow_supported(const GemmParams& p);
+// Shape rule of the automatic choice between the tiled contractions.
 bool mfma_preferred(const GemmParams& p);
 
 }  // namespace oaa

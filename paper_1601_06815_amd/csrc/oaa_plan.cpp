@@ -167,9 +167,18 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
 oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipStream_t s, const char* what) {
   g.F = p->F;
   oaa_contraction_t c = p->contraction;
-  if (c == OAA_CONTRACTION_AUTO) c = oaa::mfma_preferred(g) ? OAA_CONTRACTION_MFMA : OAA_CONTRACTION_VALU;
+  if (c == OAA_CONTRACTION_AUTO)
+    c = oaa::mfma_preferred(g)      ? OAA_CONTRACTION_MFMA
+        : oaa::narrow_supported(g) ? OAA_CONTRACTION_NARROW
+                                   : OAA_CONTRACTION_VALU;
+  if (c == OAA_CONTRACTION_NARROW && !oaa::narrow_supported(g))
+    return fail(OAA_ERR_UNSUPPORTED, "%s: the streaming contraction needs C <= %d", what, oaa::kNarrowMaxC);
   return timed(p, stage, s, what, [&] {
-    return c == OAA_CONTRACTION_MFMA ? oaa::launch_cgemm_mfma(g, s) : oaa::launch_cgemm_valu(g, s);
+    switch (c) {
+      case OAA_CONTRACTION_MFMA: return oaa::launch_cgemm_mfma(g, s);
+      case OAA_CONTRACTION_NARROW: return oaa::launch_cgemm_narrow(g, s);
+      default: return oaa::launch_cgemm_valu(g, s);
+    }
   });
 }
 
@@ -209,30 +218,36 @@ oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n)
   if (BP > kMaxInt || (long long)N * N > kMaxInt || (long long)B * C > kMaxInt || (long long)B * K > kMaxInt ||
       (long long)K * C > kMaxInt)
     return fail(OAA_ERR_UNSUPPORTED, "layer too large for 32-bit tile and plane indices");
-  // the overlap-add keeps one block row of output (2n-1 rows) in LDS
-  {
-    const long long acc = (long long)(2 * n - 1) * ((long long)T * n + n - 1) * 4;
-    const long long tile = (long long)(2 * n - 1) * (L / 2 + 1) * 8;
-    if (acc + tile > 160 * 1024)
-      return fail(OAA_ERR_UNSUPPORTED, "one block row of output (%lld bytes) exceeds the 160 KiB LDS", acc + tile);
-  }
   const unsigned long long eW = (unsigned long long)F * C * K;
   const unsigned long long eX = (unsigned long long)F * C * BP;
   const unsigned long long eG = (unsigned long long)F * K * BP;
   if (eX > kMaxElems || eG > kMaxElems || eW > kMaxElems)
     return fail(OAA_ERR_UNSUPPORTED, "spectra exceed the addressable workspace");
 
-  // split of the weight-gradient reduction over B*P so that the contraction
-  // (96- or 128-row by 128-column tiles, two workgroups per CU) runs in at
-  // least eight rounds of 512 workgroups
-  const long long rows = ((C + 95) / 96) * 96 - C < ((C + 127) / 128) * 128 - C ? (C + 95) / 96 : (C + 127) / 128;
-  const long long tiles = rows * ((K + 127) / 128) * F;
-  long long split = tiles >= 4096 ? 1 : (4096 + tiles - 1) / tiles;
-  const long long max_split = (BP + 63) / 64;
-  if (split > max_split) split = max_split;
+  // split of the weight-gradient reduction over B*P, shared by every
+  // contraction engine (the inverse adds the partial sums):
+  //  * tiled engines: 96- or 128-row by 128-column tiles, two workgroups per
+  //    CU, at least eight rounds of 512 workgroups; chunks of 16 tiles;
+  //  * few input channels (the streaming engine): about 2048 workgroups of 64
+  //    kernels, chunks of at least 1024 tiles, a multiple of 128.
+  long long split, quantum;
+  if (C <= oaa::kNarrowMaxC) {
+    const long long groups = (long long)F * ((K + 63) / 64);
+    split = groups >= 2048 ? 1 : (2048 + groups - 1) / groups;
+    const long long max_split = (BP + 1023) / 1024;
+    if (split > max_split) split = max_split;
+    quantum = 128;
+  } else {
+    const long long rows = ((C + 95) / 96) * 96 - C < ((C + 127) / 128) * 128 - C ? (C + 95) / 96 : (C + 127) / 128;
+    const long long tiles = rows * ((K + 127) / 128) * F;
+    split = tiles >= 4096 ? 1 : (4096 + tiles - 1) / tiles;
+    const long long max_split = (BP + 63) / 64;
+    if (split > max_split) split = max_split;
+    quantum = 16;
+  }
   if (split < 1) split = 1;
   long long kchunk = (BP + split - 1) / split;
-  kchunk = (kchunk + 15) / 16 * 16;
+  kchunk = (kchunk + quantum - 1) / quantum * quantum;
   split = (BP + kchunk - 1) / kchunk;
 
   oaa_plan_s* p = new (std::nothrow) oaa_plan_s();
@@ -340,8 +355,12 @@ oaa_status_t oaa_plan_bind_workspace(oaa_plan_t plan, void* dev_ptr, size_t byte
 
 oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which) {
   if (oaa_status_t st = check_plan(plan, false)) return st;
-  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA)
+  if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA &&
+      which != OAA_CONTRACTION_NARROW)
     return fail(OAA_ERR_INVALID_ARG, "unknown contraction %d", (int)which);
+  if (which == OAA_CONTRACTION_NARROW && plan->C > oaa::kNarrowMaxC)
+    return fail(OAA_ERR_UNSUPPORTED, "the streaming contraction needs C <= %d (plan has C=%d)", oaa::kNarrowMaxC,
+                plan->C);
   plan->contraction = which;
   return OAA_OK;
 }

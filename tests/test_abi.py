@@ -126,12 +126,34 @@ def test_null_and_workspace_validation(lib):
         assert lib.oaa_conv_backward_filter(h, fake, None, fake, None) == 4   # no cached window spectra
         assert lib.oaa_conv_backward_filter(h, fake, fake, None, None) == 1
         assert lib.oaa_plan_set_contraction(h, 7) == 1
-        assert lib.oaa_plan_set_contraction(h, 3) == 1
+        assert lib.oaa_plan_set_contraction(h, 4) == 1
+        assert lib.oaa_plan_set_contraction(h, 3) == 0                    # streaming: C = 3 <= 4
         assert lib.oaa_plan_set_contraction(h, 1) == 0
         assert lib.oaa_plan_region(h, 4, None, None) == 1
         g = binding.Geometry()
         assert lib.oaa_plan_geometry(h, None) == 1
         assert lib.oaa_plan_geometry(h, ctypes.byref(g)) == 0 and g.L == 16 and g.T == 4
+    finally:
+        binding.oaa_plan_destroy(h)
+
+
+def test_streaming_contraction_needs_few_channels(lib):
+    h = binding.oaa_plan_create(1, 5, 4, 16, 3)
+    try:
+        assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_NARROW) == 2
+        assert "C <= 4" in binding.oaa_last_error_detail()
+        assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_MFMA) == 0
+    finally:
+        binding.oaa_plan_destroy(h)
+
+
+@pytest.mark.parametrize("dims,split", [((64, 3, 64, 224, 7), 15), ((2, 3, 64, 224, 7), 2), ((1, 3, 4, 32, 5), 1),
+                                        ((2, 3, 20, 100, 3), 3)])
+def test_split_for_few_channels(lib, dims, split):
+    """Few input channels: chunks of at least 1024 tiles in multiples of 128."""
+    h = binding.oaa_plan_create(*dims)
+    try:
+        assert binding.oaa_plan_geometry(h)["split"] == split
     finally:
         binding.oaa_plan_destroy(h)
 

@@ -83,6 +83,31 @@ def test_contraction_variants(gpu_lib, contraction, shape):
     check_whole(x, w, g, contraction)
 
 
+NARROW = [  # C <= 4: odd and even tile counts, K off multiples of 16, K > 64, K > 256, split reduction
+    (1, 1, 1, 9, 3),
+    (2, 2, 17, 13, 4),
+    (1, 3, 70, 30, 7),
+    (2, 4, 300, 12, 2),
+    (2, 3, 20, 100, 3),
+    (3, 3, 64, 45, 5),
+]
+
+
+@pytest.mark.parametrize("shape", NARROW, ids=lambda s: "x".join(map(str, s)))
+def test_narrow_contraction(gpu_lib, shape):
+    """The streaming contraction for few input channels, forced, against the
+    oracle; and against the tiled vector-ALU contraction on the same inputs."""
+    B, C, K, N, n = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=5 + sum(shape))
+    check_whole(x, w, g, binding.CONTRACTION_NARROW)
+    plan, y, dx, dw = run_layer(x, w, g, binding.CONTRACTION_NARROW)
+    _, y2, dx2, dw2 = run_layer(x, w, g, binding.CONTRACTION_VALU)
+    for a, b in ((y, y2), (dx, dx2), (dw, dw2)):
+        assert relerr(a, b) <= TOL
+    if plan.geometry["split"] > 1:
+        print(f"split {plan.geometry['split']}", flush=True)
+
+
 @pytest.mark.parametrize("name", ["tiny", "plane224_n3", "plane224_n5", "plane224_n8"])
 def test_named_small_layers(gpu_lib, name):
     ly = LAYERS[name]

@@ -29,9 +29,11 @@ using namespace tile;
 //
 // One workgroup per (plane, block row, run of tile columns). LDS: zbuf
 // [TQ + 1][TS] float2: column transforms (rows [0, L/2]) of tiles q0-1 ..
-// q0+nq-1 of the block row, folded along u with the block row above.
+// q0+nq-1 of the block row, folded along u with the block row above; then
+// obuf [n][TQ][n + 1] floats: the block row's output, written to HBM row by
+// row with consecutive lanes on consecutive pixels.
 template <int L>
-__global__ void __launch_bounds__(kMaxThreads) irfft2_fold_crop_kernel(FoldCropParams p) {
+__global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irfft2_fold_crop_kernel(FoldCropParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int RT = L / 2 + 1;
   extern __shared__ float smem[];
@@ -39,6 +41,8 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_crop_kernel(FoldCropP
   const int n = p.n, T = p.T, M = p.M;
   const int TS = odd_at_least(RT * V);
   float2* zbuf = reinterpret_cast<float2*>(smem);
+  float* obuf = smem + size_t(p.TQ + 1) * TS * 2;
+  const int OS = n | 1;  // obuf stride between tiles, odd
   const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
   const unsigned rest = wg / p.nchunk;
@@ -80,7 +84,8 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_crop_kernel(FoldCropP
     }
   }
   __syncthreads();
-  // fold along v with the left neighbour, inverse row transforms, crop
+  // fold along v with the left neighbour, inverse row transforms, crop to the
+  // tile's n x n output block in LDS
   const int npair = (n + 1) >> 1;
   for (int task = tid; task < npair * nq; task += nthr) {
     const int q = task % nq, pr = task / nq;
@@ -96,19 +101,31 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_crop_kernel(FoldCropP
     }
     float zr[L], zi[L];
     irfft_pair<L>(A, Bv, zr, zi);
-    const int i0 = strip * n + r0 - p.off;
-    const int j0 = (q0 + q) * n - p.off;
-    const bool w0 = i0 >= 0 && i0 < M;
-    const bool w1 = r0 + 1 < n && i0 + 1 >= 0 && i0 + 1 < M;
+    float* o0 = obuf + (size_t(r0) * nq + q) * OS;
+    float* o1 = o0 + size_t(nq) * OS;
+    const bool has1 = r0 + 1 < n;
 #pragma unroll
     for (int s = 0; s < L / 2; ++s) {
-      const int j = j0 + s;
-      if (s < n && j >= 0 && j < M) {
+      if (s < n) {
         const int pos = bitrev(s, L);
-        if (w0) out[size_t(i0) * M + j] = zr[pos] * scale;
-        if (w1) out[size_t(i0 + 1) * M + j] = zi[pos] * scale;
+        o0[s] = zr[pos] * scale;
+        if (has1) o1[s] = zi[pos] * scale;
       }
     }
+  }
+  __syncthreads();
+  // the block row's valid output: rows strip*n - off + [0, n), columns
+  // q0*n - off + [0, nq*n), both clipped to [0, M)
+  const int W = nq * n;
+  const int i0 = strip * n - p.off, j0 = q0 * n - p.off;
+  const int rb = max(0, -i0), re_ = min(n, M - i0);
+  const int cb = max(0, -j0), ce = min(W, M - j0);
+  const int wr = ce - cb;
+  if (wr <= 0 || re_ <= rb) return;
+  for (int e = tid; e < (re_ - rb) * wr; e += nthr) {
+    const int r = rb + e / wr, c = cb + e % wr;
+    const int q = c / n, s = c - q * n;
+    out[size_t(i0 + r) * M + j0 + c] = obuf[(size_t(r) * nq + q) * OS + s];
   }
 }
 
@@ -119,8 +136,10 @@ template <int L>
 hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   const int TS = odd_at_least((L / 2 + 1) * V);
-  const size_t per_tile = size_t(TS) * 8;
-  int tq = std::min<int>(std::min<int>(p.T, OAA_FOLD_TQ_MAX), int(kLdsBudget / per_tile) - 1);
+  const size_t zb = size_t(TS) * 8;                 // column transforms of one tile
+  const size_t ob = size_t(p.n) * (p.n | 1) * 4;    // output block of one tile
+  int tq = std::min<int>(std::min<int>(p.T, OAA_FOLD_TQ_MAX),
+                         kLdsBudget > zb ? int((kLdsBudget - zb) / (zb + ob)) : 0);
   if (tq < 1) return hipErrorInvalidConfiguration;
   const int nchunk = (p.T + tq - 1) / tq;
   p.TQ = (p.T + nchunk - 1) / nchunk;
@@ -128,7 +147,7 @@ hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   p.SPW = 1;
   p.ngroups = p.T;
   const long planes = long(p.n_img) * p.n_ch;
-  const size_t lds = per_tile * (p.TQ + 1);
+  const size_t lds = zb * (p.TQ + 1) + ob * p.TQ;
   const int tasks = std::max((p.TQ + 1) * V, ((p.n + 1) / 2) * p.TQ);
   const long nwg = planes * p.T * p.nchunk;
   hipLaunchKernelGGL(irfft2_fold_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);

@@ -35,7 +35,7 @@ using namespace tile;
 // TS >= ROWS * V (rounded up to whole row pairs) odd, ROWS = L/2 when
 // windows fill at most half a tile (ZH), else L. Row r of tile q's row transform is at zbuf[q * TS + r * V + v].
 template <int L, bool ZH>
-__global__ void __launch_bounds__(kMaxThreads) tile_rfft2_kernel(TileFwdParams p) {
+__global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_TILE)) tile_rfft2_kernel(TileFwdParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int ROWS = ZH ? L / 2 : L;
   constexpr int S = ZH ? L / 2 : L;         // row entries that may be nonzero
@@ -52,7 +52,7 @@ __global__ void __launch_bounds__(kMaxThreads) tile_rfft2_kernel(TileFwdParams p
   const int nq = min(p.TQ, p.T - q0);
   const int R = p.R, pitch = p.pitch;
   const int W = (nq - 1) * pitch + R;
-  const int Wp = (p.TQ - 1) * pitch + R + L;  // row stride: reads past W stay inside the row
+  const int Wp = bank_stride((p.TQ - 1) * pitch + R + L);  // reads past W stay inside the row
   const int TS = odd_at_least(2 * PAIRS * V);
   float* img_s = smem;                                                                 // [R+1][Wp]
   float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R + 1) * Wp));  // [TQ][TS]
@@ -140,7 +140,7 @@ __global__ void __launch_bounds__(kMaxThreads) tile_rfft2_kernel(TileFwdParams p
 // LDS: ring [2n][Wp] floats, then zbuf [TQ][TS] float2 (row transforms,
 // rows [0, ROWS)).
 template <int L, bool ZH>
-__global__ void __launch_bounds__(kMaxThreads) window_rfft2_kernel(WindowParams p) {
+__global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) window_rfft2_kernel(WindowParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int ROWS = ZH ? L / 2 : L;
   constexpr int S = ZH ? L / 2 : L;
@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(kMaxThreads) window_rfft2_kernel(WindowParams 
   const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
   const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
   const int W = (nq + 1) * n;                  // framed columns [q0 n, q0 n + W)
-  const int Wp = (p.TQ - 1) * n + L;           // row stride: window reads stay inside the row
+  const int Wp = bank_stride((p.TQ - 1) * n + L);  // window reads stay inside the row
   float* ring = smem;                                                               // [2n][Wp]
   float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R) * Wp));  // [TQ][TS]
   const float* src = p.src + size_t(plane) * H * H;
@@ -305,7 +305,7 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
 // A workgroup takes TQ consecutive tiles of one channel (they may span block
 // rows and images), so its spectrum reads are contiguous.
 template <int L>
-__global__ void __launch_bounds__(kMaxThreads) irfft2_crop_kernel(CropParams p) {
+__global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irfft2_crop_kernel(CropParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int RT = L / 2;  // rows kept from the column transforms (>= n)
   extern __shared__ float smem[];
@@ -364,7 +364,7 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
   constexpr int PAIRS = (ROWS + 1) / 2;
   const int TS = odd_at_least(2 * PAIRS * V);
   auto lds_for = [&](int tq) {
-    const size_t Wp = size_t(tq - 1) * p.pitch + p.R + L;
+    const size_t Wp = size_t(bank_stride((tq - 1) * p.pitch + p.R + L));
     return even_floats(size_t(p.R + 1) * Wp) * 4 + size_t(TS) * tq * 8;
   };
   int nchunk = (p.T + OAA_FWD_TQ_MAX - 1) / OAA_FWD_TQ_MAX;
@@ -386,7 +386,7 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   constexpr int PAIRS = (ROWS + 1) / 2;
   const int TS = odd_at_least(2 * PAIRS * V);
   auto lds_for = [&](int tq) {
-    const size_t Wp = size_t(tq - 1) * p.n + L;
+    const size_t Wp = size_t(bank_stride((tq - 1) * p.n + L));
     return even_floats(size_t(2 * p.n) * Wp) * 4 + size_t(TS) * tq * 8;
   };
   int nchunk = (p.T + OAA_WINDOW_TQ_MAX - 1) / OAA_WINDOW_TQ_MAX;

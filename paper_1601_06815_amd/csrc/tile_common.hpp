@@ -23,8 +23,26 @@
 #define OAA_CROP_TQ_MAX 64
 #endif
 
+// Minimum waves per SIMD asked of the register allocator, per transform
+// kernel, for L <= 32 (1: no constraint). L = 64 always takes what it needs.
+#ifndef OAA_WAVES_TILE
+#define OAA_WAVES_TILE 1
+#endif
+#ifndef OAA_WAVES_WINDOW
+#define OAA_WAVES_WINDOW 1
+#endif
+#ifndef OAA_WAVES_FOLD
+#define OAA_WAVES_FOLD 1
+#endif
+#ifndef OAA_WAVES_CROP
+#define OAA_WAVES_CROP 1
+#endif
+
 namespace oaa {
 namespace tile {
+
+template <int L>
+constexpr int fft_waves(int want) { return L <= 32 ? want : 1; }
 
 constexpr int kMaxThreads = 256;
 constexpr size_t kLdsBudget = 60 * 1024;
@@ -35,6 +53,9 @@ inline int pick_threads(int tasks) {
 }
 
 __host__ __device__ inline int odd_at_least(int v) { return v | 1; }
+// Smallest row stride >= w that is 1 mod 32 (words): lanes that read the same
+// column of different LDS rows then fall in different banks.
+__host__ __device__ inline int bank_stride(int w) { return w + ((33 - (w & 31)) & 31); }
 __host__ __device__ inline size_t even_floats(size_t n) { return (n + 1) & ~size_t(1); }
 
 // Workgroups are dispatched round-robin over the 8 XCDs, each with its own L2.

@@ -45,20 +45,42 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_TILE)) til
   const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
   const unsigned rest = wg / p.nchunk;
-  const int strip = int(rest % p.T);
-  const unsigned plane = rest / p.T;
-  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
-  const int q0 = chunk * p.TQ;
-  const int nq = min(p.TQ, p.T - q0);
   const int R = p.R, pitch = p.pitch;
+  int strip, img, ch, q0, nq;
+  if (p.gather) {  // kernels q0 .. q0+nq-1 of channel ch, side by side
+    strip = 0;
+    img = 0;
+    ch = int(rest);
+    q0 = chunk * p.TQ;
+    nq = min(p.TQ, p.n_img - q0);
+  } else {  // tiles q0 .. q0+nq-1 of block row `strip` of plane (img, ch)
+    strip = int(rest % p.T);
+    const unsigned plane = rest / p.T;
+    img = int(plane / p.n_ch);
+    ch = int(plane % p.n_ch);
+    q0 = chunk * p.TQ;
+    nq = min(p.TQ, p.T - q0);
+  }
   const int W = (nq - 1) * pitch + R;
   const int Wp = bank_stride((p.TQ - 1) * pitch + R + L);  // reads past W stay inside the row
   const int TS = odd_at_least(2 * PAIRS * V);
   float* img_s = smem;                                                                 // [R+1][Wp]
   float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R + 1) * Wp));  // [TQ][TS]
 
-  const float* src = p.src + size_t(plane) * p.H * p.H;
-  stage_rows(img_s, Wp, src, p.H, strip * pitch - p.off, q0 * pitch - p.off, R, W);
+  if (p.gather) {
+    const size_t pstride = size_t(p.n_ch) * p.H * p.H;
+    const float* src = p.src + size_t(q0) * pstride + size_t(ch) * p.H * p.H;
+    for (int e = tid; e < nq * R * R; e += nthr) {
+      const int q = e / (R * R), rs = e - q * R * R;
+      const int r = rs / R, c = rs - r * R;
+      img_s[r * Wp + q * pitch + c] = src[size_t(q) * pstride + rs];
+    }
+    // pitch == R: the row has no gaps; clear what the row reads may touch past W
+    for (int e = tid; e < R * (Wp - W); e += nthr) img_s[(e / (Wp - W)) * Wp + W + e % (Wp - W)] = 0.f;
+  } else {
+    const float* src = p.src + (size_t(img) * p.n_ch + ch) * p.H * p.H;
+    stage_rows(img_s, Wp, src, p.H, strip * pitch - p.off, q0 * pitch - p.off, R, W);
+  }
   for (int c = tid; c < Wp; c += nthr) img_s[R * Wp + c] = 0.f;
   __syncthreads();
 
@@ -310,8 +332,12 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
   constexpr int RT = L / 2;  // rows kept from the column transforms (>= n)
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
+  const int n = p.n, H = p.H;
   const int TS = odd_at_least((RT + 1) * V);
-  float2* zbuf = reinterpret_cast<float2*>(smem);  // [TQ][TS]
+  const int OS = n | 1;  // obuf stride between tiles, odd
+  float2* zbuf = reinterpret_cast<float2*>(smem);                   // [TQ][TS]
+  float* obuf = smem + size_t(p.TQ) * TS * 2;                       // [n][TQ][OS]
+  int* tbase = reinterpret_cast<int*>(obuf + size_t(n) * p.TQ * OS);  // [TQ] x 3
   const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
   const int ch = int(wg / p.nchunk);
@@ -319,8 +345,16 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
   const int tiles = p.n_img * P;
   const int t0 = chunk * p.TQ;
   const int nq = min(p.TQ, tiles - t0);
-  const int n = p.n, H = p.H;
   const size_t fstride = size_t(p.n_ch) * tiles;
+  // per tile: offset of its block in the output plane set, valid rows and columns
+  for (int q = tid; q < nq; q += nthr) {
+    const int t = t0 + q;
+    const int img = t / P, pp = t - img * P;
+    const int prow = pp / p.T, qcol = pp - prow * p.T;
+    tbase[q] = prow * n * H + qcol * n;
+    tbase[p.TQ + q] = img;
+    tbase[2 * p.TQ + q] = (min(n, H - prow * n) << 16) | min(n, H - qcol * n);
+  }
   inverse_columns<L, RT>(p.src + size_t(ch) * tiles + t0, fstride, p.nsplit, p.split_stride, nq, TS, zbuf);
   __syncthreads();
   const float scale = 1.0f / float(L * L);
@@ -337,19 +371,28 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
     }
     float zr[L], zi[L];
     irfft_pair<L>(A, Bv, zr, zi);
-    const int t = t0 + q;
-    const int img = t / P, pp = t - img * P;
-    const int prow = pp / p.T, qcol = pp - prow * p.T;
-    const int gr0 = prow * n + r0, gc0 = qcol * n;
-    float* o = p.dst + (size_t(img) * p.n_ch + ch) * H * H;
-    const bool w0 = gr0 < H, w1 = r0 + 1 < n && gr0 + 1 < H;
+    float* o0 = obuf + (size_t(r0) * p.TQ + q) * OS;
+    float* o1 = o0 + size_t(p.TQ) * OS;
+    const bool has1 = r0 + 1 < n;
 #pragma unroll
     for (int s = 0; s < L / 2; ++s) {
-      if (s < n && gc0 + s < H) {
+      if (s < n) {
         const int pos = bitrev(s, L);
-        if (w0) o[size_t(gr0) * H + gc0 + s] = zr[pos] * scale;
-        if (w1) o[size_t(gr0 + 1) * H + gc0 + s] = zi[pos] * scale;
+        o0[s] = zr[pos] * scale;
+        if (has1) o1[s] = zi[pos] * scale;
       }
+    }
+  }
+  __syncthreads();
+  // row r of every tile, tiles in order: neighbouring tiles of a block row
+  // are neighbours in the output row
+  for (int e = tid; e < n * nq * n; e += nthr) {
+    const int s = e % n, rest = e / n;
+    const int q = rest % nq, r = rest / nq;
+    const int lim = tbase[2 * p.TQ + q];
+    if (r < (lim >> 16) && s < (lim & 0xffff)) {
+      float* o = p.dst + (size_t(tbase[p.TQ + q]) * p.n_ch + ch) * H * H;
+      o[tbase[q] + r * H + s] = obuf[(size_t(r) * p.TQ + q) * OS + s];
     }
   }
 }
@@ -367,14 +410,17 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
     const size_t Wp = size_t(bank_stride((tq - 1) * p.pitch + p.R + L));
     return even_floats(size_t(p.R + 1) * Wp) * 4 + size_t(TS) * tq * 8;
   };
-  int nchunk = (p.T + OAA_FWD_TQ_MAX - 1) / OAA_FWD_TQ_MAX;
-  while (nchunk < p.T && lds_for((p.T + nchunk - 1) / nchunk) > kLdsBudget) ++nchunk;
-  p.TQ = (p.T + nchunk - 1) / nchunk;
-  p.nchunk = (p.T + p.TQ - 1) / p.TQ;
+  // tiles along a row: a block row of T tiles, or (gather) the n_img kernels
+  const int run = p.gather ? p.n_img : p.T;
+  const int tq_max = p.gather ? 16 : OAA_FWD_TQ_MAX;  // 16 kernels: 128-byte spectrum stores
+  int nchunk = (run + tq_max - 1) / tq_max;
+  while (nchunk < run && lds_for((run + nchunk - 1) / nchunk) > kLdsBudget) ++nchunk;
+  p.TQ = (run + nchunk - 1) / nchunk;
+  p.nchunk = (run + p.TQ - 1) / p.TQ;
   const size_t lds = lds_for(p.TQ);
   if (lds > kLdsBudget) return hipErrorInvalidConfiguration;
   const int tasks = std::max(PAIRS * p.TQ, V * p.TQ);
-  const long nwg = long(p.n_img) * p.n_ch * p.T * p.nchunk;
+  const long nwg = p.gather ? long(p.n_ch) * p.nchunk : long(p.n_img) * p.n_ch * p.T * p.nchunk;
   hipLaunchKernelGGL((tile_rfft2_kernel<L, ZH>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }
@@ -410,7 +456,8 @@ template <int L>
 hipError_t launch_crop_L(CropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   const int TS = odd_at_least((L / 2 + 1) * V);
-  const size_t per_tile = size_t(TS) * 8;
+  // column transforms, output block and three tile descriptors per tile
+  const size_t per_tile = size_t(TS) * 8 + size_t(p.n) * (p.n | 1) * 4 + 3 * 4;
   const long tiles = long(p.n_img) * p.T * p.T;
   // runs of consecutive tiles (128-byte reads) as LDS allows, shortened to
   // keep about 2048 workgroups when there are few tiles (the weight gradient)

@@ -26,6 +26,8 @@ struct TileFwdParams {
   int T;             // blocks per side
   int TQ;            // tiles per workgroup chunk along a block row
   int nchunk;        // ceil(T / TQ)
+  int gather;        // 1: kernel planes (T = 1, R = H): a workgroup takes TQ
+                     // consecutive images (kernels) of one channel
 };
 
 // Spectra (optionally the sum of `nsplit` partial spectra spaced

@@ -123,6 +123,7 @@ oaa_status_t run_filter_fft(oaa_plan_t p, const float* w, hipStream_t s) {
   t.off = 0;
   t.R = p->n;
   t.T = 1;
+  t.gather = 1;
   oaa_status_t st = timed(p, OAA_STAGE_W_SPECTRUM, s, "kernel spectra",
                           [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
   if (st == OAA_OK) p->w_valid = true;

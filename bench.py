@@ -34,20 +34,22 @@ PROFILE_DIR = os.path.join(ROOT, "profiles")
 def stage_work(ly, geo):
     """Algorithmic bytes (HBM) and flops per launch of each stage."""
     B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
-    F, P, S = geo["F"], geo["P"], geo["split"]
+    F, P, S, L = geo["F"], geo["P"], geo["split"], geo["L"]
     BP = B * P
     cplx = 8
-    prod_flops = 8.0 * BP * C * K * F
+    # the contractions compute the bins that are not conjugates of others
+    Fu = (L // 2 + 1) ** 2 + (L // 2 - 1) ** 2
+    prod_flops = 8.0 * BP * C * K * Fu
     return {
         "w_spectrum": dict(bytes=K * C * n * n * 4 + F * C * K * cplx),
         "x_spectrum": dict(bytes=B * C * N * N * 4 + F * C * BP * cplx),
         "g_spectrum": dict(bytes=B * K * M * M * 4 + F * K * BP * cplx),
-        "fwd_product": dict(flops=prod_flops, bytes=(F * C * K + F * C * BP + F * K * BP) * cplx),
-        "fwd_inverse": dict(bytes=F * K * BP * cplx + B * K * M * M * 4),
-        "bwd_data_product": dict(flops=prod_flops, bytes=(F * C * K + F * K * BP + F * C * BP) * cplx),
-        "bwd_data_inverse": dict(bytes=F * C * BP * cplx + B * C * N * N * 4),
-        "bwd_filter_product": dict(flops=prod_flops, bytes=(F * C * BP + F * K * BP + S * F * C * K) * cplx),
-        "bwd_filter_inverse": dict(bytes=S * F * C * K * cplx + K * C * n * n * 4),
+        "fwd_product": dict(flops=prod_flops, bytes=(Fu * C * K + Fu * C * BP + Fu * K * BP) * cplx),
+        "fwd_inverse": dict(bytes=Fu * K * BP * cplx + B * K * M * M * 4),
+        "bwd_data_product": dict(flops=prod_flops, bytes=(Fu * C * K + Fu * K * BP + Fu * C * BP) * cplx),
+        "bwd_data_inverse": dict(bytes=Fu * C * BP * cplx + B * C * N * N * 4),
+        "bwd_filter_product": dict(flops=prod_flops, bytes=(Fu * C * BP + Fu * K * BP + S * Fu * C * K) * cplx),
+        "bwd_filter_inverse": dict(bytes=S * Fu * C * K * cplx + K * C * n * n * 4),
     }
 
 

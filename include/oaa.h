@@ -84,7 +84,10 @@ typedef enum {
   OAA_REGION_G_SPECTRUM = 2, /* [F][K][B*P]      upstream-gradient window spectra */
   OAA_REGION_PRODUCT = 3     /* after forward: [F][K][B*P] output spectra;
                                 after backward_data: [F][C][B*P];
-                                after backward_filter: [split][F][C][K] partial sums */
+                                after backward_filter: [split][F][C][K] partial sums.
+                                Bins (u, v) with u > L/2 and v in {0, L/2} are
+                                not written: they are the conjugates of bins
+                                (L-u, v), the spectra being Hermitian there. */
 } oaa_region_t;
 
 /* Contraction implementation (the per-bin complex matrix product). */

@@ -2,7 +2,8 @@
 // Section 2: the Hadamard product of block and kernel spectra, summed over the
 // C channels of the layer; Section 3.2 for the two backward products).
 //
-// For every bin f the three passes are complex matrix products:
+// For every bin f (the unique bins only, see unique_bin) the three passes are
+// complex matrix products:
 //   forward          Yhat[f]  (K x BP) = What[f]^T   (K x C)  * Xhat[f] (C x BP)
 //   backward_data    dXhat[f] (C x BP) = conj What[f] (C x K)  * Ghat[f] (K x BP)
 //   backward_filter  dWhat[f] (C x K)  = conj Xhat[f] (C x BP) * Ghat[f]^T (BP x K)
@@ -80,7 +81,7 @@ struct TileCoords {
 template <int TM, int TN>
 __device__ __forceinline__ TileCoords tile_coords(const GemmParams& p) {
   TileCoords t;
-  t.f = blockIdx.z;
+  t.f = unique_bin(blockIdx.z, p.L);
   t.split = blockIdx.y;
   const int tiles_n = (p.N + TN - 1) / TN;
   t.m0 = (blockIdx.x / tiles_n) * TM;
@@ -194,7 +195,7 @@ __global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
   const int tm = lw % tiles_m;
   lw /= tiles_m;
   const int split = lw % p.nsplit;
-  const int f = lw / p.nsplit;
+  const int f = unique_bin(int(lw / p.nsplit), p.L);
   const int m0 = tm * TM, n0 = tn * TN;
   const int k_begin = split * p.kchunk;
   const int k_end = min(p.Kr, k_begin + p.kchunk);

@@ -65,6 +65,12 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
     const bool up = live && strip > 0;
     const float2* cur = in + size_t(strip) * T + (live ? Qt : 0) + size_t(v) * fstride;
     const float2* abv = cur - (up ? T : 0);
+    // Columns v = 0 and v = L/2 hold no products in rows u > L/2: there the
+    // folded column h is Hermitian, so with g = h on rows [0, L/2] (rows 0 and
+    // L/2 halved) and zero elsewhere, h = g + conj(g mirrored) and the
+    // inverse of h is 2 Re(inverse of g).
+    const bool mir = v == 0 || v == L / 2;
+    const float edge = mir ? 0.5f : 1.f;
     float re[L], im[L];
 #pragma unroll
     for (int u = 0; u < L; ++u) {
@@ -72,15 +78,24 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
       const float2 a = abv[u * ustride];
       const float2 f = cmad(live ? c : make_float2(0.f, 0.f), twiddle<L, +1>(n * u),
                             up ? a : make_float2(0.f, 0.f));
-      re[u] = f.x;
-      im[u] = f.y;
+      if (u > L / 2) {
+        re[u] = mir ? 0.f : f.x;
+        im[u] = mir ? 0.f : f.y;
+      } else if (u == 0 || u == L / 2) {
+        re[u] = f.x * edge;
+        im[u] = f.y * edge;
+      } else {
+        re[u] = f.x;
+        im[u] = f.y;
+      }
     }
     fft_dif<L, +1, false>(re, im);
+    const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
     float2* zt = zbuf + qq * TS + v;
 #pragma unroll
     for (int r = 0; r < RT; ++r) {
       const int pos = bitrev(r, L);
-      zt[r * V] = make_float2(re[pos], im[pos]);
+      zt[r * V] = make_float2(re[pos] * rs, im[pos] * is);
     }
   }
   __syncthreads();

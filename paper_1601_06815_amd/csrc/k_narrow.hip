@@ -62,7 +62,7 @@ __device__ __forceinline__ void store_vec(float2* p, const float2 (&v)[VEC]) {
 template <int CN, int VEC>
 __global__ void __launch_bounds__(kThreads) narrow_forward_kernel(GemmParams p) {
   __shared__ float2 ws[CN][kKB];
-  const int f = blockIdx.y;
+  const int f = unique_bin(blockIdx.y, p.L);
   const int K = p.M;
   const long BP = p.N;
   const float2* A = p.A + size_t(f) * p.a_fstride;
@@ -109,7 +109,7 @@ __global__ void __launch_bounds__(kThreads) narrow_forward_kernel(GemmParams p) 
 template <int CN, int VEC>
 __global__ void __launch_bounds__(kThreads) narrow_bwd_data_kernel(GemmParams p) {
   __shared__ float2 ws[CN][kKB];
-  const int f = blockIdx.y;
+  const int f = unique_bin(blockIdx.y, p.L);
   const int K = p.Kr;
   const long BP = p.N;
   const float2* A = p.A + size_t(f) * p.a_fstride;
@@ -198,7 +198,7 @@ __global__ void __launch_bounds__(kThreads) narrow_bwd_filter_kernel(GemmParams 
   const int kbase = (blockIdx.x * (kThreads / 64) + wave) * kKG;
   const int K = p.N;
   if (kbase >= K) return;  // no barrier below: idle waves may leave
-  const int f = blockIdx.z, split = blockIdx.y;
+  const int f = unique_bin(blockIdx.z, p.L), split = blockIdx.y;
   const long BP = p.Kr;
   const float2* A = p.A + size_t(f) * p.a_fstride;
   const float2* B = p.B + size_t(f) * p.b_fstride;

@@ -312,12 +312,27 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
         im[u] += z.y;
       }
     }
+    // Columns v = 0 and v = L/2 hold no products in rows u > L/2: there the
+    // column h is Hermitian, so with g = h on rows [0, L/2] (rows 0 and L/2
+    // halved) and zero elsewhere, the inverse of h is 2 Re(inverse of g).
+    const bool mir = v == 0 || v == L / 2;
+#pragma unroll
+    for (int u = 0; u < L; ++u) {
+      if (u > L / 2) {
+        re[u] = mir ? 0.f : re[u];
+        im[u] = mir ? 0.f : im[u];
+      } else if (u == 0 || u == L / 2) {
+        re[u] *= mir ? 0.5f : 1.f;
+        im[u] *= mir ? 0.5f : 1.f;
+      }
+    }
     fft_dif<L, +1, false>(re, im);
+    const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
     float2* zt = zbuf + q * TS + v;
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
       const int pos = bitrev(r, L);
-      zt[r * V] = make_float2(re[pos], im[pos]);
+      zt[r * V] = make_float2(re[pos] * rs, im[pos] * is);
     }
   }
 }

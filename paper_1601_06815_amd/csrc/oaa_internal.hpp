@@ -72,6 +72,22 @@ struct FoldCropParams {
 // B + f*b_fstride + (b_trans ? n*ldb + kk : kk*ldb + n). With nsplit > 1 the
 // reduction is split into ranges of kchunk and split s writes its partial
 // product to Cmat + s*c_sstride.
+// Frequency bins of the half spectrum: f = u * (L/2 + 1) + v, u < L, v <= L/2.
+// In the columns v = 0 and v = L/2 the spectrum of a real tile is Hermitian
+// in u, so bin (u, v) with u > L/2 is the conjugate of bin (L - u, v). The
+// contractions compute only the other unique_bins(L) bins (the products stay
+// Hermitian there); the inverse transforms read the mirrored bins instead.
+__host__ __device__ inline int unique_bins(int L) {
+  return (L / 2 + 1) * (L / 2 + 1) + (L / 2 - 1) * (L / 2 - 1);
+}
+// The fp-th computed bin: all of rows u <= L/2, then v in [1, L/2) of the rest.
+__host__ __device__ inline int unique_bin(int fp, int L) {
+  const int V = L / 2 + 1, head = (L / 2 + 1) * V;
+  if (fp < head) return fp;
+  const int t = fp - head, w = L / 2 - 1;
+  return (L / 2 + 1 + t / w) * V + 1 + t % w;
+}
+
 struct GemmParams {
   const float2* A;
   const float2* B;
@@ -81,7 +97,8 @@ struct GemmParams {
   size_t a_fstride, b_fstride, c_fstride;
   int nsplit, kchunk;
   size_t c_sstride;
-  int F;
+  int F;              // bins computed: unique_bins(L)
+  int L;              // transform side
   bool a_trans, a_conj, b_trans, b_conj;
 };
 

@@ -166,7 +166,8 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
 }
 
 oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipStream_t s, const char* what) {
-  g.F = p->F;
+  g.F = oaa::unique_bins(p->L);
+  g.L = p->L;
   oaa_contraction_t c = p->contraction;
   if (c == OAA_CONTRACTION_AUTO)
     c = oaa::mfma_preferred(g)      ? OAA_CONTRACTION_MFMA

@@ -254,3 +254,23 @@ def test_oaa_spectra_are_explicit_dft_sums():
             ref = sum(blk[r, s] * np.exp(-2j * np.pi * (u * r + v * s) / L)
                       for r in range(n) for s in range(n))
             assert abs(Xh[0, 0, P, Q, u, v] - ref) < 1e-12
+
+
+def test_half_spectrum_edge_columns_are_hermitian():
+    """Why the contractions may skip bins: for real tiles, columns v = 0 and
+    v = L/2 of the half spectrum satisfy X[L-u, v] = conj(X[u, v]), and so do
+    the bin-wise products of such spectra summed over channels."""
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((2, 3, 20, 20))
+    w = rng.standard_normal((4, 3, 5, 5))
+    L = oaa.fft_size(5)
+    Xh = oaa.block_spectra(x, 5, L)
+    Yh = oaa.forward_product(Xh, oaa.filter_spectra(w, L))
+    for S in (Xh, Yh):
+        for v in (0, L // 2):
+            col = S[..., v]
+            mirrored = np.conj(col[..., (-np.arange(L)) % L])
+            assert np.allclose(col, mirrored, rtol=0, atol=1e-12 * np.abs(col).max())
+    # the other columns are not symmetric: the skipped set is exactly these two
+    col = Xh[..., 1]
+    assert not np.allclose(col, np.conj(col[..., (-np.arange(L)) % L]))

@@ -23,6 +23,11 @@ Sections 3.2 and 3.3):
    (P*n, Q*n) of the full (T*n + n - 1)^2 result.
 7. Keep the valid region: rows and columns [n-1, N).
 
+The block pitch b (the block side) is the kernel side n in the paper. Any
+b >= n - 1 with b + n - 1 <= L gives the same result: block results then
+overlap only their immediate neighbours. The functions below take b as an
+option (default n).
+
 The two backward convolutions of Section 3.2 are written as the exact
 adjoints of steps 1-7 (the paper gives no formula for them; this is the
 reading taken): the upstream gradient g is placed at offset (n-1, n-1) in
@@ -55,22 +60,33 @@ def fft_size(n):
     return L
 
 
-def block_grid(N, n):
-    """Blocks per side, ceil(N/n) (Section 2)."""
-    return -(-N // n)
+def block_grid(N, b):
+    """Blocks per side, ceil(N/b) (Section 2, with b = n there)."""
+    return -(-N // b)
 
 
-def block_spectra(x, n, L=None):
-    """Steps 1-3 on the input: x[B,C,N,N] -> X_hat[B,C,T,T,L,L//2+1]."""
+def check_tiling(n, L, b):
+    """Block pitch b and transform side L that reproduce the convolution:
+    every block result (support b + n - 1) fits the tile and overlaps only
+    its immediate neighbours."""
+    if b < max(1, n - 1) or b + n - 1 > L:
+        raise ValueError(f"block pitch b={b} needs max(1, n-1) <= b and b + n - 1 <= L (n={n}, L={L})")
+
+
+def block_spectra(x, n, L=None, b=None):
+    """Steps 1-3 on the input: x[B,C,N,N] -> X_hat[B,C,T,T,L,L//2+1], blocks
+    of b x b (default n x n)."""
     x = np.asarray(x, dtype=np.float64)
     B, C, N, _ = x.shape
     L = fft_size(n) if L is None else L
-    T = block_grid(N, n)
-    xz = np.zeros((B, C, T * n, T * n))
+    b = n if b is None else b
+    check_tiling(n, L, b)
+    T = block_grid(N, b)
+    xz = np.zeros((B, C, T * b, T * b))
     xz[:, :, :N, :N] = x
-    blocks = xz.reshape(B, C, T, n, T, n).transpose(0, 1, 2, 4, 3, 5)   # [B,C,T,T,n,n]
+    blocks = xz.reshape(B, C, T, b, T, b).transpose(0, 1, 2, 4, 3, 5)   # [B,C,T,T,b,b]
     tiles = np.zeros((B, C, T, T, L, L))
-    tiles[..., :n, :n] = blocks
+    tiles[..., :b, :b] = blocks
     return np.fft.rfft2(tiles)
 
 
@@ -84,26 +100,28 @@ def filter_spectra(w, L=None):
     return np.fft.rfft2(tiles)
 
 
-def window_spectra(g, n, N, L=None, side=None):
+def window_spectra(g, n, N, L=None, side=None, b=None):
     """Adjoint of steps 6-7, then 2-3, on the upstream gradient:
-    g[B,K,M,M] -> G_hat[B,K,T,T,L,L//2+1]. Windows are side x side
-    (default 2n-1, the padded size of Section 3.2; any side in [2n-1, L]
-    gives the same backward results, since rows and columns past 2n-2 only
-    meet kernel taps beyond n)."""
+    g[B,K,M,M] -> G_hat[B,K,T,T,L,L//2+1]. Windows start every b (default n)
+    and are side x side (default b+n-1, for b = n the padded size 2n-1 of
+    Section 3.2; any side in [b+n-1, L] gives the same backward results,
+    since rows and columns past b+n-2 only meet kernel taps beyond n)."""
     g = np.asarray(g, dtype=np.float64)
     B, K, M, _ = g.shape
     L = fft_size(n) if L is None else L
-    side = 2 * n - 1 if side is None else side
-    if not 2 * n - 1 <= side <= L:
-        raise ValueError("window side must lie in [2n-1, L]")
-    T = block_grid(N, n)
-    S = T * n + side
+    b = n if b is None else b
+    check_tiling(n, L, b)
+    side = b + n - 1 if side is None else side
+    if not b + n - 1 <= side <= L:
+        raise ValueError("window side must lie in [b+n-1, L]")
+    T = block_grid(N, b)
+    S = T * b + side
     gfull = np.zeros((B, K, S, S))
     gfull[:, :, n - 1:n - 1 + M, n - 1:n - 1 + M] = g
     tiles = np.zeros((B, K, T, T, L, L))
     for P in range(T):
         for Q in range(T):
-            tiles[:, :, P, Q, :side, :side] = gfull[:, :, P * n:P * n + side, Q * n:Q * n + side]
+            tiles[:, :, P, Q, :side, :side] = gfull[:, :, P * b:P * b + side, Q * b:Q * b + side]
     return np.fft.rfft2(tiles)
 
 
@@ -122,45 +140,48 @@ def backward_filter_product(Gh, Xh):
     return np.einsum('bkpquv,bcpquv->kcuv', Gh, np.conj(Xh))
 
 
-def overlap_add(Yh, n, N, L):
+def overlap_add(Yh, n, N, L, b=None):
     """Steps 5-7: inverse transform, overlap by n-1 and add, valid crop.
-    Y_hat[B,K,T,T,L,L//2+1] -> y[B,K,M,M]."""
+    Y_hat[B,K,T,T,L,L//2+1] -> y[B,K,M,M]; blocks b apart (default n)."""
+    b = n if b is None else b
     B, K, T, _, _, _ = Yh.shape
-    t = np.fft.irfft2(Yh, s=(L, L))[..., :2 * n - 1, :2 * n - 1]
-    S = T * n + n - 1
+    R = b + n - 1                      # support of a block result
+    t = np.fft.irfft2(Yh, s=(L, L))[..., :R, :R]
+    S = T * b + n - 1
     yfull = np.zeros((B, K, S, S))
     for P in range(T):
         for Q in range(T):
-            yfull[:, :, P * n:P * n + 2 * n - 1, Q * n:Q * n + 2 * n - 1] += t[:, :, P, Q]
+            yfull[:, :, P * b:P * b + R, Q * b:Q * b + R] += t[:, :, P, Q]
     M = N - n + 1
     return yfull[:, :, n - 1:n - 1 + M, n - 1:n - 1 + M]
 
 
-def forward(x, w, L=None):
+def forward(x, w, L=None, b=None):
     """OaA forward convolution layer, steps 1-7."""
     n = np.asarray(w).shape[-1]
     N = np.asarray(x).shape[-1]
     L = fft_size(n) if L is None else L
-    return overlap_add(forward_product(block_spectra(x, n, L), filter_spectra(w, L)), n, N, L)
+    return overlap_add(forward_product(block_spectra(x, n, L, b), filter_spectra(w, L)), n, N, L, b)
 
 
-def backward_data(g, w, N, L=None, side=None):
+def backward_data(g, w, N, L=None, side=None, b=None):
     """OaA error propagation: window spectra times conj(kernel spectra), summed
-    over K, inverse, top-left n x n of each tile placed at its block."""
+    over K, inverse, top-left b x b of each tile placed at its block."""
     w = np.asarray(w, dtype=np.float64)
     K, C, n, _ = w.shape
     L = fft_size(n) if L is None else L
-    dXh = backward_data_product(window_spectra(g, n, N, L, side), filter_spectra(w, L))
-    blk = np.fft.irfft2(dXh, s=(L, L))[..., :n, :n]                     # [B,C,T,T,n,n]
+    b = n if b is None else b
+    dXh = backward_data_product(window_spectra(g, n, N, L, side, b), filter_spectra(w, L))
+    blk = np.fft.irfft2(dXh, s=(L, L))[..., :b, :b]                     # [B,C,T,T,b,b]
     B, _, T, _, _, _ = blk.shape
-    dx = blk.transpose(0, 1, 2, 4, 3, 5).reshape(B, C, T * n, T * n)
+    dx = blk.transpose(0, 1, 2, 4, 3, 5).reshape(B, C, T * b, T * b)
     return np.ascontiguousarray(dx[:, :, :N, :N])
 
 
-def backward_filter(x, g, n, L=None, side=None):
+def backward_filter(x, g, n, L=None, side=None, b=None):
     """OaA weight gradient: window spectra times conj(block spectra), summed
     over the batch and all blocks, inverse, top-left n x n."""
     N = np.asarray(x).shape[-1]
     L = fft_size(n) if L is None else L
-    dWh = backward_filter_product(window_spectra(g, n, N, L, side), block_spectra(x, n, L))
+    dWh = backward_filter_product(window_spectra(g, n, N, L, side, b), block_spectra(x, n, L, b))
     return np.ascontiguousarray(np.fft.irfft2(dWh, s=(L, L))[..., :n, :n])

@@ -233,6 +233,32 @@ def test_oaa_backward_independent_of_window_side(shape):
         oaa.window_spectra(g, n, N, L, side=2 * n - 2)
 
 
+@pytest.mark.parametrize("shape", SHAPES)
+def test_oaa_block_pitch_other_than_n(shape):
+    """Blocks of side b != n (the larger-block tiling) reproduce the direct
+    definition for every b in [max(1, n-1), L-n+1], in all three passes."""
+    x, w, g = _rand(shape, 17)
+    N, n = shape[3], shape[4]
+    for L in (oaa.fft_size(n), 2 * oaa.fft_size(n)):
+        for b in sorted({max(1, n - 1), n, n + 1, L // 2, L - n + 1}):
+            if b < max(1, n - 1) or b + n - 1 > L:
+                continue
+            assert relerr(oaa.forward(x, w, L, b), oracle.conv_forward(x, w)) < 1e-12, (L, b)
+            assert relerr(oaa.backward_data(g, w, N, L, b=b), oracle.conv_backward_data(g, w, N)) < 1e-12, (L, b)
+            assert relerr(oaa.backward_filter(x, g, n, L, b=b), oracle.conv_backward_filter(x, g, n)) < 1e-12, (L, b)
+            # any window side in [b+n-1, L] (the GPU path uses 2b when 2b <= L)
+            if 2 * b <= L:
+                assert relerr(oaa.backward_data(g, w, N, L, 2 * b, b), oracle.conv_backward_data(g, w, N)) < 1e-12
+
+
+def test_oaa_tiling_rejects_overlapping_neighbours():
+    x = np.zeros((1, 1, 20, 20))
+    with pytest.raises(ValueError):
+        oaa.block_spectra(x, 7, 16, 5)      # b < n - 1: results reach past the next block
+    with pytest.raises(ValueError):
+        oaa.block_spectra(x, 7, 16, 11)     # b + n - 1 > L: a block result wraps around
+
+
 def test_oaa_fft_size_and_block_grid():
     assert [oaa.fft_size(n) for n in (1, 2, 3, 5, 7, 8, 9, 16, 17, 32)] == \
         [2, 4, 8, 16, 16, 16, 32, 32, 64, 64]

@@ -123,6 +123,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layer", default="large128")
     ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma", "narrow"])
+    ap.add_argument("--tiling", default="auto", choices=["auto", "paper"],
+                    help="auto: the library's block size (fewer, larger blocks where that cuts work); "
+                         "paper: blocks of the kernel's size n")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--stages-out", default=None, help="also write per-stage timings as JSON here")
@@ -157,7 +160,7 @@ def main():
     print(f"[bench] inputs for {ly.name} drawn in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
     which = {"auto": binding.CONTRACTION_AUTO, "valu": binding.CONTRACTION_VALU,
              "mfma": binding.CONTRACTION_MFMA, "narrow": binding.CONTRACTION_NARROW}[args.contraction]
-    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which)
+    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which, tiling=args.tiling)
     geo = plan.geometry
     xd, wd, gd = (torch.from_numpy(a).to(dev) for a in (x, w, g))
     y = torch.empty((ly.B, ly.K, ly.M, ly.M), dtype=torch.float32, device=dev)
@@ -244,7 +247,7 @@ def main():
         "config": {"workload": f"{ly.name}: x[{ly.B},{ly.C},{ly.N},{ly.N}] w[{ly.K},{ly.C},{ly.n},{ly.n}] "
                                f"valid stride 1, forward + backward_data + backward_filter",
                    "B": ly.B, "C": ly.C, "K": ly.K, "N": ly.N, "n": ly.n,
-                   "L": geo["L"], "T": geo["T"], "split": geo["split"],
+                   "L": geo["L"], "block": geo["b"], "T": geo["T"], "split": geo["split"], "tiling": args.tiling,
                    "contraction": args.contraction},
         "roofline": roof,
         "stages": per_stage,

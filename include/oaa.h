@@ -62,15 +62,17 @@ typedef enum {
   OAA_ERR_HIP = 5            /* the HIP runtime reported an error             */
 } oaa_status_t;
 
-/* Sizes derived from (B, C, K, N, n). */
+/* Sizes derived from (B, C, K, N, n) and the tiling (L, b). */
 typedef struct {
   int B, C, K, N, n;
   int M;      /* output side, N - n + 1                                      */
-  int T;      /* blocks per side, ceil(N / n)                                */
+  int T;      /* blocks per side, ceil(N / b)                                */
   int P;      /* blocks per plane, T * T                                     */
-  int L;      /* transform side: smallest power of two >= 2n - 1, at least 2 */
+  int L;      /* transform side (oaa_plan_create: smallest power of two
+                 >= 2n - 1, at least 2)                                      */
   int F;      /* stored frequency bins per tile, L * (L/2 + 1)               */
   int split;  /* partial sums of the weight-gradient contraction             */
+  int b;      /* block pitch: blocks are b x b (oaa_plan_create: b = n)      */
 } oaa_geometry_t;
 
 /* Workspace regions (see oaa_plan_region). Every spectrum is complex64
@@ -112,12 +114,24 @@ typedef enum {
   OAA_STAGE_COUNT = 9
 } oaa_stage_t;
 
-/* Create a plan for x[B,C,N,N] and w[K,C,n,n]. Host-only: makes no HIP call
- * and allocates no device memory. Requires B, C, K >= 1 and 1 <= n <= N
- * (else OAA_ERR_INVALID_ARG); n <= 32 and element counts within 2^31 blocks
- * per spectrum row (else OAA_ERR_UNSUPPORTED). On success *plan is set; on
- * failure *plan is set to NULL. */
+/* Create a plan for x[B,C,N,N] and w[K,C,n,n] with the paper's tiling
+ * (Section 2: blocks of the kernel's size, b = n; transform side L the
+ * smallest power of two >= 2n - 1, Sections 3.2-3.3). Host-only: makes no
+ * HIP call and allocates no device memory. Requires B, C, K >= 1 and
+ * 1 <= n <= N (else OAA_ERR_INVALID_ARG); n <= 32 and element counts within
+ * 2^31 blocks per spectrum row (else OAA_ERR_UNSUPPORTED). On success *plan
+ * is set; on failure *plan is set to NULL. */
 oaa_status_t oaa_plan_create(oaa_plan_t* plan, int B, int C, int K, int N, int n);
+
+/* Same, with blocks of b x b (pitch b) in L x L transforms. Block results
+ * then have support b + n - 1 and the result is the same convolution for any
+ * b with max(1, n-1) <= b <= L/2 (the overlap-add is done in the frequency
+ * domain, which needs 2b <= L). L must be a power of two in [2, 64]
+ * (else OAA_ERR_UNSUPPORTED); a b outside that range is OAA_ERR_INVALID_ARG.
+ * L = b = 0 lets the library choose: L in {L0, 2 L0} (L0 the paper's side)
+ * and b by a work estimate of contraction and transforms. Larger blocks
+ * mean fewer tiles: fewer spectra to transform, store and contract. */
+oaa_status_t oaa_plan_create_tiled(oaa_plan_t* plan, int B, int C, int K, int N, int n, int L, int b);
 
 /* Release the host structure (and any timing events). NULL is a no-op.
  * Does not free the workspace. */

@@ -25,11 +25,12 @@ _c_int, _c_size, _vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
 
 
 class Geometry(ctypes.Structure):
-    _fields_ = [(k, ctypes.c_int) for k in ("B", "C", "K", "N", "n", "M", "T", "P", "L", "F", "split")]
+    _fields_ = [(k, ctypes.c_int) for k in ("B", "C", "K", "N", "n", "M", "T", "P", "L", "F", "split", "b")]
 
 
 SIGNATURES = {
     "oaa_plan_create": (_c_int, [ctypes.POINTER(_vp), _c_int, _c_int, _c_int, _c_int, _c_int]),
+    "oaa_plan_create_tiled": (_c_int, [ctypes.POINTER(_vp), _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int]),
     "oaa_plan_destroy": (_c_int, [_vp]),
     "oaa_plan_geometry": (_c_int, [_vp, ctypes.POINTER(Geometry)]),
     "oaa_plan_workspace_bytes": (_c_size, [_vp]),
@@ -86,6 +87,12 @@ def _check(st):
 def oaa_plan_create(B, C, K, N, n):
     h = _vp()
     _check(load().oaa_plan_create(ctypes.byref(h), B, C, K, N, n))
+    return h.value
+
+
+def oaa_plan_create_tiled(B, C, K, N, n, L, b):
+    h = _vp()
+    _check(load().oaa_plan_create_tiled(ctypes.byref(h), B, C, K, N, n, L, b))
     return h.value
 
 
@@ -157,9 +164,17 @@ class Plan:
     workspace tensor. Calls enqueue on torch's current stream of the tensors'
     device and return without synchronising."""
 
-    def __init__(self, B, C, K, N, n, device="cuda", contraction=CONTRACTION_AUTO):
+    def __init__(self, B, C, K, N, n, device="cuda", contraction=CONTRACTION_AUTO, tiling="paper"):
+        """tiling: "paper" (blocks of n, oaa_plan_create), "auto" (the
+        library's choice) or an (L, b) pair (oaa_plan_create_tiled)."""
         import torch
-        self.handle = oaa_plan_create(B, C, K, N, n)
+        if tiling == "paper":
+            self.handle = oaa_plan_create(B, C, K, N, n)
+        elif tiling == "auto":
+            self.handle = oaa_plan_create_tiled(B, C, K, N, n, 0, 0)
+        else:
+            L, b = tiling
+            self.handle = oaa_plan_create_tiled(B, C, K, N, n, L, b)
         self.geometry = oaa_plan_geometry(self.handle)
         self.device = torch.device(device)
         nbytes = oaa_plan_workspace_bytes(self.handle)

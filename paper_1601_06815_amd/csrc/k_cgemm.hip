@@ -23,6 +23,12 @@
 
 #include "oaa_internal.hpp"
 
+// Minimum waves per SIMD asked of the register allocator for the
+// matrix-core kernel.
+#ifndef OAA_WAVES_GEMM
+#define OAA_WAVES_GEMM 1
+#endif
+
 namespace oaa {
 
 namespace {
@@ -178,7 +184,7 @@ __device__ __forceinline__ unsigned xcd_local_order(unsigned w, unsigned nwg) {
 // MB x NB blocks of 16 x 16 per wave, waves in a 2 x 2 grid:
 // tile (32*MB) x (32*NB) complex per workgroup.
 template <int MB, int NB, bool AT, bool AC, bool BT, bool BC>
-__global__ void __launch_bounds__(kThreads) cgemm_mfma_kernel(GemmParams p) {
+__global__ void __launch_bounds__(kThreads, OAA_WAVES_GEMM) cgemm_mfma_kernel(GemmParams p) {
   constexpr int TM = 32 * MB, TN = 32 * NB;
   constexpr int LDA = TM + 16, LDB = TN + 16;  // padded LDS row strides (floats)
   __shared__ float Asr[2][kKC][LDA], Asi[2][kKC][LDA];

@@ -18,6 +18,7 @@
 
 struct oaa_plan_s {
   int B, C, K, N, n;
+  int b;  // block pitch (block side); the paper's tiling has b = n
   int M, T, P, L, F;
   int split, kchunk;
   size_t off[4];
@@ -137,9 +138,9 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
   t.n_img = p->B;
   t.n_ch = p->C;
   t.H = p->N;
-  t.pitch = p->n;
+  t.pitch = p->b;
   t.off = 0;
-  t.R = p->n;
+  t.R = p->b;
   t.T = p->T;
   oaa_status_t st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
                           [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
@@ -156,7 +157,7 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
   t.n_img = p->B;
   t.n_ch = p->K;
   t.H = p->M;
-  t.n = p->n;
+  t.n = p->b;        // window pitch; windows are 2b x 2b (>= b + n - 1 rows)
   t.off = p->n - 1;
   t.T = p->T;
   oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient window spectra",
@@ -184,6 +185,35 @@ oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipSt
   });
 }
 
+// Tiling with the least estimated work: candidate transform sides L0 (the
+// smallest power of two >= 2n-1) and 2 L0, block pitches b in
+// [max(1, n-1), L/2]. Per tile: the contraction, 8 C K flops per computed bin,
+// and four transforms per channel pair (input, gradient window, two
+// inverses), about 2.5 L^2 log2(L^2) flops each on the vector units, weighted
+// 4x against the matrix cores. Ties go to the smaller L.
+void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
+  (void)B;
+  const int L0 = pow2_at_least(2 * n - 1);
+  double best = 0;
+  L = L0;
+  b = n;
+  for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
+    int lg = 0;
+    while ((1 << lg) < Lc) ++lg;
+    const double fft = 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg);
+    const double con = 8.0 * C * K * oaa::unique_bins(Lc);
+    for (int bc = (n > 1 ? n - 1 : 1); 2 * bc <= Lc; ++bc) {
+      const double T = double((N + bc - 1) / bc);
+      const double cost = T * T * (con + fft) * (Lc > L0 ? 1.1 : 1.0);
+      if (best == 0 || cost < best) {
+        best = cost;
+        L = Lc;
+        b = bc;
+      }
+    }
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -203,17 +233,33 @@ const char* oaa_status_string(oaa_status_t status) {
 const char* oaa_last_error_detail(void) { return g_detail.c_str(); }
 
 oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n) {
+  if (n >= 1 && n <= 32) return oaa_plan_create_tiled(out, B, C, K, N, n, pow2_at_least(2 * n - 1), n);
+  return oaa_plan_create_tiled(out, B, C, K, N, n, 0, 0);
+}
+
+oaa_status_t oaa_plan_create_tiled(oaa_plan_t* out, int B, int C, int K, int N, int n, int L, int b) {
   if (!out) return fail(OAA_ERR_INVALID_ARG, "plan output pointer is NULL");
   *out = nullptr;
   if (B < 1 || C < 1 || K < 1 || N < 1 || n < 1)
     return fail(OAA_ERR_INVALID_ARG, "dimensions must be positive (B=%d C=%d K=%d N=%d n=%d)", B, C, K, N, n);
   if (n > N) return fail(OAA_ERR_INVALID_ARG, "kernel side n=%d exceeds input side N=%d", n, N);
   if (n > 32) return fail(OAA_ERR_UNSUPPORTED, "kernel side n=%d > 32 (transform side would exceed 64)", n);
+  if (L < 0 || b < 0) return fail(OAA_ERR_INVALID_ARG, "negative tiling (L=%d b=%d)", L, b);
+  if (L == 0 && b == 0) {
+    choose_tiling(B, C, K, N, n, L, b);
+  } else if (L == 0 || b == 0) {
+    return fail(OAA_ERR_INVALID_ARG, "give both L and b, or neither (L=%d b=%d)", L, b);
+  }
+  if (L < 2 || L > 64 || (L & (L - 1)))
+    return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
+  // block results (support b + n - 1) may only reach the next block, and the
+  // frequency-domain overlap-add and the 2b gradient windows need 2b <= L
+  if (b < (n > 1 ? n - 1 : 1) || 2 * b > L)
+    return fail(OAA_ERR_INVALID_ARG, "block pitch b=%d needs max(1, n-1) <= b <= L/2 (n=%d, L=%d)", b, n, L);
 
   const int M = N - n + 1;
-  const int T = (N + n - 1) / n;
+  const int T = (N + b - 1) / b;
   const long long P = (long long)T * T;
-  const int L = pow2_at_least(2 * n - 1);
   const int F = L * (L / 2 + 1);
   const long long BP = (long long)B * P;
   // index ranges the kernels keep in 32-bit integers
@@ -254,7 +300,7 @@ oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n)
 
   oaa_plan_s* p = new (std::nothrow) oaa_plan_s();
   if (!p) return fail(OAA_ERR_INVALID_ARG, "out of host memory");
-  p->B = B; p->C = C; p->K = K; p->N = N; p->n = n;
+  p->B = B; p->C = C; p->K = K; p->N = N; p->n = n; p->b = b;
   p->M = M; p->T = T; p->P = (int)P; p->L = L; p->F = F;
   p->split = (int)split;
   p->kchunk = (int)kchunk;
@@ -326,6 +372,7 @@ oaa_status_t oaa_plan_geometry(oaa_plan_t plan, oaa_geometry_t* out) {
   if (!out) return fail(OAA_ERR_INVALID_ARG, "geometry output pointer is NULL");
   out->B = plan->B; out->C = plan->C; out->K = plan->K; out->N = plan->N; out->n = plan->n;
   out->M = plan->M; out->T = plan->T; out->P = plan->P; out->L = plan->L; out->F = plan->F;
+  out->b = plan->b;
   out->split = plan->split;
   return OAA_OK;
 }
@@ -394,7 +441,7 @@ oaa_status_t oaa_conv_forward(oaa_plan_t p, const float* x, const float* w, floa
   o.src = region(p, OAA_REGION_PRODUCT);
   o.dst = y;
   o.n_img = p->B; o.n_ch = p->K;
-  o.M = p->M; o.n = p->n; o.off = p->n - 1; o.T = p->T;
+  o.M = p->M; o.n = p->b; o.off = p->n - 1; o.T = p->T;
   return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
                [&] { return oaa::launch_irfft2_fold_crop(p->L, o, s); });
 }
@@ -427,7 +474,7 @@ oaa_status_t oaa_conv_backward_data(oaa_plan_t p, const float* g, const float* w
   c.nsplit = 1; c.split_stride = 0;
   c.dst = dx;
   c.n_img = p->B; c.n_ch = p->C;
-  c.H = p->N; c.n = p->n; c.T = p->T;
+  c.H = p->N; c.n = p->b; c.T = p->T;
   return timed(p, OAA_STAGE_BWD_DATA_INVERSE, s, "inverse transform + block crop",
                [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
 }

@@ -80,8 +80,41 @@ def test_geometry_of_named_layers(lib, name, expect):
             assert o1 + s1 <= o2, "regions overlap"
         assert offs[-1][0] + offs[-1][1] <= binding.oaa_plan_workspace_bytes(h)
         assert g["split"] >= 1
+        assert g["b"] == ly.n          # the paper's tiling: blocks of the kernel's size
     finally:
         binding.oaa_plan_destroy(h)
+
+
+@pytest.mark.parametrize("name,L,b", [("tiny", 16, 8), ("mid56", 8, 4), ("first224", 16, 8), ("large128", 32, 16)])
+def test_library_tiling_choice(lib, name, L, b):
+    """L = b = 0: fewer, larger blocks where that cuts the estimated work."""
+    ly = LAYERS[name]
+    h = binding.oaa_plan_create_tiled(ly.B, ly.C, ly.K, ly.N, ly.n, 0, 0)
+    try:
+        g = binding.oaa_plan_geometry(h)
+        assert (g["L"], g["b"]) == (L, b)
+        assert g["T"] == -(-ly.N // b) and g["P"] == g["T"] ** 2 and g["F"] == L * (L // 2 + 1)
+    finally:
+        binding.oaa_plan_destroy(h)
+
+
+@pytest.mark.parametrize("dims,status", [
+    ((1, 1, 1, 20, 5, 16, 8), 0), ((1, 1, 1, 20, 5, 16, 4), 0), ((1, 1, 1, 20, 5, 16, 3), 1),   # b < n-1
+    ((1, 1, 1, 20, 5, 16, 9), 1), ((1, 1, 1, 20, 5, 12, 6), 2), ((1, 1, 1, 20, 5, 128, 8), 2),  # 2b > L, L
+    ((1, 1, 1, 20, 5, 16, 0), 1), ((1, 1, 1, 20, 5, 0, 8), 1), ((1, 1, 1, 20, 1, 2, 1), 0),
+    ((1, 1, 1, 20, 5, 0, 0), 0), ((1, 1, 1, 20, 5, -2, 4), 1),
+])
+def test_tiled_plan_validation(lib, dims, status):
+    h = ctypes.c_void_p(12345)
+    st = lib.oaa_plan_create_tiled(ctypes.byref(h), *dims)
+    assert st == status, (dims, st, binding.oaa_last_error_detail())
+    if status == 0:
+        g = binding.oaa_plan_geometry(h.value)
+        if dims[5]:
+            assert (g["L"], g["b"]) == dims[5:]
+        lib.oaa_plan_destroy(h)
+    else:
+        assert h.value is None
 
 
 @pytest.mark.parametrize("dims,status", [

@@ -42,10 +42,10 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
-def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO):
+def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper"):
     B, C, N, _ = x.shape
     K, _, n, _ = w.shape
-    plan = binding.Plan(B, C, K, N, n, device=DEV, contraction=contraction)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, contraction=contraction, tiling=tiling)
     xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
     y = plan.forward(xd, wd)
     dx = plan.backward_data(gd, wd)
@@ -54,8 +54,8 @@ def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO):
     return plan, y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
 
 
-def check_whole(x, w, g, contraction=binding.CONTRACTION_AUTO):
-    _, y, dx, dw = run_layer(x, w, g, contraction)
+def check_whole(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper"):
+    _, y, dx, dw = run_layer(x, w, g, contraction, tiling)
     N, n = x.shape[-1], w.shape[-1]
     e = (relerr(y, oracle.conv_forward(x, w)),
          relerr(dx, oracle.conv_backward_data(g, w, N)),
@@ -108,6 +108,28 @@ def test_narrow_contraction(gpu_lib, shape):
         print(f"split {plan.geometry['split']}", flush=True)
 
 
+TILED = [  # (B, C, K, N, n, L, b): b = n - 1, b between n and L/2, b = L/2, L twice the paper's
+    (1, 3, 4, 32, 5, 16, 4),
+    (2, 2, 3, 13, 4, 8, 4),
+    (1, 5, 6, 29, 5, 16, 8),
+    (2, 3, 5, 21, 3, 8, 4),
+    (1, 4, 7, 40, 7, 32, 16),
+    (2, 6, 5, 23, 3, 16, 8),
+    (1, 70, 66, 24, 3, 8, 4),
+    (2, 1, 2, 17, 1, 4, 2),
+    (1, 2, 3, 36, 9, 32, 12),
+    (1, 40, 33, 50, 16, 32, 15),
+]
+
+
+@pytest.mark.parametrize("shape", TILED, ids=lambda s: "x".join(map(str, s)))
+def test_tiled_layers_all_passes(gpu_lib, shape):
+    """Blocks of b != n (the library's larger-block tiling) against the oracle."""
+    B, C, K, N, n, L, b = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=31 + sum(shape))
+    check_whole(x, w, g, tiling=(L, b))
+
+
 @pytest.mark.parametrize("name", ["tiny", "plane224_n3", "plane224_n5", "plane224_n8"])
 def test_named_small_layers(gpu_lib, name):
     ly = LAYERS[name]
@@ -115,20 +137,22 @@ def test_named_small_layers(gpu_lib, name):
     check_whole(x, w, g)
 
 
+@pytest.mark.parametrize("tiling", ["paper", "auto"])
 @pytest.mark.parametrize("name,batch,C,K", [("first224", 2, None, None), ("mid56", 2, None, None),
                                             ("large128", 1, 16, 32)])
-def test_reduced_large_layers_whole(gpu_lib, name, batch, C, K):
+def test_reduced_large_layers_whole(gpu_lib, name, batch, C, K, tiling):
     ly = LAYERS[name]
     ly = Layer(ly.name, batch, C or ly.C, K or ly.K, ly.N, ly.n, ly.x_dist, ly.w_var, ly.g_dist)
     x, w, g = make_inputs(ly, seed=0)
-    check_whole(x, w, g)
+    check_whole(x, w, g, tiling=tiling)
 
 
+@pytest.mark.parametrize("tiling", ["paper", "auto"])
 @pytest.mark.parametrize("name", ["first224", "mid56", "large128"])
-def test_full_size_layers_sampled(gpu_lib, name):
+def test_full_size_layers_sampled(gpu_lib, name, tiling):
     ly = LAYERS[name]
     x, w, g = make_inputs(ly, seed=0)
-    _, y, dx, dw = run_layer(x, w, g)
+    _, y, dx, dw = run_layer(x, w, g, tiling=tiling)
     rng = np.random.default_rng(1)
     S = 48
     B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M

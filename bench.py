@@ -123,9 +123,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layer", default="large128")
     ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma", "narrow"])
-    ap.add_argument("--tiling", default="auto", choices=["auto", "paper"],
+    ap.add_argument("--tiling", default="auto",
                     help="auto: the library's block size (fewer, larger blocks where that cuts work); "
-                         "paper: blocks of the kernel's size n")
+                         "paper: blocks of the kernel's size n; L:b an explicit transform side and block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--stages-out", default=None, help="also write per-stage timings as JSON here")
@@ -160,7 +160,8 @@ def main():
     print(f"[bench] inputs for {ly.name} drawn in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
     which = {"auto": binding.CONTRACTION_AUTO, "valu": binding.CONTRACTION_VALU,
              "mfma": binding.CONTRACTION_MFMA, "narrow": binding.CONTRACTION_NARROW}[args.contraction]
-    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which, tiling=args.tiling)
+    tiling = args.tiling if args.tiling in ("auto", "paper") else tuple(int(v) for v in args.tiling.split(":"))
+    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which, tiling=tiling)
     geo = plan.geometry
     xd, wd, gd = (torch.from_numpy(a).to(dev) for a in (x, w, g))
     y = torch.empty((ly.B, ly.K, ly.M, ly.M), dtype=torch.float32, device=dev)

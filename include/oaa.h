@@ -125,9 +125,10 @@ oaa_status_t oaa_plan_create(oaa_plan_t* plan, int B, int C, int K, int N, int n
 
 /* Same, with blocks of b x b (pitch b) in L x L transforms. Block results
  * then have support b + n - 1 and the result is the same convolution for any
- * b with max(1, n-1) <= b <= L/2 (the overlap-add is done in the frequency
- * domain, which needs 2b <= L). L must be a power of two in [2, 64]
- * (else OAA_ERR_UNSUPPORTED); a b outside that range is OAA_ERR_INVALID_ARG.
+ * b with max(1, n-1) <= b <= L - n + 1 (up to L/2 the forward overlap-add is
+ * done on the spectra; above, after the inverse). L must be a power of two
+ * in [2, 64] (else OAA_ERR_UNSUPPORTED); a b outside that range is
+ * OAA_ERR_INVALID_ARG.
  * L = b = 0 lets the library choose: L in {L0, 2 L0} (L0 the paper's side)
  * and b by a work estimate of contraction and transforms. Larger blocks
  * mean fewer tiles: fewer spectra to transform, store and contract. */

@@ -145,6 +145,136 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
 }
 
 // ---------------------------------------------------------------------------
+// Forward output for blocks with 2b > L (support S = b + n - 1 <= L): a block
+// result shifted by b would wrap inside L, so the neighbours are added in
+// space after the inverse.
+//
+// One workgroup per (plane, block row P, run of tile columns) with the halo
+// column q0 - 1. Column inverses of the block row's tiles (rows [0, b), zc)
+// and of the row above (rows [b, S), za); row inverses of those rows, each
+// written over its own row's spectrum (S <= L real values in the 2 (L/2 + 1)
+// floats of a row); then every output pixel of the block row is the sum, in
+// a fixed order, of its tile's value and the overhangs of the left, upper and
+// upper-left neighbours.
+template <int L>
+__global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCropParams p) {
+  constexpr int V = L / 2 + 1;
+  extern __shared__ float smem[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int b = p.n, S = p.S, na = S - b, T = p.T, M = p.M;
+  const int TQ1 = p.TQ + 1;
+  const int TSc = odd_at_least(b * V), TSa = odd_at_least(na * V);
+  float2* zc = reinterpret_cast<float2*>(smem);  // [TQ+1][TSc]
+  float2* za = zc + size_t(TQ1) * TSc;            // [TQ+1][TSa]
+  // real rows after the row inverses: row r of tile qq at float offset
+  // 2 (qq TS + r V) of the same array
+  const float* sc = reinterpret_cast<const float*>(zc);
+  const float* sa = reinterpret_cast<const float*>(za);
+  const int SSc = 2 * TSc, SSa = 2 * TSa, RS = 2 * V;
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
+  const int chunk = int(wg % p.nchunk);
+  const unsigned rest = wg / p.nchunk;
+  const int strip = int(rest % T);
+  const unsigned plane = rest / T;
+  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
+  const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
+  const size_t tiles_per_ch = size_t(p.n_img) * T * T;
+  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
+  const size_t ustride = size_t(V) * fstride;
+  const float2* in = p.src + size_t(ch) * tiles_per_ch + size_t(img) * T * T;
+  float* out = p.dst + size_t(plane) * M * M;
+  const float scale = 1.0f / float(L * L);
+
+  // column inverses: part 0 = this block row, part 1 = the block row above
+  for (int task = tid; task < 2 * (nq + 1) * V; task += nthr) {
+    const int qq = task % (nq + 1), rest2 = task / (nq + 1);
+    const int v = rest2 % V, part = rest2 / V;
+    const int Qt = q0 - 1 + qq, Pt = strip - part;
+    const bool live = Qt >= 0 && Pt >= 0 && (part == 0 || na > 0);
+    const float2* col = in + size_t(live ? Pt : 0) * T + (live ? Qt : 0) + size_t(v) * fstride;
+    // columns v = 0 and v = L/2 hold no products in rows u > L/2 (Hermitian
+    // there): inverse of the rows [0, L/2] with rows 0, L/2 halved, twice
+    // the real part
+    const bool mir = v == 0 || v == L / 2;
+    float re[L], im[L];
+#pragma unroll
+    for (int u = 0; u < L; ++u) {
+      const float2 z = col[u * ustride];
+      float zr = live ? z.x : 0.f, zi = live ? z.y : 0.f;
+      if (u > L / 2) {
+        zr = mir ? 0.f : zr;
+        zi = mir ? 0.f : zi;
+      } else if (u == 0 || u == L / 2) {
+        zr *= mir ? 0.5f : 1.f;
+        zi *= mir ? 0.5f : 1.f;
+      }
+      re[u] = zr;
+      im[u] = zi;
+    }
+    fft_dif<L, +1, false>(re, im);
+    const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
+    if (part == 0) {
+      float2* zt = zc + qq * TSc + v;
+#pragma unroll
+      for (int r = 0; r < L; ++r)
+        if (r < b) zt[r * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+    } else {
+      float2* zt = za + qq * TSa + v;
+#pragma unroll
+      for (int r = 0; r < L; ++r)
+        if (r >= b && r < S) zt[(r - b) * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+    }
+  }
+  __syncthreads();
+  // row inverses, two rows per task (a missing partner row is zero)
+  const int pc = (b + 1) / 2, pa = (na + 1) / 2;
+  for (int task = tid; task < (nq + 1) * (pc + pa); task += nthr) {
+    const int qq = task % (nq + 1), k = task / (nq + 1);
+    const bool above = k >= pc;
+    const int r0 = 2 * (above ? k - pc : k), rows = above ? na : b;
+    const float2* zt = above ? za + qq * TSa + r0 * V : zc + qq * TSc + r0 * V;
+    const bool has1 = r0 + 1 < rows;
+    float2 A[V], Bv[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      A[v] = zt[v];
+      Bv[v] = has1 ? zt[V + v] : make_float2(0.f, 0.f);
+    }
+    float zr[L], zi[L];
+    irfft_pair<L>(A, Bv, zr, zi);
+    float* d0 = reinterpret_cast<float*>(const_cast<float2*>(zt));  // this task's own two rows
+#pragma unroll
+    for (int s = 0; s < L; ++s) {
+      if (s < S) {
+        d0[s] = zr[bitrev(s, L)] * scale;
+        if (has1) d0[RS + s] = zi[bitrev(s, L)] * scale;
+      }
+    }
+  }
+  __syncthreads();
+  // output rows strip*b - off + [0, b), columns q0*b - off + [0, nq b), clipped
+  const int W = nq * b;
+  const int i0 = strip * b - p.off, j0 = q0 * b - p.off;
+  const int rb = max(0, -i0), re_ = min(b, M - i0);
+  const int cb = max(0, -j0), ce = min(W, M - j0);
+  const int wr = ce - cb;
+  if (wr <= 0 || re_ <= rb) return;
+  for (int e = tid; e < (re_ - rb) * wr; e += nthr) {
+    const int r = rb + e / wr, c = cb + e % wr;
+    const int q = c / b, s = c - q * b;
+    const float* own = sc + (q + 1) * SSc + r * RS;
+    const float* left = sc + q * SSc + r * RS;
+    float v = own[s];
+    if (s < na) v += left[b + s];
+    if (r < na) {
+      v += sa[(q + 1) * SSa + r * RS + s];
+      if (s < na) v += sa[q * SSa + r * RS + b + s];
+    }
+    out[size_t(i0 + r) * M + j0 + c] = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 
 template <int L>
@@ -169,7 +299,37 @@ hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int L>
+hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
+  constexpr int V = L / 2 + 1;
+  const int b = p.n, S = p.S, na = S - b;
+  if (na < 0 || S > L || 2 * b <= L) return hipErrorInvalidValue;
+  const size_t per_tile = size_t(odd_at_least(b * V) + odd_at_least(na * V)) * 8;
+  int tq = std::min<int>(p.T, int(kLdsBudget / per_tile) - 1);
+  if (tq < 1) return hipErrorInvalidConfiguration;
+  const int nchunk = (p.T + tq - 1) / tq;
+  p.TQ = (p.T + nchunk - 1) / nchunk;
+  p.nchunk = nchunk;
+  const long planes = long(p.n_img) * p.n_ch;
+  const size_t lds = per_tile * (p.TQ + 1);
+  const int tasks = std::max(2 * (p.TQ + 1) * V, (p.TQ + 1) * ((b + 1) / 2 + (na + 1) / 2));
+  const long nwg = planes * p.T * p.nchunk;
+  hipLaunchKernelGGL(irfft2_overlap_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_irfft2_overlap_crop(int L, const FoldCropParams& p, hipStream_t s) {
+  switch (L) {
+    case 4: return launch_overlap_crop_L<4>(p, s);
+    case 8: return launch_overlap_crop_L<8>(p, s);
+    case 16: return launch_overlap_crop_L<16>(p, s);
+    case 32: return launch_overlap_crop_L<32>(p, s);
+    case 64: return launch_overlap_crop_L<64>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_irfft2_fold_crop(int L, const FoldCropParams& p, hipStream_t s) {
   switch (L) {

@@ -151,13 +151,13 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_TILE)) til
 }
 
 // ---------------------------------------------------------------------------
-// Gradient windows: window (P, Q) is the 2n x 2n region of the framed plane
-// (plane rows/cols shifted by -off) starting at (P n, Q n). A workgroup walks
-// down the window rows [pb, pe) of one plane for a run of window columns.
-// Consecutive window rows share n input rows, so the input sits in a ring of
-// 2n rows in LDS (framed row a in ring row a mod 2n) and only the n new rows
-// are loaded per step, prefetched into registers while the current windows
-// are transformed.
+// Gradient windows: window (P, Q) is the S x S region of the framed plane
+// (plane rows/cols shifted by -off) starting at (P n, Q n), n the window
+// pitch and S <= 2n. A workgroup walks down the window rows [pb, pe) of one
+// plane for a run of window columns. Consecutive window rows share input
+// rows, so the input sits in a ring of 2n rows in LDS (framed row a in ring
+// row a mod 2n) and only the n new rows are loaded per step, prefetched into
+// registers while the current windows are transformed.
 //
 // LDS: ring [2n][Wp] floats, then zbuf [TQ][TS] float2 (row transforms,
 // rows [0, ROWS)).
@@ -170,7 +170,7 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
   constexpr int PF = L < 16 ? L : 16;
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
-  const int n = p.n, T = p.T, H = p.H, R = 2 * n;
+  const int n = p.n, T = p.T, H = p.H, R = 2 * n, SW = p.S;
   const int TS = odd_at_least(2 * PAIRS * V);
   const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
@@ -180,7 +180,7 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
   const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
   const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
   const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
-  const int W = (nq + 1) * n;                  // framed columns [q0 n, q0 n + W)
+  const int W = (nq - 1) * n + SW;             // framed columns [q0 n, q0 n + W) the windows cover
   const int Wp = bank_stride((p.TQ - 1) * n + L);  // window reads stay inside the row
   float* ring = smem;                                                               // [2n][Wp]
   float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(R) * Wp));  // [TQ][TS]
@@ -214,11 +214,12 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
       const int q = task % nq, pr = task / nq;
       const int r0 = 2 * pr;
       float2* zt = zbuf + q * TS + r0 * V;
-      if (r0 >= R) {
+      if (r0 >= SW) {
 #pragma unroll
         for (int k = 0; k < 2 * V; ++k) zt[k] = make_float2(0.f, 0.f);
         continue;
       }
+      const bool has_b = r0 + 1 < SW;  // row r0 + 1 inside the window
       int sa = slot0 + r0;
       if (sa >= R) sa -= R;
       int sb = sa + 1;
@@ -230,9 +231,9 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
       for (int s = 0; s < L; ++s) {
         if (s < S) {
           const float x0 = row_a[s], x1 = row_b[s];
-          const bool in = s < R;
+          const bool in = s < SW;
           zr[s] = in ? x0 : 0.f;
-          zi[s] = in ? x1 : 0.f;
+          zi[s] = in && has_b ? x1 : 0.f;
         } else {
           zr[s] = 0.f;
           zi[s] = 0.f;
@@ -341,10 +342,10 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
 // Inverse + top-left n x n crop, scattered to the blocks of the output planes.
 // A workgroup takes TQ consecutive tiles of one channel (they may span block
 // rows and images), so its spectrum reads are contiguous.
-template <int L>
+template <int L, bool FULL>
 __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irfft2_crop_kernel(CropParams p) {
   constexpr int V = L / 2 + 1;
-  constexpr int RT = L / 2;  // rows kept from the column transforms (>= n)
+  constexpr int RT = FULL ? L : L / 2;  // rows kept from the column transforms (>= n)
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int n = p.n, H = p.H;
@@ -378,19 +379,19 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
     const int q = task % nq, pr = task / nq;
     const int r0 = 2 * pr;
     const float2* zt = zbuf + q * TS + r0 * V;
+    const bool has1 = r0 + 1 < n;
     float2 A[V], Bv[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) {
       A[v] = zt[v];
-      Bv[v] = zt[V + v];  // row n (odd n) is read but discarded
+      Bv[v] = has1 ? zt[V + v] : make_float2(0.f, 0.f);  // no row n for odd n
     }
     float zr[L], zi[L];
     irfft_pair<L>(A, Bv, zr, zi);
     float* o0 = obuf + (size_t(r0) * p.TQ + q) * OS;
     float* o1 = o0 + size_t(p.TQ) * OS;
-    const bool has1 = r0 + 1 < n;
 #pragma unroll
-    for (int s = 0; s < L / 2; ++s) {
+    for (int s = 0; s < (FULL ? L : L / 2); ++s) {
       if (s < n) {
         const int pos = bitrev(s, L);
         o0[s] = zr[pos] * scale;
@@ -467,10 +468,11 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int L>
-hipError_t launch_crop_L(CropParams p, hipStream_t s) {
+template <int L, bool FULL>
+hipError_t launch_crop_LF(CropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
-  const int TS = odd_at_least((L / 2 + 1) * V);
+  constexpr int RT = FULL ? L : L / 2;
+  const int TS = odd_at_least((RT + 1) * V);
   // column transforms, output block and three tile descriptors per tile
   const size_t per_tile = size_t(TS) * 8 + size_t(p.n) * (p.n | 1) * 4 + 3 * 4;
   const long tiles = long(p.n_img) * p.T * p.T;
@@ -486,8 +488,15 @@ hipError_t launch_crop_L(CropParams p, hipStream_t s) {
   const size_t lds = per_tile * p.TQ;
   const int tasks = std::max(V * p.TQ, ((p.n + 1) / 2) * p.TQ);
   const long nwg = long(p.n_ch) * p.nchunk;
-  hipLaunchKernelGGL(irfft2_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
+  hipLaunchKernelGGL((irfft2_crop_kernel<L, FULL>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
+}
+
+// blocks of more than L/2 rows need every row of the column transforms
+template <int L>
+hipError_t launch_crop_L(const CropParams& p, hipStream_t s) {
+  if (p.n > L / 2) return launch_crop_LF<L, true>(p, s);
+  return launch_crop_LF<L, false>(p, s);
 }
 
 }  // namespace
@@ -506,7 +515,8 @@ hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s) {
 }
 
 hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s) {
-  const bool zh = 4 * p.n <= L;
+  if (p.S > 2 * p.n || p.S > L || p.S < 1) return hipErrorInvalidValue;
+  const bool zh = 2 * p.S <= L;
   switch (L) {
     case 2: return zh ? launch_window_L<2, true>(p, s) : launch_window_L<2, false>(p, s);
     case 4: return zh ? launch_window_L<4, true>(p, s) : launch_window_L<4, false>(p, s);

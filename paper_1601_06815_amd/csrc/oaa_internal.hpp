@@ -50,7 +50,8 @@ struct WindowParams {
   const float* src;  // [n_img][n_ch][H][H]
   float2* dst;       // [F][n_ch][n_img * T * T]
   int n_img, n_ch;
-  int H, n, off, T;
+  int H, n, off, T;  // n: window pitch b
+  int S;             // window side, in [b + n_kernel - 1, min(2b, L)]
   int TQ, nchunk;    // window columns per workgroup, ceil(T / TQ)
   int SPW, ngroups;  // window rows per workgroup, ceil(T / SPW)
 };
@@ -61,7 +62,8 @@ struct FoldCropParams {
   const float2* src;  // [F][n_ch][n_img * T * T]
   float* dst;         // [n_img][n_ch][M][M]
   int n_img, n_ch;
-  int M, n, off, T;
+  int M, n, off, T;   // n: block pitch b (block side); off: n_kernel - 1
+  int S;              // support of a block result, b + n_kernel - 1 (<= L)
   int TQ, nchunk, SPW, ngroups;
 };
 
@@ -106,6 +108,9 @@ hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
 hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s);
 hipError_t launch_irfft2_fold_crop(int L, const FoldCropParams& p, hipStream_t s);
+// Same result for blocks larger than L/2 (where the frequency-domain fold
+// would wrap): inverse transforms, then the overlap-add in space.
+hipError_t launch_irfft2_overlap_crop(int L, const FoldCropParams& p, hipStream_t s);
 hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s);
 hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s);
 // Streaming contraction for few input channels (C <= kNarrowMaxC), for the

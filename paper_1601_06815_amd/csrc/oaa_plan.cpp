@@ -157,7 +157,8 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
   t.n_img = p->B;
   t.n_ch = p->K;
   t.H = p->M;
-  t.n = p->b;        // window pitch; windows are 2b x 2b (>= b + n - 1 rows)
+  t.n = p->b;        // window pitch
+  t.S = 2 * p->b <= p->L ? 2 * p->b : p->L;  // window side, >= b + n - 1
   t.off = p->n - 1;
   t.T = p->T;
   oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient window spectra",
@@ -187,10 +188,14 @@ oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipSt
 
 // Tiling with the least estimated work: candidate transform sides L0 (the
 // smallest power of two >= 2n-1) and 2 L0, block pitches b in
-// [max(1, n-1), L/2]. Per tile: the contraction, 8 C K flops per computed bin,
-// and four transforms per channel pair (input, gradient window, two
+// [max(1, n-1), L-n+1]. Per tile: the contraction, 8 C K flops per computed
+// bin, and four transforms per channel pair (input, gradient window, two
 // inverses), about 2.5 L^2 log2(L^2) flops each on the vector units, weighted
-// 4x against the matrix cores. Ties go to the smaller L.
+// 4x against the matrix cores, and a further 1.5x at L = 32 and 3x at L = 64
+// (register-resident transforms of those sides run at lower occupancy, as
+// measured); blocks over L/2 add half a transform (the forward inverse then
+// transforms the columns of the block row above too). Ties go to the smaller
+// L.
 void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   (void)B;
   const int L0 = pow2_at_least(2 * n - 1);
@@ -200,11 +205,13 @@ void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
     int lg = 0;
     while ((1 << lg) < Lc) ++lg;
-    const double fft = 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg);
+    const double eff = Lc <= 16 ? 1.0 : (Lc == 32 ? 1.5 : 3.0);
+    const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg);
     const double con = 8.0 * C * K * oaa::unique_bins(Lc);
-    for (int bc = (n > 1 ? n - 1 : 1); 2 * bc <= Lc; ++bc) {
+    for (int bc = (n > 1 ? n - 1 : 1); bc + n - 1 <= Lc; ++bc) {
       const double T = double((N + bc - 1) / bc);
-      const double cost = T * T * (con + fft) * (Lc > L0 ? 1.1 : 1.0);
+      const double f = 2 * bc <= Lc ? fft : fft * 1.125;
+      const double cost = T * T * (con + f) * (Lc > L0 ? 1.1 : 1.0);
       if (best == 0 || cost < best) {
         best = cost;
         L = Lc;
@@ -252,10 +259,10 @@ oaa_status_t oaa_plan_create_tiled(oaa_plan_t* out, int B, int C, int K, int N, 
   }
   if (L < 2 || L > 64 || (L & (L - 1)))
     return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
-  // block results (support b + n - 1) may only reach the next block, and the
-  // frequency-domain overlap-add and the 2b gradient windows need 2b <= L
-  if (b < (n > 1 ? n - 1 : 1) || 2 * b > L)
-    return fail(OAA_ERR_INVALID_ARG, "block pitch b=%d needs max(1, n-1) <= b <= L/2 (n=%d, L=%d)", b, n, L);
+  // block results (support b + n - 1) must fit the transform and may only
+  // reach the next block
+  if (b < (n > 1 ? n - 1 : 1) || b + n - 1 > L)
+    return fail(OAA_ERR_INVALID_ARG, "block pitch b=%d needs max(1, n-1) <= b <= L-n+1 (n=%d, L=%d)", b, n, L);
 
   const int M = N - n + 1;
   const int T = (N + b - 1) / b;
@@ -442,8 +449,14 @@ oaa_status_t oaa_conv_forward(oaa_plan_t p, const float* x, const float* w, floa
   o.dst = y;
   o.n_img = p->B; o.n_ch = p->K;
   o.M = p->M; o.n = p->b; o.off = p->n - 1; o.T = p->T;
+  o.S = p->b + p->n - 1;
+  // the overlap-add in the frequency domain needs neighbours shifted by b not
+  // to wrap into the block (2b <= L); larger blocks add their neighbours in space
+  if (2 * p->b <= p->L)
+    return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
+                 [&] { return oaa::launch_irfft2_fold_crop(p->L, o, s); });
   return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
-               [&] { return oaa::launch_irfft2_fold_crop(p->L, o, s); });
+               [&] { return oaa::launch_irfft2_overlap_crop(p->L, o, s); });
 }
 
 oaa_status_t oaa_conv_backward_data(oaa_plan_t p, const float* g, const float* w, float* dx, void* stream) {

@@ -85,7 +85,7 @@ def test_geometry_of_named_layers(lib, name, expect):
         binding.oaa_plan_destroy(h)
 
 
-@pytest.mark.parametrize("name,L,b", [("tiny", 16, 8), ("mid56", 8, 4), ("first224", 16, 8), ("large128", 32, 16)])
+@pytest.mark.parametrize("name,L,b", [("tiny", 16, 11), ("mid56", 16, 14), ("first224", 16, 10), ("large128", 32, 16)])
 def test_library_tiling_choice(lib, name, L, b):
     """L = b = 0: fewer, larger blocks where that cuts the estimated work."""
     ly = LAYERS[name]
@@ -100,7 +100,8 @@ def test_library_tiling_choice(lib, name, L, b):
 
 @pytest.mark.parametrize("dims,status", [
     ((1, 1, 1, 20, 5, 16, 8), 0), ((1, 1, 1, 20, 5, 16, 4), 0), ((1, 1, 1, 20, 5, 16, 3), 1),   # b < n-1
-    ((1, 1, 1, 20, 5, 16, 9), 1), ((1, 1, 1, 20, 5, 12, 6), 2), ((1, 1, 1, 20, 5, 128, 8), 2),  # 2b > L, L
+    ((1, 1, 1, 20, 5, 16, 12), 0), ((1, 1, 1, 20, 5, 16, 13), 1),                                # b > L-n+1
+    ((1, 1, 1, 20, 5, 12, 6), 2), ((1, 1, 1, 20, 5, 128, 8), 2), ((1, 1, 1, 20, 1, 4, 4), 0),
     ((1, 1, 1, 20, 5, 16, 0), 1), ((1, 1, 1, 20, 5, 0, 8), 1), ((1, 1, 1, 20, 1, 2, 1), 0),
     ((1, 1, 1, 20, 5, 0, 0), 0), ((1, 1, 1, 20, 5, -2, 4), 1),
 ])

@@ -119,6 +119,19 @@ TILED = [  # (B, C, K, N, n, L, b): b = n - 1, b between n and L/2, b = L/2, L t
     (2, 1, 2, 17, 1, 4, 2),
     (1, 2, 3, 36, 9, 32, 12),
     (1, 40, 33, 50, 16, 32, 15),
+    # blocks over L/2 (overlap-add after the inverse), up to b = L - n + 1
+    (1, 3, 4, 32, 5, 16, 12),
+    (2, 2, 3, 13, 4, 8, 5),
+    (1, 5, 6, 29, 5, 16, 10),
+    (2, 3, 5, 21, 3, 8, 6),
+    (1, 4, 7, 40, 7, 32, 26),
+    (2, 1, 2, 17, 1, 4, 4),
+    (1, 70, 66, 24, 3, 8, 6),
+    (1, 40, 33, 50, 16, 32, 17),
+    (2, 3, 64, 60, 7, 16, 10),
+    (1, 3, 4, 70, 16, 64, 49),
+    (1, 2, 3, 36, 9, 64, 40),
+    (1, 2, 2, 9, 9, 32, 24),
 ]
 
 

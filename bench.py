@@ -72,14 +72,15 @@ def source_digest(fname):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, stage):
-    """HBM bytes per launch from committed rocprofv3 counter runs, or None if
-    absent or taken on a different version of the kernel's source."""
+def measured_traffic(workload, geo, stage):
+    """HBM bytes per launch from committed rocprofv3 counter runs of the same
+    workload and tiling, or None if absent or taken on a different version of
+    the kernel's source."""
     path = os.path.join(PROFILE_DIR, "traffic.json")
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path)).get(f"{workload}/{stage}")
+        rec = json.load(open(path)).get(f"{workload}@{geo['L']}:{geo['b']}/{stage}")
     except (ValueError, OSError):
         return None
     if not rec or rec.get("source_sha256") != source_digest(KERNEL_SOURCE[stage]):
@@ -211,7 +212,7 @@ def main():
         achieved = wk["bytes"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS}
-    roof["traffic"] = measured_traffic(ly.name, dom)
+    roof["traffic"] = measured_traffic(ly.name, geo, dom)
     roof["kernel"] = dom
     roof["ms_per_launch"] = per_stage[dom]["ms_per_launch"]
     for name, st in per_stage.items():

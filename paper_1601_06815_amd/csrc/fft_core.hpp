@@ -74,6 +74,93 @@ __host__ __device__ __forceinline__ void fft_dif(float (&re)[L], float (&im)[L])
   }
 }
 
+// ---------------------------------------------------------------------------
+// Transforms split over a pair of neighbouring lanes (h = lane bit 0), for
+// long sides where one lane cannot hold a whole sequence at good occupancy.
+
+// Value of x in the other lane of the pair, via DPP quad permute [1,0,3,2].
+__device__ __forceinline__ float pair_swap(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));
+}
+
+// Length-L transform; lane h holds elements h L/2 + i, i < L/2. The first
+// decimation-in-frequency stage pairs element i of lane 0 with element i of
+// lane 1; then each lane transforms its half alone. On return lane h holds
+// coefficient 2m + h at position bitrev(m, L/2). Both lanes of every pair
+// must execute this together.
+template <int L, int SIGN>
+__device__ __forceinline__ void fft_dif_split(float (&re)[L / 2], float (&im)[L / 2], int h) {
+#pragma unroll
+  for (int i = 0; i < L / 2; ++i) {
+    const float pr = pair_swap(re[i]), pi = pair_swap(im[i]);
+    if (h == 0) {
+      re[i] += pr;
+      im[i] += pi;
+    } else {
+      // (a - b) * exp(SIGN 2 pi i i / L): a from lane 0, b from this lane
+      twiddle_mul<L, SIGN>(i, pr - re[i], pi - im[i], re[i], im[i]);
+    }
+  }
+  fft_dif<L / 2, SIGN, false>(re, im);
+}
+
+// Same when elements [L/2, L) are zero: both lanes hold elements [0, L/2)
+// on entry and no exchange is needed.
+template <int L, int SIGN>
+__device__ __forceinline__ void fft_dif_split_zh(float (&re)[L / 2], float (&im)[L / 2], int h) {
+  if (h == 1) {
+#pragma unroll
+    for (int i = 0; i < L / 2; ++i) twiddle_mul<L, SIGN>(i, re[i], im[i], re[i], im[i]);
+  }
+  fft_dif<L / 2, SIGN, false>(re, im);
+}
+
+// Inverse real transform of two rows split over a lane pair: getA(v),
+// getB(v) return bin v in [0, L/2] of the two half spectra. On return lane h
+// holds L * row0[s] in zr and L * row1[s] in zi for s = 2m + h at position
+// bitrev(m, L/2). The imaginary parts of bins 0 and L/2 are ignored.
+template <int L, class FA, class FB>
+__device__ __forceinline__ void irfft_pair_split(FA getA, FB getB, float (&zr)[L / 2], float (&zi)[L / 2], int h) {
+  constexpr int H = L / 2;
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    // lane 0: z[i]; lane 1: z[H + i], built from bin L - (H + i) = H - i
+    const int v = h ? H - i : i;
+    const float2 a = getA(v), b = getB(v);
+    if (i == 0) {
+      zr[0] = a.x;
+      zi[0] = b.x;
+    } else {
+      zr[i] = h ? a.x + b.y : a.x - b.y;
+      zi[i] = h ? b.x - a.y : a.y + b.x;
+    }
+  }
+  fft_dif_split<L, +1>(zr, zi, h);
+}
+
+// Inverse column transform split over a lane pair: getU(u) returns row u of
+// the column. Columns that hold only rows [0, L/2] of a Hermitian sequence
+// (mir) are transformed as rows [0, L/2] with rows 0 and L/2 halved; the
+// caller then takes twice the real part. On return lane h holds row 2m + h
+// at position bitrev(m, L/2).
+template <int L, class FU>
+__device__ __forceinline__ void column_inverse_split(FU getU, bool mir, float (&re)[L / 2], float (&im)[L / 2], int h) {
+  constexpr int H = L / 2;
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    float2 z = getU(h * H + i);
+    if (i == 0) {  // rows 0 and L/2
+      z.x *= mir ? 0.5f : 1.f;
+      z.y *= mir ? 0.5f : 1.f;
+    } else if (h == 1 && mir) {  // rows past L/2
+      z = make_float2(0.f, 0.f);
+    }
+    re[i] = z.x;
+    im[i] = z.y;
+  }
+  fft_dif_split<L, +1>(re, im, h);
+}
+
 // Forward real transform of two real rows at once: z = row0 + i*row1 is
 // transformed and the Hermitian halves separated. Outputs bins v = 0..L/2 of
 // both rows. zr/zi hold the two rows on entry and are clobbered.

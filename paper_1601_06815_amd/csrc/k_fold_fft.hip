@@ -57,8 +57,37 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
   float* out = p.dst + size_t(plane) * M * M;
   const float scale = 1.0f / float(L * L);
 
+  constexpr bool SPLIT = L >= 64;
+  constexpr int HL = L / 2;
+  if (SPLIT) {
+    for (int task = tid; task < 2 * (nq + 1) * V; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int qq = base % (nq + 1), v = base / (nq + 1);
+      const int Qt = q0 - 1 + qq;
+      const bool live = Qt >= 0;
+      const bool up = live && strip > 0;
+      const float2* cur = in + size_t(strip) * T + (live ? Qt : 0) + size_t(v) * fstride;
+      const float2* abv = cur - (up ? T : 0);
+      const bool mir = v == 0 || v == L / 2;
+      float re[HL], im[HL];
+      column_inverse_split<L>(
+          [&](int u) {
+            const float2 c = cur[u * ustride];
+            const float2 a = abv[u * ustride];
+            return cmad(live ? c : make_float2(0.f, 0.f), twiddle<L, +1>(n * u), up ? a : make_float2(0.f, 0.f));
+          },
+          mir, re, im, h);
+      const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
+      float2* zt = zbuf + qq * TS + v;
+#pragma unroll
+      for (int m = 0; m < HL; ++m) {
+        const int r = 2 * m + h;
+        if (r < RT) zt[r * V] = make_float2(re[bitrev(m, HL)] * rs, im[bitrev(m, HL)] * is);
+      }
+    }
+  }
   // column tasks: tile column q0 - 1 + qq (qq = 0 is the halo), bin column v
-  for (int task = tid; task < (nq + 1) * V; task += nthr) {
+  for (int task = tid; task < (SPLIT ? 0 : (nq + 1) * V); task += nthr) {
     const int qq = task % (nq + 1), v = task / (nq + 1);
     const int Qt = q0 - 1 + qq;
     const bool live = Qt >= 0;
@@ -102,7 +131,30 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
   // fold along v with the left neighbour, inverse row transforms, crop to the
   // tile's n x n output block in LDS
   const int npair = (n + 1) >> 1;
-  for (int task = tid; task < npair * nq; task += nthr) {
+  if (SPLIT) {
+    for (int task = tid; task < 2 * npair * nq; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int q = base % nq, pr = base / nq;
+      const int r0 = 2 * pr;
+      const float2* za = zbuf + (q + 1) * TS + r0 * V;
+      const float2* zb = zbuf + q * TS + r0 * V;
+      float zr[HL], zi[HL];
+      irfft_pair_split<L>([&](int k) { return cmad(za[k], twiddle<L, +1>(n * k), zb[k]); },
+                          [&](int k) { return cmad(za[V + k], twiddle<L, +1>(n * k), zb[V + k]); }, zr, zi, h);
+      float* o0 = obuf + (size_t(r0) * nq + q) * OS;
+      float* o1 = o0 + size_t(nq) * OS;
+      const bool has1 = r0 + 1 < n;
+#pragma unroll
+      for (int m = 0; m < HL; ++m) {
+        const int sx = 2 * m + h;
+        if (sx < n) {
+          o0[sx] = zr[bitrev(m, HL)] * scale;
+          if (has1) o1[sx] = zi[bitrev(m, HL)] * scale;
+        }
+      }
+    }
+  }
+  for (int task = tid; task < (SPLIT ? 0 : npair * nq); task += nthr) {
     const int q = task % nq, pr = task / nq;
     const int r0 = 2 * pr;
     const float2* za = zbuf + (q + 1) * TS + r0 * V;
@@ -185,8 +237,39 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
   float* out = p.dst + size_t(plane) * M * M;
   const float scale = 1.0f / float(L * L);
 
+  constexpr bool SPLIT = L >= 64;
+  constexpr int HL = L / 2;
+  if (SPLIT) {
+    for (int task = tid; task < 4 * (nq + 1) * V; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int qq = base % (nq + 1), rest2 = base / (nq + 1);
+      const int v = rest2 % V, part = rest2 / V;
+      const int Qt = q0 - 1 + qq, Pt = strip - part;
+      const bool live = Qt >= 0 && Pt >= 0 && (part == 0 || na > 0);
+      const float2* col = in + size_t(live ? Pt : 0) * T + (live ? Qt : 0) + size_t(v) * fstride;
+      const bool mir = v == 0 || v == L / 2;
+      float re[HL], im[HL];
+      column_inverse_split<L>(
+          [&](int u) {
+            const float2 z = col[u * ustride];
+            return live ? z : make_float2(0.f, 0.f);
+          },
+          mir, re, im, h);
+      const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
+#pragma unroll
+      for (int m = 0; m < HL; ++m) {
+        const int r = 2 * m + h;
+        const float2 val = make_float2(re[bitrev(m, HL)] * rs, im[bitrev(m, HL)] * is);
+        if (part == 0) {
+          if (r < b) zc[qq * TSc + v + r * V] = val;
+        } else {
+          if (r >= b && r < S) za[qq * TSa + v + (r - b) * V] = val;
+        }
+      }
+    }
+  }
   // column inverses: part 0 = this block row, part 1 = the block row above
-  for (int task = tid; task < 2 * (nq + 1) * V; task += nthr) {
+  for (int task = tid; task < (SPLIT ? 0 : 2 * (nq + 1) * V); task += nthr) {
     const int qq = task % (nq + 1), rest2 = task / (nq + 1);
     const int v = rest2 % V, part = rest2 / V;
     const int Qt = q0 - 1 + qq, Pt = strip - part;
@@ -228,7 +311,32 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
   __syncthreads();
   // row inverses, two rows per task (a missing partner row is zero)
   const int pc = (b + 1) / 2, pa = (na + 1) / 2;
-  for (int task = tid; task < (nq + 1) * (pc + pa); task += nthr) {
+  if (SPLIT) {
+    for (int task = tid; task < 2 * (nq + 1) * (pc + pa); task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int qq = base % (nq + 1), k = base / (nq + 1);
+      const bool above = k >= pc;
+      const int r0 = 2 * (above ? k - pc : k), rows = above ? na : b;
+      const float2* zt = above ? za + qq * TSa + r0 * V : zc + qq * TSc + r0 * V;
+      const bool has1 = r0 + 1 < rows;
+      float zr[HL], zi[HL];
+      irfft_pair_split<L>([&](int v) { return zt[v]; },
+                          [&](int v) { return has1 ? zt[V + v] : make_float2(0.f, 0.f); }, zr, zi, h);
+      // both lanes have read their bins: the pair's rows may be overwritten
+      // once the partner is done too, which the exchange inside the
+      // transform guarantees for the lanes of the pair
+      float* d0 = reinterpret_cast<float*>(const_cast<float2*>(zt));
+#pragma unroll
+      for (int m = 0; m < HL; ++m) {
+        const int sx = 2 * m + h;
+        if (sx < S) {
+          d0[sx] = zr[bitrev(m, HL)] * scale;
+          if (has1) d0[RS + sx] = zi[bitrev(m, HL)] * scale;
+        }
+      }
+    }
+  }
+  for (int task = tid; task < (SPLIT ? 0 : (nq + 1) * (pc + pa)); task += nthr) {
     const int qq = task % (nq + 1), k = task / (nq + 1);
     const bool above = k >= pc;
     const int r0 = 2 * (above ? k - pc : k), rows = above ? na : b;
@@ -293,7 +401,7 @@ hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   p.ngroups = p.T;
   const long planes = long(p.n_img) * p.n_ch;
   const size_t lds = zb * (p.TQ + 1) + ob * p.TQ;
-  const int tasks = std::max((p.TQ + 1) * V, ((p.n + 1) / 2) * p.TQ);
+  const int tasks = (L >= 64 ? 2 : 1) * std::max((p.TQ + 1) * V, ((p.n + 1) / 2) * p.TQ);
   const long nwg = planes * p.T * p.nchunk;
   hipLaunchKernelGGL(irfft2_fold_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
@@ -312,7 +420,7 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
   p.nchunk = nchunk;
   const long planes = long(p.n_img) * p.n_ch;
   const size_t lds = per_tile * (p.TQ + 1);
-  const int tasks = std::max(2 * (p.TQ + 1) * V, (p.TQ + 1) * ((b + 1) / 2 + (na + 1) / 2));
+  const int tasks = (L >= 64 ? 2 : 1) * std::max(2 * (p.TQ + 1) * V, (p.TQ + 1) * ((b + 1) / 2 + (na + 1) / 2));
   const long nwg = planes * p.T * p.nchunk;
   hipLaunchKernelGGL(irfft2_overlap_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();

@@ -29,6 +29,70 @@ namespace {
 using namespace tile;
 
 // ---------------------------------------------------------------------------
+// Pass bodies with each transform split over a lane pair (h = lane bit 0),
+// used for L = 64 where a whole sequence per lane would need ~270 VGPRs.
+
+// Two real rows (row_a, row_b; entries s >= R, and s >= L/2 under ZH, are
+// zero) -> their half spectra, bins v of zt[v] and zt[V + v]. Lane h writes
+// the bins of its parity.
+template <int L, bool ZH>
+__device__ __forceinline__ void row_pair_split(const float* row_a, const float* row_b, int R, bool has_b,
+                                               float2* zt, int h) {
+  constexpr int H = L / 2, V = L / 2 + 1;
+  float zr[H], zi[H];
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    const int s = ZH ? i : h * H + i;
+    const bool in = s < R;
+    const float a = row_a[s], b = row_b[s];
+    zr[i] = in ? a : 0.f;
+    zi[i] = in && has_b ? b : 0.f;
+  }
+  if (ZH)
+    fft_dif_split_zh<L, -1>(zr, zi, h);
+  else
+    fft_dif_split<L, -1>(zr, zi, h);
+  // lane h holds Z[2m + h]; bin v pairs Z[v] with Z[L - v] (same parity)
+#pragma unroll
+  for (int m = 0; m <= H / 2; ++m) {
+    const int ps = bitrev(m, H);
+    const int p0 = bitrev(m == 0 ? 0 : H - m, H);   // partner of v = 2m (lane 0)
+    const int p1 = bitrev(H - 1 - (m < H / 2 ? m : 0), H);  // partner of v = 2m + 1 (lane 1)
+    const float a = zr[ps], b = zi[ps];
+    const float c = h ? zr[p1] : zr[p0], d = h ? zi[p1] : zi[p0];
+    const int v = 2 * m + h;
+    if (h == 0 || m < H / 2) {
+      zt[v] = make_float2(0.5f * (a + c), 0.5f * (b - d));
+      zt[V + v] = make_float2(0.5f * (b + d), 0.5f * (c - a));
+    }
+  }
+}
+
+// Complex column (rows [0, ROWS) of zt at stride V, zero beyond) -> forward
+// transform, coefficient U stored at o[U * ustride]; lane h stores U of its parity.
+template <int L, bool ZH>
+__device__ __forceinline__ void column_split_store(const float2* zt, int ROWS, float2* o, size_t ustride, int h) {
+  constexpr int H = L / 2, V = L / 2 + 1;
+  float re[H], im[H];
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    const int r = ZH ? i : h * H + i;
+    const float2 z = zt[(r < ROWS ? r : 0) * V];
+    re[i] = r < ROWS ? z.x : 0.f;
+    im[i] = r < ROWS ? z.y : 0.f;
+  }
+  if (ZH)
+    fft_dif_split_zh<L, -1>(re, im, h);
+  else
+    fft_dif_split<L, -1>(re, im, h);
+#pragma unroll
+  for (int m = 0; m < H; ++m) {
+    const int pos = bitrev(m, H);
+    o[size_t(2 * m + h) * ustride] = make_float2(re[pos], im[pos]);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Forward: windows -> spectra
 //
 // LDS: img [R + 1][Wp] floats (row R stays zero), then zbuf [TQ][TS] float2,
@@ -84,9 +148,24 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_TILE)) til
   for (int c = tid; c < Wp; c += nthr) img_s[R * Wp + c] = 0.f;
   __syncthreads();
 
+  constexpr bool SPLIT = L >= 64;
   // pass 1: real rows, two per lane (row R is the zero row); pairs past the
   // window write zero rows, so pass 2 reads every row unconditionally
-  for (int task = tid; task < PAIRS * nq; task += nthr) {
+  if (SPLIT) {
+    for (int task = tid; task < 2 * PAIRS * nq; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int q = base % nq, pr = base / nq;
+      const int r0 = 2 * pr;
+      float2* zt = zbuf + q * TS + r0 * V;
+      if (r0 >= R) {
+        for (int v = h; v < 2 * V; v += 2) zt[v] = make_float2(0.f, 0.f);
+        continue;
+      }
+      const float* row_a = img_s + r0 * Wp + q * pitch;
+      row_pair_split<L, ZH>(row_a, row_a + Wp, R, true, zt, h);
+    }
+  }
+  for (int task = tid; task < (SPLIT ? 0 : PAIRS * nq); task += nthr) {
     const int q = task % nq, pr = task / nq;
     const int r0 = 2 * pr;
     float2* zt = zbuf + q * TS + r0 * V;
@@ -125,7 +204,14 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_TILE)) til
   const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
   const size_t ustride = size_t(V) * fstride;
   float2* out = p.dst + size_t(ch) * tiles_per_ch + size_t(img) * p.T * p.T + size_t(strip) * p.T + q0;
-  for (int task = tid; task < V * nq; task += nthr) {
+  if (SPLIT) {
+    for (int task = tid; task < 2 * V * nq; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int q = base % nq, v = base / nq;
+      column_split_store<L, ZH>(zbuf + q * TS + v, ROWS, out + size_t(v) * fstride + q, ustride, h);
+    }
+  }
+  for (int task = tid; task < (SPLIT ? 0 : V * nq); task += nthr) {
     const int q = task % nq, v = task / nq;
     const float2* zt = zbuf + q * TS + v;
     float re[L], im[L];
@@ -201,7 +287,8 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
     if (s0 > 0) stage_rows(ring, Wp, src, H, a0 + (R - s0) - p.off, col0, s0, W);
   }
   RowPrefetch<PF> pf;
-  const bool use_pf = OAA_WINDOW_PREFETCH && RowPrefetch<PF>::fits(n, W);
+  // (L = 64: the registers are worth more to the split transforms)
+  const bool use_pf = L <= 32 && OAA_WINDOW_PREFETCH && RowPrefetch<PF>::fits(n, W);
 
   for (int P = pb; P < pe; ++P) {
     const int a0 = P * n;
@@ -210,7 +297,25 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
     const bool next = P + 1 < pe;
     if (next && use_pf) pf.load(src, H, a0 + R - p.off, col0, n, W);
     // pass 1: window rows two at a time; pairs past the window write zero rows
-    for (int task = tid; task < PAIRS * nq; task += nthr) {
+    constexpr bool SPLIT = L >= 64;
+    if (SPLIT) {
+      for (int task = tid; task < 2 * PAIRS * nq; task += nthr) {
+        const int h = task & 1, base = task >> 1;
+        const int q = base % nq, pr = base / nq;
+        const int r0 = 2 * pr;
+        float2* zt = zbuf + q * TS + r0 * V;
+        if (r0 >= SW) {
+          for (int k = h; k < 2 * V; k += 2) zt[k] = make_float2(0.f, 0.f);
+          continue;
+        }
+        int sa = slot0 + r0;
+        if (sa >= R) sa -= R;
+        int sb = sa + 1;
+        if (sb >= R) sb -= R;
+        row_pair_split<L, ZH>(ring + sa * Wp + q * n, ring + sb * Wp + q * n, SW, r0 + 1 < SW, zt, h);
+      }
+    }
+    for (int task = tid; task < (SPLIT ? 0 : PAIRS * nq); task += nthr) {
       const int q = task % nq, pr = task / nq;
       const int r0 = 2 * pr;
       float2* zt = zbuf + q * TS + r0 * V;
@@ -258,7 +363,14 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
     }
     // pass 2: complex columns, bin-major stores of window row P
     float2* out = out_base + size_t(P) * T;
-    for (int task = tid; task < V * nq; task += nthr) {
+    if (SPLIT) {
+      for (int task = tid; task < 2 * V * nq; task += nthr) {
+        const int h = task & 1, base = task >> 1;
+        const int q = base % nq, v = base / nq;
+        column_split_store<L, ZH>(zbuf + q * TS + v, ROWS, out + size_t(v) * fstride + q, ustride, h);
+      }
+    }
+    for (int task = tid; task < (SPLIT ? 0 : V * nq); task += nthr) {
       const int q = task % nq, v = task / nq;
       const float2* zt = zbuf + q * TS + v;
       float re[L], im[L];
@@ -371,11 +483,64 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
     tbase[p.TQ + q] = img;
     tbase[2 * p.TQ + q] = (min(n, H - prow * n) << 16) | min(n, H - qcol * n);
   }
-  inverse_columns<L, RT>(p.src + size_t(ch) * tiles + t0, fstride, p.nsplit, p.split_stride, nq, TS, zbuf);
-  __syncthreads();
+  constexpr bool SPLIT = L >= 64;
   const float scale = 1.0f / float(L * L);
   const int npair = (n + 1) >> 1;
-  for (int task = tid; task < npair * nq; task += nthr) {
+  if (SPLIT) {
+    constexpr int HL = L / 2;
+    const float2* in = p.src + size_t(ch) * tiles + t0;
+    const size_t ustride = size_t(V) * fstride;
+    for (int task = tid; task < 2 * V * nq; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int q = base % nq, v = base / nq;
+      const float2* col = in + q + size_t(v) * fstride;
+      float re[HL], im[HL];
+      column_inverse_split<L>(
+          [&](int u) {
+            float2 z = col[u * ustride];
+            for (int sp = 1; sp < p.nsplit; ++sp) {
+              const float2 t = col[sp * p.split_stride + u * ustride];
+              z.x += t.x;
+              z.y += t.y;
+            }
+            return z;
+          },
+          v == 0 || v == L / 2, re, im, h);
+      const bool mir = v == 0 || v == L / 2;
+      const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
+      float2* zt = zbuf + q * TS + v;
+#pragma unroll
+      for (int m = 0; m < HL; ++m) {
+        const int r = 2 * m + h;
+        if (r < RT) zt[r * V] = make_float2(re[bitrev(m, HL)] * rs, im[bitrev(m, HL)] * is);
+      }
+    }
+    __syncthreads();
+    for (int task = tid; task < 2 * npair * nq; task += nthr) {
+      const int h = task & 1, base = task >> 1;
+      const int q = base % nq, pr = base / nq;
+      const int r0 = 2 * pr;
+      const float2* zt = zbuf + q * TS + r0 * V;
+      const bool has1 = r0 + 1 < n;
+      float zr[HL], zi[HL];
+      irfft_pair_split<L>([&](int v) { return zt[v]; },
+                          [&](int v) { return has1 ? zt[V + v] : make_float2(0.f, 0.f); }, zr, zi, h);
+      float* o0 = obuf + (size_t(r0) * p.TQ + q) * OS;
+      float* o1 = o0 + size_t(p.TQ) * OS;
+#pragma unroll
+      for (int m = 0; m < HL; ++m) {
+        const int sx = 2 * m + h;
+        if (sx < n) {
+          o0[sx] = zr[bitrev(m, HL)] * scale;
+          if (has1) o1[sx] = zi[bitrev(m, HL)] * scale;
+        }
+      }
+    }
+  } else {
+    inverse_columns<L, RT>(p.src + size_t(ch) * tiles + t0, fstride, p.nsplit, p.split_stride, nq, TS, zbuf);
+  }
+  __syncthreads();
+  for (int task = tid; task < (SPLIT ? 0 : npair * nq); task += nthr) {
     const int q = task % nq, pr = task / nq;
     const int r0 = 2 * pr;
     const float2* zt = zbuf + q * TS + r0 * V;
@@ -435,7 +600,7 @@ hipError_t launch_fwd_L(TileFwdParams p, hipStream_t s) {
   p.nchunk = (run + p.TQ - 1) / p.TQ;
   const size_t lds = lds_for(p.TQ);
   if (lds > kLdsBudget) return hipErrorInvalidConfiguration;
-  const int tasks = std::max(PAIRS * p.TQ, V * p.TQ);
+  const int tasks = (L >= 64 ? 2 : 1) * std::max(PAIRS * p.TQ, V * p.TQ);
   const long nwg = p.gather ? long(p.n_ch) * p.nchunk : long(p.n_img) * p.n_ch * p.T * p.nchunk;
   hipLaunchKernelGGL((tile_rfft2_kernel<L, ZH>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
@@ -462,7 +627,7 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   if (planes < 2048) ng = int(std::min<long>(p.T, (2048 + planes - 1) / planes));
   p.SPW = (p.T + ng - 1) / ng;
   p.ngroups = (p.T + p.SPW - 1) / p.SPW;
-  const int tasks = std::max(PAIRS * p.TQ, V * p.TQ);
+  const int tasks = (L >= 64 ? 2 : 1) * std::max(PAIRS * p.TQ, V * p.TQ);
   const long nwg = planes * p.ngroups * p.nchunk;
   hipLaunchKernelGGL((window_rfft2_kernel<L, ZH>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
@@ -486,7 +651,7 @@ hipError_t launch_crop_LF(CropParams p, hipStream_t s) {
   p.TQ = int((tiles + nchunk - 1) / nchunk);
   p.nchunk = int(nchunk);
   const size_t lds = per_tile * p.TQ;
-  const int tasks = std::max(V * p.TQ, ((p.n + 1) / 2) * p.TQ);
+  const int tasks = (L >= 64 ? 2 : 1) * std::max(V * p.TQ, ((p.n + 1) / 2) * p.TQ);
   const long nwg = long(p.n_ch) * p.nchunk;
   hipLaunchKernelGGL((irfft2_crop_kernel<L, FULL>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();

@@ -430,6 +430,7 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
 
 hipError_t launch_irfft2_overlap_crop(int L, const FoldCropParams& p, hipStream_t s) {
   switch (L) {
+    case 2: return launch_overlap_crop_L<2>(p, s);
     case 4: return launch_overlap_crop_L<4>(p, s);
     case 8: return launch_overlap_crop_L<8>(p, s);
     case 16: return launch_overlap_crop_L<16>(p, s);

@@ -227,3 +227,15 @@ def test_twiddle_table_matches_libm(tmp_path):
             ulp = np.spacing(np.float32(max(abs(ref), 1e-30)))
             worst = max(worst, abs(float(got) - float(ref)) / float(ulp) if abs(ref) > 1e-7 else abs(float(got)) * 1e7)
     assert worst <= 1.0
+
+
+def test_paper_sweep_configurations():
+    """The three sweeps of Section 3 as configured for the benchmark module."""
+    from paper_1601_06815_amd.sweeps import sweep_configs
+    k = sweep_configs("kernels")
+    assert all(c[1:] == (1, 1, c[3], 32, 5) for c in k) and [c[3] for c in k][0] == 25 and k[-1][3] == 750
+    s = sweep_configs("ksize")
+    assert [c[5] for c in s] == list(range(1, 33)) and all(c[3:5] == (100, 64) for c in s)
+    i = sweep_configs("input")
+    assert [c[4] for c in i] == list(range(8, 257, 8)) and all(c[5] == 5 for c in i)
+    assert len(sweep_configs("all")) == len(k) + len(s) + len(i)

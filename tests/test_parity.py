@@ -126,6 +126,7 @@ TILED = [  # (B, C, K, N, n, L, b): b = n - 1, b between n and L/2, b = L/2, L t
     (2, 3, 5, 21, 3, 8, 6),
     (1, 4, 7, 40, 7, 32, 26),
     (2, 1, 2, 17, 1, 4, 4),
+    (1, 2, 3, 9, 1, 2, 2),
     (1, 70, 66, 24, 3, 8, 6),
     (1, 40, 33, 50, 16, 32, 17),
     (2, 3, 64, 60, 7, 16, 10),

@@ -8,25 +8,28 @@
 //   backward_data    dXhat[f] (C x BP) = conj What[f] (C x K)  * Ghat[f] (K x BP)
 //   backward_filter  dWhat[f] (C x K)  = conj Xhat[f] (C x BP) * Ghat[f]^T (BP x K)
 //
-// Two implementations share the operand staging: each 256-lane workgroup
-// loads a 16-deep slice of the reduction for its output tile from global
-// memory into registers with branch-free, clamped addresses (all loads in
-// flight at once), stores it to LDS as separate real and imaginary planes,
-// and prefetches the next slice while the current one is consumed.
-//  * vector ALU: 64 x 64 complex tile, 4 x 4 complex accumulators per lane;
-//  * fp32 matrix cores (v_mfma_f32_16x16x4f32): 128 x 128 (or 96 x 128)
-//    complex tile per workgroup, double-buffered LDS with one barrier per
-//    slice, workgroups renumbered so that tiles sharing operands run on the
-//    same XCD; each complex multiply-accumulate of a 16 x 16 x 4 block is four
-//    real MFMAs, re += ar*br + (-ai)*bi and im += ar*bi + ai*br.
+// Two implementations, both staging 16-deep slices of the reduction for one
+// output tile through LDS as separate real and imaginary planes, with the
+// next slice loaded into registers while the current one is consumed:
+//  * vector ALU: 64 x 64 complex tile per 256-lane workgroup, 4 x 4 complex
+//    accumulators per lane, four real multiply-adds per complex one;
+//  * fp32 matrix cores (v_mfma_f32_16x16x4f32): 128 x 64 (or 96 x 64)
+//    complex tile per workgroup, persistent workgroups walking the tiles in
+//    XCD-local rounds, operands read through buffer resources, LDS slices
+//    laid out so that one 16-byte read serves four matrix-core steps, and
+//    three real products per complex multiply-add (Gauss's form).
 #include <algorithm>
 
 #include "oaa_internal.hpp"
 
 // Minimum waves per SIMD asked of the register allocator for the
-// matrix-core kernel.
+// matrix-core kernel, and its 16-column blocks per wave (tile width / 32);
+// overridable at build time for tuning sweeps.
 #ifndef OAA_WAVES_GEMM
-#define OAA_WAVES_GEMM 1
+#define OAA_WAVES_GEMM 2
+#endif
+#ifndef OAA_GEMM_NB
+#define OAA_GEMM_NB 2
 #endif
 
 namespace oaa {
@@ -173,133 +176,316 @@ __global__ void __launch_bounds__(kThreads) cgemm_valu_kernel(GemmParams p) {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
-// L2). Renumber them so that consecutive logical tiles, which share operand
-// slices, run on the same XCD at about the same time.
-__device__ __forceinline__ unsigned xcd_local_order(unsigned w, unsigned nwg) {
-  const unsigned q = nwg / 8, r = nwg % 8, x = w % 8, j = w / 8;
-  return x * q + min(x, r) + j;
+// LDS layout of an operand slice: [row][k'] with separate real and imaginary
+// planes, k' = (k % 4) * (kKC / 4) + k / 4. The matrix-core step s of a slice
+// uses reduction index k = 4 s + (lane / 16), so one 16-byte read gives a
+// lane its values for all four steps of a slice. Rows are padded to kLdk
+// floats, which keeps those reads and the stores below free of bank
+// conflicts (at most two-way for k-contiguous operands).
+constexpr int kLdk = kKC + 4;
+__device__ __forceinline__ constexpr int kperm(int k) { return (k % 4) * (kKC / 4) + k / 4; }
+
+// buffer resource over the first `bytes` bytes at base (bytes < 2^31)
+// (base and bytes are the same in every lane; saying so keeps the resource in
+// scalar registers)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t operand_resource(const float2* base, unsigned bytes) {
+  const unsigned long long a = reinterpret_cast<unsigned long long>(base);
+  const unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(a));
+  const unsigned hi = __builtin_amdgcn_readfirstlane(unsigned(a >> 32));
+  void* pu = reinterpret_cast<void*>((static_cast<unsigned long long>(hi) << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(pu, short(0), int(__builtin_amdgcn_readfirstlane(bytes)), 0x00020000);
 }
 
-// MB x NB blocks of 16 x 16 per wave, waves in a 2 x 2 grid:
-// tile (32*MB) x (32*NB) complex per workgroup.
-template <int MB, int NB, bool AT, bool AC, bool BT, bool BC>
-__global__ void __launch_bounds__(kThreads, OAA_WAVES_GEMM) cgemm_mfma_kernel(GemmParams p) {
-  constexpr int TM = 32 * MB, TN = 32 * NB;
-  constexpr int LDA = TM + 16, LDB = TN + 16;  // padded LDS row strides (floats)
-  __shared__ float Asr[2][kKC][LDA], Asi[2][kKC][LDA];
-  __shared__ float Bsr[2][kKC][LDB], Bsi[2][kKC][LDB];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * 16 * MB, wn = (wave & 1) * 16 * NB;
+// One operand's ROWS x kKC slices, read through a buffer resource over one
+// bin's matrix; element (row, k) is at k*ld + row (ROW_CONTIG) or row*ld + k.
+// Per tile, each lane computes the byte offsets of its elements relative to
+// the slice start (an offset past the resource for rows outside the matrix,
+// which the hardware reads as zero); per slice only a scalar offset changes.
+//  * ROW_CONTIG: lane t < G*ROWS (G = 256 / ROWS, 2 or 4) takes row t % ROWS
+//    and reduction indices t / ROWS + G i; loads are coalesced along rows,
+//    and each lane's values form runs of four in k', stored with 16-byte
+//    writes. The resource ends at the tile's reduction bound.
+//  * k-contiguous: lane t takes k = t % kKC of rows t / kKC + (256/kKC) i;
+//    loads are coalesced along k; elements past the reduction bound are
+//    redirected out of range per slice.
+template <bool ROW_CONTIG, int ROWS>
+struct Operand {
+  static constexpr int G = ROW_CONTIG ? (kThreads / ROWS >= 4 ? 4 : 2) : 1;
+  static constexpr int PER = ROW_CONTIG ? kKC / G : ROWS * kKC / kThreads;
+  static_assert(!ROW_CONTIG || (ROWS == 64 || ROWS == 96 || ROWS == 128), "row tile");
+  static constexpr unsigned kOut = 0x80000000u;
+  unsigned voff[PER];
+  float2 v[PER];
+  int kl;  // k-contiguous: this lane's reduction index within a slice
 
-  // logical tile order: bin, split, row tile, column tile (fastest)
-  const unsigned tiles_m = (p.M + TM - 1) / TM, tiles_n = (p.N + TN - 1) / TN;
-  const unsigned nwg = gridDim.x;
-  unsigned lw = xcd_local_order(blockIdx.x, nwg);
-  const int tn = lw % tiles_n;
-  lw /= tiles_n;
-  const int tm = lw % tiles_m;
-  lw /= tiles_m;
-  const int split = lw % p.nsplit;
-  const int f = unique_bin(int(lw / p.nsplit), p.L);
-  const int m0 = tm * TM, n0 = tn * TN;
-  const int k_begin = split * p.kchunk;
-  const int k_end = min(p.Kr, k_begin + p.kchunk);
-  const float2* A = p.A + size_t(f) * p.a_fstride;
-  const float2* B = p.B + size_t(f) * p.b_fstride;
-
-  floatx4 accr[MB][NB], acci[MB][NB];
-#pragma unroll
-  for (int i = 0; i < MB; ++i)
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      accr[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-      acci[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
-
-  const int lr = lane & 15;  // operand row (A) / column (B) within a 16-block
-  const int lk = lane >> 4;  // operand reduction index within a 4-step
-
-  Slice<AT, TM> sa;
-  Slice<!BT, TN> sb;
-  sa.load(A, p.lda, m0, p.M, k_begin, k_end);
-  sb.load(B, p.ldb, n0, p.N, k_begin, k_end);
-  sa.template store<LDA>(Asr[0], Asi[0], AC);
-  sb.template store<LDB>(Bsr[0], Bsi[0], BC);
-  __syncthreads();
-  int buf = 0;
-  for (int k0 = k_begin; k0 < k_end; k0 += kKC) {
-    const bool more = k0 + kKC < k_end;
-    if (more) {
-      sa.load(A, p.lda, m0, p.M, k0 + kKC, k_end);
-      sb.load(B, p.ldb, n0, p.N, k0 + kKC, k_end);
-    }
-#pragma unroll
-    for (int ks = 0; ks < kKC; ks += 4) {
-      const int kr = ks + lk;
-      float ar[MB], ai[MB], nai[MB], br[NB], bi[NB];
-#pragma unroll
-      for (int i = 0; i < MB; ++i) {
-        ar[i] = Asr[buf][kr][wm + 16 * i + lr];
-        ai[i] = Asi[buf][kr][wm + 16 * i + lr];
-        nai[i] = -ai[i];
-      }
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        br[j] = Bsr[buf][kr][wn + 16 * j + lr];
-        bi[j] = Bsi[buf][kr][wn + 16 * j + lr];
-      }
-        // four independent sweeps, so that dependent accumulations are
-        // MB*NB instructions apart
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            accr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i], br[j], accr[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i], bi[j], acci[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            accr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(nai[i], bi[j], accr[i][j], 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ai[i], br[j], acci[i][j], 0, 0, 0);
-    }
-    if (more) {
-      sa.template store<LDA>(Asr[buf ^ 1], Asi[buf ^ 1], AC);
-      sb.template store<LDB>(Bsr[buf ^ 1], Bsi[buf ^ 1], BC);
-    }
-    __syncthreads();
-    buf ^= 1;
+  __device__ __forceinline__ bool active() const {
+    return !ROW_CONTIG || int(threadIdx.x) < G * ROWS;
   }
 
-  // 16 x 16 result block: lane holds rows 4*(lane/16) + r, r < 4, of column lane % 16
-  float2* Cm = p.C + size_t(f) * p.c_fstride + size_t(split) * p.c_sstride;
+  __device__ __forceinline__ void set_tile(int r0, int nrows, unsigned ld) {
+    const int t = threadIdx.x;
+    if (ROW_CONTIG) {
+      const int r = r0 + t % ROWS, kg = t / ROWS;
+      const bool ok = r < nrows && active();
 #pragma unroll
-  for (int i = 0; i < MB; ++i)
+      for (int i = 0; i < PER; ++i) voff[i] = ok ? (unsigned(kg + G * i) * ld + unsigned(r)) * 8u : kOut;
+    } else {
+      kl = t % kKC;
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int nn = n0 + wn + 16 * j + lr;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm + 16 * i + 4 * lk + r;
-        if (m < p.M && nn < p.N) Cm[size_t(m) * p.ldc + nn] = make_float2(accr[i][j][r], acci[i][j][r]);
+      for (int i = 0; i < PER; ++i) {
+        const int r = r0 + t / kKC + (kThreads / kKC) * i;
+        voff[i] = r < nrows ? (unsigned(r) * ld + unsigned(kl)) * 8u : kOut;
       }
     }
+  }
+
+  // slice starting at reduction index k0 of a tile whose reduction ends at
+  // ke, from a matrix of `elems` elements at base. The resource starts at the
+  // slice, so that the hardware's range check sees only the lane offsets.
+  __device__ __forceinline__ void load(const float2* base, size_t elems, unsigned ld, int k0, int ke) {
+    if (ROW_CONTIG) {
+      const __amdgpu_buffer_rsrc_t rs = operand_resource(base + size_t(k0) * ld, unsigned(ke - k0) * ld * 8u);
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        v[i] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rs, voff[i], 0, 0));
+    } else {
+      const __amdgpu_buffer_rsrc_t rs = operand_resource(base + k0, unsigned(elems - size_t(k0)) * 8u);
+      const bool kok = kl < ke - k0;
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        v[i] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rs, kok ? voff[i] : kOut, 0, 0));
+    }
+  }
+
+  __device__ __forceinline__ void store(float (*re)[kLdk], float (*im)[kLdk], bool conj) const {
+    const int t = threadIdx.x;
+    if (ROW_CONTIG) {
+      if (!active()) return;
+      const int r = t % ROWS, kg = t / ROWS;
+      // values i = q + (4/G) m, m < 4, share k % 4 = (kg + G q) % 4 and have k / 4 = m + const
+#pragma unroll
+      for (int q = 0; q < 4 / G; ++q) {
+        const int kp = kperm(kg + G * q);
+        floatx4 xr, xi;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          xr[m] = v[q + (4 / G) * m].x;
+          xi[m] = conj ? -v[q + (4 / G) * m].y : v[q + (4 / G) * m].y;
+        }
+        *reinterpret_cast<floatx4*>(&re[r][kp]) = xr;
+        *reinterpret_cast<floatx4*>(&im[r][kp]) = xi;
+      }
+    } else {
+      const int kp = kperm(kl);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int r = t / kKC + (kThreads / kKC) * i;
+        re[r][kp] = v[i].x;
+        im[r][kp] = conj ? -v[i].y : v[i].y;
+      }
+    }
+  }
+};
+
+// One output tile of the logical tile sequence: bin, split, row tile, column
+// tile (fastest).
+struct MfmaTile {
+  int f, split, m0, n0, kb, ke;
+};
+
+template <int TM, int TN>
+__device__ __forceinline__ MfmaTile mfma_tile(const GemmParams& p, unsigned t, unsigned tiles_m, unsigned tiles_n) {
+  MfmaTile c;
+  c.n0 = int(t % tiles_n) * TN;
+  t /= tiles_n;
+  c.m0 = int(t % tiles_m) * TM;
+  t /= tiles_m;
+  c.split = int(t % unsigned(p.nsplit));
+  c.f = unique_bin(int(t / unsigned(p.nsplit)), p.L);
+  c.kb = c.split * p.kchunk;
+  c.ke = min(p.Kr, c.kb + p.kchunk);
+  return c;
+}
+
+// Persistent matrix-core contraction. MB x NB blocks of 16 x 16 per wave,
+// waves in a 2 x 2 grid: tile (32*MB) x (32*NB) complex per workgroup. The
+// grid (a multiple of 8 workgroups) walks the logical tile sequence in
+// rounds; in each round the workgroups of one XCD take consecutive tiles, so
+// that tiles sharing operand slices share that XCD's L2. Each workgroup
+// streams the reduction slices of all its tiles through one double-buffered
+// LDS pipeline: the first slice of its next tile is loaded while the last
+// slice of the current one is multiplied.
+//
+// Each complex multiply-add uses three real products (Gauss): with
+// p1 = sum ar br, p2 = sum ai bi and p3 = sum (ar + ai)(br + bi), the result
+// is re = p1 - p2, im = p3 - p1 - p2.
+template <int MB, int NB, bool AT, bool AC, bool BT, bool BC>
+__global__ void __launch_bounds__(kThreads, OAA_WAVES_GEMM) cgemm_mfma_kernel(GemmParams p, unsigned ntiles) {
+  constexpr int TM = 32 * MB, TN = 32 * NB;
+  __shared__ __attribute__((aligned(16))) float Asr[2][TM][kLdk], Asi[2][TM][kLdk];
+  __shared__ __attribute__((aligned(16))) float Bsr[2][TN][kLdk], Bsi[2][TN][kLdk];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * 16 * MB, wn = (wave & 1) * 16 * NB;
+  const int lr = lane & 15;  // operand row (A) / column (B) within a 16-block
+  const int lk = lane >> 4;  // reduction index within a matrix-core step
+
+  const unsigned tiles_m = (p.M + TM - 1) / TM, tiles_n = (p.N + TN - 1) / TN;
+  const unsigned nwg = gridDim.x;
+  unsigned ct = (blockIdx.x % 8) * (nwg / 8) + blockIdx.x / 8;  // this workgroup's first tile
+  if (ct >= ntiles) return;
+  MfmaTile cur = mfma_tile<TM, TN>(p, ct, tiles_m, tiles_n);
+  int ck = cur.kb;
+  // load cursor: one slice ahead of the compute cursor
+  unsigned lt = ct;
+  MfmaTile nx = cur;
+  int lkk = ck;
+
+  Operand<AT, TM> sa;
+  Operand<!BT, TN> sb;
+  auto set_tile = [&](const MfmaTile& t) {
+    sa.set_tile(t.m0, p.M, unsigned(p.lda));
+    sb.set_tile(t.n0, p.N, unsigned(p.ldb));
+  };
+  auto load_slice = [&](const MfmaTile& t, int k0) {
+    sa.load(p.A + size_t(t.f) * p.a_fstride, p.a_fstride, unsigned(p.lda), k0, t.ke);
+    sb.load(p.B + size_t(t.f) * p.b_fstride, p.b_fstride, unsigned(p.ldb), k0, t.ke);
+  };
+  auto advance = [&](unsigned& t, MfmaTile& c, int& k, bool reload) {
+    k += kKC;
+    if (k >= c.ke) {
+      t += nwg;
+      if (t < ntiles) {
+        c = mfma_tile<TM, TN>(p, t, tiles_m, tiles_n);
+        k = c.kb;
+        if (reload) set_tile(c);
+      }
+    }
+  };
+
+  set_tile(nx);
+  load_slice(nx, lkk);
+  sa.store(Asr[0], Asi[0], AC);
+  sb.store(Bsr[0], Bsi[0], BC);
+  advance(lt, nx, lkk, true);
+  __syncthreads();
+
+  floatx4 p1[MB][NB], p2[MB][NB], p3[MB][NB];
+  auto zero = [&]() {
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        p1[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        p2[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        p3[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+  };
+  zero();
+
+  int buf = 0;
+  for (;;) {
+    const bool more = lt < ntiles;
+    if (more) load_slice(nx, lkk);
+    floatx4 Ar[MB], Ai[MB], Br[NB], Bi[NB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      Ar[i] = *reinterpret_cast<const floatx4*>(&Asr[buf][wm + 16 * i + lr][4 * lk]);
+      Ai[i] = *reinterpret_cast<const floatx4*>(&Asi[buf][wm + 16 * i + lr][4 * lk]);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      Br[j] = *reinterpret_cast<const floatx4*>(&Bsr[buf][wn + 16 * j + lr][4 * lk]);
+      Bi[j] = *reinterpret_cast<const floatx4*>(&Bsi[buf][wn + 16 * j + lr][4 * lk]);
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      float as[MB], bs[NB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) as[i] = Ar[i][s] + Ai[i][s];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) bs[j] = Br[j][s] + Bi[j][s];
+      // three independent sweeps, so that dependent accumulations are
+      // MB*NB instructions apart
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          p1[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(Ar[i][s], Br[j][s], p1[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          p3[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(as[i], bs[j], p3[i][j], 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          p2[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(Ai[i][s], Bi[j][s], p2[i][j], 0, 0, 0);
+    }
+    if (more) {
+      sa.store(Asr[buf ^ 1], Asi[buf ^ 1], AC);
+      sb.store(Bsr[buf ^ 1], Bsi[buf ^ 1], BC);
+    }
+    if (ck + kKC >= cur.ke) {
+      // 16 x 16 result block: lane holds rows 4*(lane/16) + r, r < 4, of column lane % 16
+      float2* Cm = p.C + size_t(cur.f) * p.c_fstride + size_t(cur.split) * p.c_sstride;
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int nn = cur.n0 + wn + 16 * j + lr;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = cur.m0 + wm + 16 * i + 4 * lk + r;
+            const float re = p1[i][j][r] - p2[i][j][r];
+            const float im = p3[i][j][r] - p1[i][j][r] - p2[i][j][r];
+            if (m < p.M && nn < p.N) Cm[size_t(m) * p.ldc + nn] = make_float2(re, im);
+          }
+        }
+      zero();
+    }
+    __syncthreads();
+    if (!more) break;
+    buf ^= 1;
+    advance(ct, cur, ck, false);
+    advance(lt, nx, lkk, true);
+  }
+}
+
+// Workgroups per CU and CU count of the current device for one kernel
+// instantiation, queried once per device.
+template <class Kern>
+hipError_t resident_groups(Kern kern, unsigned& groups) {
+  static int cached[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (cached[dev] == 0) {
+    int cus = 0, per_cu = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kThreads, 0);
+    if (e != hipSuccess) return e;
+    cached[dev] = (per_cu < 1 ? 1 : per_cu) * (cus < 1 ? 1 : cus);
+  }
+  groups = unsigned(cached[dev]);
+  return hipSuccess;
 }
 
 template <int MB, int NB, bool AT, bool AC, bool BT, bool BC>
 hipError_t launch_mfma_shape(const GemmParams& p, hipStream_t s) {
-  const unsigned tiles = unsigned(((p.M + 32 * MB - 1) / (32 * MB)) * ((p.N + 32 * NB - 1) / (32 * NB)));
-  const unsigned nwg = tiles * unsigned(p.nsplit) * unsigned(p.F);
-  hipLaunchKernelGGL((cgemm_mfma_kernel<MB, NB, AT, AC, BT, BC>), dim3(nwg), dim3(kThreads), 0, s, p);
+  const unsigned long long tiles = (unsigned long long)((p.M + 32 * MB - 1) / (32 * MB)) *
+                                   ((p.N + 32 * NB - 1) / (32 * NB)) * unsigned(p.nsplit) * unsigned(p.F);
+  if (tiles == 0) return hipSuccess;
+  if (tiles > 0xffffffffull) return hipErrorInvalidValue;
+  auto kern = cgemm_mfma_kernel<MB, NB, AT, AC, BT, BC>;
+  unsigned groups = 0;
+  hipError_t e = resident_groups(kern, groups);
+  if (e != hipSuccess) return e;
+  unsigned long long nwg = groups < tiles ? groups : tiles;
+  nwg = (nwg + 7) / 8 * 8;  // whole rounds over the 8 XCDs
+  hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(kThreads), 0, s, p, unsigned(tiles));
   return hipGetLastError();
 }
 
@@ -308,8 +494,8 @@ template <bool AT, bool AC, bool BT, bool BC>
 hipError_t launch_mfma(const GemmParams& p, hipStream_t s) {
   const long waste128 = (long)((p.M + 127) / 128) * 128 - p.M;
   const long waste96 = (long)((p.M + 95) / 96) * 96 - p.M;
-  if (waste96 < waste128) return launch_mfma_shape<3, 4, AT, AC, BT, BC>(p, s);
-  return launch_mfma_shape<4, 4, AT, AC, BT, BC>(p, s);
+  if (waste96 < waste128) return launch_mfma_shape<3, OAA_GEMM_NB, AT, AC, BT, BC>(p, s);
+  return launch_mfma_shape<4, OAA_GEMM_NB, AT, AC, BT, BC>(p, s);
 }
 
 template <int TM, int TN, class Kern>
@@ -335,12 +521,16 @@ hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s) {
 
 hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s) {
   if (p.kchunk % kKC != 0 && p.nsplit > 1) return hipErrorInvalidValue;
+  if (!mfma_fits(p)) return hipErrorInvalidValue;
   if (p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<true, false, false, false>(p, s);
   if (!p.a_trans && p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<false, true, false, false>(p, s);
   if (!p.a_trans && p.a_conj && p.b_trans && !p.b_conj) return launch_mfma<false, true, true, false>(p, s);
   return hipErrorInvalidValue;
 }
 
-bool mfma_preferred(const GemmParams& p) { return p.M >= 32 && p.N >= 32 && p.Kr >= 16; }
+// The matrix-core path reads each bin's operands through 32-bit byte offsets.
+bool mfma_fits(const GemmParams& p) { return p.a_fstride < (size_t(1) << 28) && p.b_fstride < (size_t(1) << 28); }
+
+bool mfma_preferred(const GemmParams& p) { return p.M >= 32 && p.N >= 32 && p.Kr >= 16 && mfma_fits(p); }
 
 }  // namespace oaa

@@ -37,9 +37,11 @@ def stage_work(ly, geo):
     F, P, S, L = geo["F"], geo["P"], geo["split"], geo["L"]
     BP = B * P
     cplx = 8
-    # the contractions compute the bins that are not conjugates of others
+    # the contractions compute the bins that are not conjugates of others;
+    # the matrix-core engine forms each complex multiply-add from three real
+    # products (Gauss), i.e. 6 real flops, where the textbook count is 8
     Fu = (L // 2 + 1) ** 2 + (L // 2 - 1) ** 2
-    prod_flops = 8.0 * BP * C * K * Fu
+    prod_flops = 6.0 * BP * C * K * Fu
     return {
         "w_spectrum": dict(bytes=K * C * n * n * 4 + F * C * K * cplx),
         "x_spectrum": dict(bytes=B * C * N * N * 4 + F * C * BP * cplx),
@@ -60,7 +62,8 @@ KERNEL_SOURCE = {
 }
 
 
-SHARED_SOURCES = ("oaa_plan.cpp", "oaa_internal.hpp", "tile_common.hpp", "fft_core.hpp", "twiddle.hpp")
+SHARED_SOURCES = ("oaa_plan.cpp", "oaa_internal.hpp", "tile_common.hpp", "fft_core.hpp", "twiddle.hpp",
+                  "buffer_io.hpp")
 
 
 def source_digest(fname):
@@ -117,6 +120,89 @@ def cpu_baseline(ly, x, w, g, budget_s=20.0):
                       f"backward_data + backward_filter, {spent:.1f} s"}
 
 
+STAGE_ORDER = ["w_spectrum", "x_spectrum", "fwd_product", "fwd_inverse", "g_spectrum", "bwd_data_product",
+               "bwd_data_inverse", "bwd_filter_product", "bwd_filter_inverse"]
+LIB_KERNELS = ("tile_rfft2_kernel", "window_rfft2_kernel", "irfft2_", "cgemm_", "narrow_")
+
+
+def _short_kernel(name):
+    name = name.replace("void oaa::(anonymous namespace)::", "")
+    return name.split("(oaa::")[0]
+
+
+def _dispatch_values(run_dir, counter):
+    """Per-dispatch values of one counter from a rocprofv3 csv run, library
+    kernels only, in dispatch order: [(kernel, value), ...]."""
+    import csv
+    import glob
+    rows = list(csv.DictReader(open(glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"),
+                                              recursive=True)[0])))
+    per = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        d = int(r["Dispatch_Id"])
+        per[d] = (_short_kernel(r["Kernel_Name"]), per.get(d, ("", 0.0))[1] + float(r["Counter_Value"]))
+    return [per[d] for d in sorted(per)]
+
+
+def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, steps=2):
+    """HBM bytes per launch of each stage from FETCH_SIZE and WRITE_SIZE runs of
+    `bench.py --layer <layer> --steps 2 --warmup 1 --no-cpu-baseline`,
+    calibrated against runs of `bench.py --copy-calibration 1024`; prints the
+    table and records the figures in profiles/traffic.json."""
+    from paper_1601_06815_amd import binding
+    from paper_1601_06815_amd.workloads import LAYERS
+    ly = LAYERS[layer]
+    h = binding.oaa_plan_create_tiled(ly.B, ly.C, ly.K, ly.N, ly.n, 0, 0)
+    geo = binding.oaa_plan_geometry(h)
+    binding.oaa_plan_destroy(h)
+    copy_bytes = 1024 * (1 << 20)
+    cf = [v for k, v in _dispatch_values(cal_fetch_dir, "FETCH_SIZE")]
+    cw = [v for k, v in _dispatch_values(cal_write_dir, "WRITE_SIZE")]
+    # a plain copy reads and writes copy_bytes; counters are in KiB
+    f_factor = copy_bytes / (sorted(cf)[len(cf) // 2] * 1024)
+    w_factor = copy_bytes / (sorted(cw)[len(cw) // 2] * 1024)
+    fetch = [(k, v) for k, v in _dispatch_values(fetch_dir, "FETCH_SIZE") if k.startswith(LIB_KERNELS)]
+    write = [(k, v) for k, v in _dispatch_values(write_dir, "WRITE_SIZE") if k.startswith(LIB_KERNELS)]
+    n = len(STAGE_ORDER)
+    fetch, write = fetch[-steps * n:], write[-steps * n:]
+    work = stage_work(ly, geo)
+    path = os.path.join(PROFILE_DIR, "traffic.json")
+    db = json.load(open(path)) if os.path.exists(path) else {}
+    db["_calibration"] = {"copy_bytes_each_way": copy_bytes, "fetch_factor": round(f_factor, 4),
+                          "write_factor": round(w_factor, 4),
+                          "note": "bytes = counter KiB x 1024 x factor; factors from a plain device copy"}
+    print(f"## {layer}, L={geo['L']} b={geo['b']} (mean over the last {steps} steps)")
+    print(f"{'stage':20s} {'kernel':48s} {'fetch MB':>9s} {'write MB':>9s} {'total MB':>9s} {'algo MB':>9s} {'ratio':>6s}")
+    for i, stage in enumerate(STAGE_ORDER):
+        fs = [fetch[j * n + i] for j in range(steps)]
+        ws = [write[j * n + i] for j in range(steps)]
+        kern = fs[0][0]
+        fb = sum(v for _, v in fs) / steps * 1024 * f_factor
+        wb = sum(v for _, v in ws) / steps * 1024 * w_factor
+        algo = work[stage]["bytes"]
+        print(f"{stage:20s} {kern[:48]:48s} {fb / 1e6:9.1f} {wb / 1e6:9.1f} {(fb + wb) / 1e6:9.1f} "
+              f"{algo / 1e6:9.1f} {(fb + wb) / algo:6.2f}")
+        db[f"{layer}@{geo['L']}:{geo['b']}/{stage}"] = {
+            "kernel": kern, "fetch_bytes": int(fb), "write_bytes": int(wb), "bytes_per_launch": int(fb + wb),
+            "source_sha256": source_digest(KERNEL_SOURCE[stage])}
+    with open(path, "w") as f:
+        json.dump(db, f, indent=1, sort_keys=True)
+        f.write("\n")
+
+
+def summarize_stats(run_dir):
+    """Short table from a rocprofv3 --kernel-trace --stats csv run."""
+    import csv
+    import glob
+    rows = list(csv.DictReader(open(glob.glob(os.path.join(run_dir, "**", "*kernel_stats.csv"), recursive=True)[0])))
+    print(f"{'kernel':64s} {'calls':>6s} {'avg us':>9s} {'min us':>9s} {'max us':>9s} {'% time':>7s}")
+    for r in rows:
+        print(f"{_short_kernel(r['Name'])[:64]:64s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:9.1f} "
+              f"{float(r['MinNs']) / 1e3:9.1f} {float(r['MaxNs']) / 1e3:9.1f} {float(r['Percentage']):7.2f}")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,7 +218,17 @@ def main():
     ap.add_argument("--stages-out", default=None, help="also write per-stage timings as JSON here")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (for counter calibration) and exit")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
+                    help="host only: HBM traffic per stage of --layer from rocprofv3 FETCH_SIZE/WRITE_SIZE runs")
+    ap.add_argument("--summarize-stats", metavar="DIR",
+                    help="host only: table of a rocprofv3 --kernel-trace --stats run")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(args.layer, *args.summarize_pmc)
+        return
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -207,7 +303,9 @@ def main():
     if "flops" in wk:
         achieved = wk["flops"] / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / FP32_MFMA_PEAK_TFLOPS}
+                "frac": achieved / FP32_MFMA_PEAK_TFLOPS,
+                "flops_counted": "6 per complex multiply-add (three real MFMA products)",
+                "complex_equiv_tflops": achieved * 8.0 / 6.0}
     else:
         achieved = wk["bytes"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -20,6 +20,7 @@
 //    three real products per complex multiply-add (Gauss's form).
 #include <algorithm>
 
+#include "buffer_io.hpp"
 #include "oaa_internal.hpp"
 
 // Minimum waves per SIMD asked of the register allocator for the
@@ -185,17 +186,6 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kLdk = kKC + 4;
 __device__ __forceinline__ constexpr int kperm(int k) { return (k % 4) * (kKC / 4) + k / 4; }
 
-// buffer resource over the first `bytes` bytes at base (bytes < 2^31)
-// (base and bytes are the same in every lane; saying so keeps the resource in
-// scalar registers)
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t operand_resource(const float2* base, unsigned bytes) {
-  const unsigned long long a = reinterpret_cast<unsigned long long>(base);
-  const unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(a));
-  const unsigned hi = __builtin_amdgcn_readfirstlane(unsigned(a >> 32));
-  void* pu = reinterpret_cast<void*>((static_cast<unsigned long long>(hi) << 32) | lo);
-  return __builtin_amdgcn_make_buffer_rsrc(pu, short(0), int(__builtin_amdgcn_readfirstlane(bytes)), 0x00020000);
-}
-
 // One operand's ROWS x kKC slices, read through a buffer resource over one
 // bin's matrix; element (row, k) is at k*ld + row (ROW_CONTIG) or row*ld + k.
 // Per tile, each lane computes the byte offsets of its elements relative to
@@ -213,7 +203,6 @@ struct Operand {
   static constexpr int G = ROW_CONTIG ? (kThreads / ROWS >= 4 ? 4 : 2) : 1;
   static constexpr int PER = ROW_CONTIG ? kKC / G : ROWS * kKC / kThreads;
   static_assert(!ROW_CONTIG || (ROWS == 64 || ROWS == 96 || ROWS == 128), "row tile");
-  static constexpr unsigned kOut = 0x80000000u;
   unsigned voff[PER];
   float2 v[PER];
   int kl;  // k-contiguous: this lane's reduction index within a slice
@@ -228,13 +217,13 @@ struct Operand {
       const int r = r0 + t % ROWS, kg = t / ROWS;
       const bool ok = r < nrows && active();
 #pragma unroll
-      for (int i = 0; i < PER; ++i) voff[i] = ok ? (unsigned(kg + G * i) * ld + unsigned(r)) * 8u : kOut;
+      for (int i = 0; i < PER; ++i) voff[i] = ok ? (unsigned(kg + G * i) * ld + unsigned(r)) * 8u : kOutOfRange;
     } else {
       kl = t % kKC;
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
         const int r = r0 + t / kKC + (kThreads / kKC) * i;
-        voff[i] = r < nrows ? (unsigned(r) * ld + unsigned(kl)) * 8u : kOut;
+        voff[i] = r < nrows ? (unsigned(r) * ld + unsigned(kl)) * 8u : kOutOfRange;
       }
     }
   }
@@ -244,16 +233,16 @@ struct Operand {
   // slice, so that the hardware's range check sees only the lane offsets.
   __device__ __forceinline__ void load(const float2* base, size_t elems, unsigned ld, int k0, int ke) {
     if (ROW_CONTIG) {
-      const __amdgpu_buffer_rsrc_t rs = operand_resource(base + size_t(k0) * ld, unsigned(ke - k0) * ld * 8u);
+      const __amdgpu_buffer_rsrc_t rs = buffer_resource(base + size_t(k0) * ld, unsigned(ke - k0) * ld * 8u);
 #pragma unroll
       for (int i = 0; i < PER; ++i)
-        v[i] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rs, voff[i], 0, 0));
+        v[i] = buffer_load_f2(rs, voff[i]);
     } else {
-      const __amdgpu_buffer_rsrc_t rs = operand_resource(base + k0, unsigned(elems - size_t(k0)) * 8u);
+      const __amdgpu_buffer_rsrc_t rs = buffer_resource(base + k0, unsigned(elems - size_t(k0)) * 8u);
       const bool kok = kl < ke - k0;
 #pragma unroll
       for (int i = 0; i < PER; ++i)
-        v[i] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rs, kok ? voff[i] : kOut, 0, 0));
+        v[i] = buffer_load_f2(rs, kok ? voff[i] : kOutOfRange);
     }
   }
 
@@ -427,21 +416,35 @@ __global__ void __launch_bounds__(kThreads, OAA_WAVES_GEMM) cgemm_mfma_kernel(Ge
       sb.store(Bsr[buf ^ 1], Bsi[buf ^ 1], BC);
     }
     if (ck + kKC >= cur.ke) {
-      // 16 x 16 result block: lane holds rows 4*(lane/16) + r, r < 4, of column lane % 16
+      // 16 x 16 result block: lane holds rows 4*(lane/16) + r, r < 4, of column
+      // lane % 16; each bin's matrix is under 2^28 elements (32-bit offsets)
       float2* Cm = p.C + size_t(cur.f) * p.c_fstride + size_t(cur.split) * p.c_sstride;
+      const unsigned ldc = unsigned(p.ldc);
+      const int mb = cur.m0 + wm + 4 * lk, nb = cur.n0 + wn + lr;
+      auto result = [&](int i, int j, int r) {
+        return make_float2(p1[i][j][r] - p2[i][j][r], p3[i][j][r] - p1[i][j][r] - p2[i][j][r]);
+      };
+      if (cur.m0 + TM <= p.M && cur.n0 + TN <= p.N) {
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int nn = cur.n0 + wn + 16 * j + lr;
+        for (int i = 0; i < MB; ++i)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int m = cur.m0 + wm + 16 * i + 4 * lk + r;
-            const float re = p1[i][j][r] - p2[i][j][r];
-            const float im = p3[i][j][r] - p1[i][j][r] - p2[i][j][r];
-            if (m < p.M && nn < p.N) Cm[size_t(m) * p.ldc + nn] = make_float2(re, im);
+            float2* row = Cm + unsigned(mb + 16 * i + r) * ldc + unsigned(nb);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) row[16 * j] = result(i, j, r);
           }
-        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = mb + 16 * i + r;
+            float2* row = Cm + unsigned(m) * ldc + unsigned(nb);
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+              if (m < p.M && nb + 16 * j < p.N) row[16 * j] = result(i, j, r);
+          }
+      }
       zero();
     }
     __syncthreads();
@@ -529,7 +532,10 @@ hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s) {
 }
 
 // The matrix-core path reads each bin's operands through 32-bit byte offsets.
-bool mfma_fits(const GemmParams& p) { return p.a_fstride < (size_t(1) << 28) && p.b_fstride < (size_t(1) << 28); }
+bool mfma_fits(const GemmParams& p) {
+  const size_t lim = size_t(1) << 28;
+  return p.a_fstride < lim && p.b_fstride < lim && p.c_fstride < lim && size_t(p.M) * size_t(p.ldc) < lim;
+}
 
 bool mfma_preferred(const GemmParams& p) { return p.M >= 32 && p.N >= 32 && p.Kr >= 16 && mfma_fits(p); }
 

@@ -121,8 +121,8 @@ hipError_t launch_cgemm_narrow(const GemmParams& p, hipStream_t s);
 bool narrow_supported(const GemmParams& p);
 // Shape rule of the automatic choice between the tiled contractions.
 bool mfma_preferred(const GemmParams& p);
-// Whether the matrix-core engine can address the operands (each bin's matrix
-// under 2 GiB).
+// Whether the matrix-core engine can address its operands and result with
+// 32-bit offsets (each bin's matrices under 2^28 complex elements).
 bool mfma_fits(const GemmParams& p);
 
 }  // namespace oaa

@@ -11,7 +11,12 @@ and the direct-convolution-equivalent rate, the shape of those curves.
 Kernel sides above 32 need transforms longer than 64 and are skipped; the
 number of kernels of the input-size sweep is not stated and is taken as 100.
 
-    python -m paper_1601_06815_amd.sweeps [--sweep kernels|ksize|input|all] [--tiling paper|auto]
+--tiling fftconv runs the paper's FFTconv baseline (Section 2): the whole
+plane as a single block, zero-padded to L >= N + n - 1, which the library
+expresses as the tiling (L, L - n + 1) with one block per plane. Planes that
+would need L > 64 are skipped.
+
+    python -m paper_1601_06815_amd.sweeps [--sweep kernels|ksize|input|all] [--tiling paper|auto|fftconv]
 
 prints one JSON line per configuration.
 """
@@ -34,6 +39,15 @@ def sweep_configs(which):
     if which in ("input", "all"):       # Section 3.4: 5 x 5 kernels, sides 4 .. 256
         out += [("input", 1, 1, 100, N, 5) for N in range(8, 257, 8)]
     return out
+
+
+def fftconv_tiling(N, n):
+    """(L, b) of a single block covering the N x N plane, or None if the
+    linear convolution needs a transform longer than 64."""
+    L = 2
+    while L < N + n - 1:
+        L *= 2
+    return (L, L - n + 1) if L <= 64 else None
 
 
 def time_layer(torch, B, C, K, N, n, tiling, reps):
@@ -72,12 +86,17 @@ def time_layer(torch, B, C, K, N, n, tiling, reps):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--sweep", default="all", choices=["kernels", "ksize", "input", "all"])
-    ap.add_argument("--tiling", default="paper", choices=["paper", "auto"])
+    ap.add_argument("--tiling", default="paper", choices=["paper", "auto", "fftconv"])
     ap.add_argument("--reps", type=int, default=20)
     args = ap.parse_args(argv)
     import torch
     for name, B, C, K, N, n in sweep_configs(args.sweep):
-        t, geo, ly = time_layer(torch, B, C, K, N, n, args.tiling, args.reps)
+        tiling = args.tiling
+        if tiling == "fftconv":
+            tiling = fftconv_tiling(N, n)
+            if tiling is None:
+                continue
+        t, geo, ly = time_layer(torch, B, C, K, N, n, tiling, args.reps)
         direct = ly.direct_flops()
         print(json.dumps({"sweep": name, "B": B, "C": C, "K": K, "N": N, "n": n, "L": geo["L"], "b": geo["b"],
                           "fwd_ms": round(t["fwd"], 4), "bwd_ms": round(t["bwd"], 4),

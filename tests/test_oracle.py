@@ -251,6 +251,24 @@ def test_oaa_block_pitch_other_than_n(shape):
                 assert relerr(oaa.backward_data(g, w, N, L, 2 * b, b), oracle.conv_backward_data(g, w, N)) < 1e-12
 
 
+@pytest.mark.parametrize("shape", [(1, 2, 3, 12, 5), (2, 1, 2, 9, 3), (1, 3, 2, 20, 7)])
+def test_oaa_single_block_is_fftconv(shape):
+    """With one block per plane (b >= N) the OaA steps are the paper's FFTconv
+    (Section 2): the whole plane zero-padded to L >= N + n - 1, one product of
+    spectra, one inverse. Pinned against the explicit-DFT convolution at the
+    same transform size."""
+    B, C, K, N, n = shape
+    x, w, _ = _rand(shape, 11 + sum(shape))
+    L = 2
+    while L < N + n - 1:
+        L *= 2
+    b = L - n + 1
+    assert oaa.block_grid(N, b) == 1
+    got = oaa.forward(x, w, L=L, b=b)
+    ref = oracle.dft_conv_forward(x, w, Lc=L)
+    assert np.max(np.abs(got - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
 def test_oaa_tiling_rejects_overlapping_neighbours():
     x = np.zeros((1, 1, 20, 20))
     with pytest.raises(ValueError):

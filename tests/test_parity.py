@@ -144,6 +144,27 @@ def test_tiled_layers_all_passes(gpu_lib, shape):
     check_whole(x, w, g, tiling=(L, b))
 
 
+FFTCONV = [  # (B, C, K, N, n, L): one block per plane, L >= N + n - 1 (the paper's FFTconv)
+    (1, 3, 4, 32, 5, 64),
+    (2, 2, 3, 13, 4, 16),
+    (1, 4, 5, 20, 7, 32),
+    (2, 6, 70, 30, 3, 32),
+    (1, 2, 2, 1, 1, 2),
+    (3, 40, 36, 25, 8, 32),
+]
+
+
+@pytest.mark.parametrize("shape", FFTCONV, ids=lambda s: "x".join(map(str, s)))
+def test_single_block_fftconv(gpu_lib, shape):
+    """The paper's FFTconv baseline as the library's single-block tiling
+    (L, L - n + 1): every pass against the oracle."""
+    B, C, K, N, n, L = shape
+    b = L - n + 1
+    assert -(-N // b) == 1
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=41 + sum(shape))
+    check_whole(x, w, g, tiling=(L, b))
+
+
 @pytest.mark.parametrize("name", ["tiny", "plane224_n3", "plane224_n5", "plane224_n8"])
 def test_named_small_layers(gpu_lib, name):
     ly = LAYERS[name]
@@ -285,3 +306,41 @@ def test_named_stream_is_used(gpu_lib):
         y = plan.forward(xd, wd)
     s.synchronize()
     assert relerr(y.cpu().numpy(), oracle.conv_forward(x, w)) <= TOL
+
+
+def test_autograd_function_matches_oracle(gpu_lib):
+    """OaAConv2dFunction: y and both gradients of <y, g> through autograd,
+    against the oracle; two forwards before one backward recompute the
+    cached spectra."""
+    from paper_1601_06815_amd.autograd import OaAConv2d, OaAConv2dFunction
+    B, C, K, N, n = 2, 3, 5, 21, 4
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=77)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling="auto")
+    xd = to_dev(x).requires_grad_(True)
+    wd = to_dev(w).requires_grad_(True)
+    y = OaAConv2dFunction.apply(xd, wd, plan)
+    # a second forward on the same plan with other inputs
+    x2, w2, _ = make_inputs(Layer("t", B, C, K, N, n), seed=78)
+    OaAConv2dFunction.apply(to_dev(x2), to_dev(w2), plan)
+    (y * to_dev(g)).sum().backward()
+    torch.cuda.synchronize()
+    e = (relerr(y.detach().cpu().numpy(), oracle.conv_forward(x, w)),
+         relerr(xd.grad.cpu().numpy(), oracle.conv_backward_data(g, w, N)),
+         relerr(wd.grad.cpu().numpy(), oracle.conv_backward_filter(x, g, n)))
+    print(f"autograd rel err fwd {e[0]:.2e} dx {e[1]:.2e} dw {e[2]:.2e}", flush=True)
+    assert max(e) <= TOL, e
+    # the layer module: same three results against torch's float64 autograd on
+    # the CPU (cross-correlation with the flipped kernel)
+    layer = OaAConv2d(C, K, n, device=DEV)
+    with torch.no_grad():
+        layer.weight.copy_(to_dev(w))
+    xd2 = to_dev(x).requires_grad_(True)
+    yl = layer(xd2)
+    (yl * to_dev(g)).sum().backward()
+    xr = torch.from_numpy(x).double().requires_grad_(True)
+    wr = torch.from_numpy(w).double().requires_grad_(True)
+    yr = torch.nn.functional.conv2d(xr, wr.flip(-1, -2))
+    (yr * torch.from_numpy(g).double()).sum().backward()
+    assert relerr(yl.detach().cpu().numpy(), yr.detach().numpy()) <= TOL
+    assert relerr(xd2.grad.cpu().numpy(), xr.grad.numpy()) <= TOL
+    assert relerr(layer.weight.grad.cpu().numpy(), wr.grad.numpy()) <= TOL

@@ -25,6 +25,10 @@ oaa
     step in the paper's order: divide into n x n blocks, zero-pad, transform,
     Hadamard product with channel sum, inverse transform, overlap by n-1 and
     add. Its intermediate spectra are what the GPU stages are compared with.
+oas
+    The output-tiled alternative: overlap-and-save forward over L x L windows
+    of x at hop L - n + 1, the error propagation as overlap-and-add over
+    blocks of g, and the weight gradient from the same windows and blocks.
 
 Every function states the passage it follows. Pins (tests/test_oracle.py)
 tie each function to library routines, closed forms and invariants that are
@@ -35,3 +39,4 @@ from .direct import (conv_forward, conv_backward_data, conv_backward_filter,  # 
                      conv_forward_at, conv_backward_data_at, conv_backward_filter_at)
 from .dft import dft_conv_forward  # noqa: F401
 from . import oaa  # noqa: F401
+from . import oas  # noqa: F401

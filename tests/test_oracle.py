@@ -18,7 +18,7 @@ import scipy.signal
 import torch
 
 import oracle
-from oracle import oaa
+from oracle import oaa, oas
 from tests.conftest import relerr
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
@@ -318,3 +318,59 @@ def test_half_spectrum_edge_columns_are_hermitian():
     # the other columns are not symmetric: the skipped set is exactly these two
     col = Xh[..., 1]
     assert not np.allclose(col, np.conj(col[..., (-np.arange(L)) % L]))
+
+
+# ---------------------------------------------------------------------------
+# output-tiled alternative (overlap-and-save forward)
+
+@pytest.mark.parametrize("Lmode", ["min", "double"])
+@pytest.mark.parametrize("shape", SHAPES + [(2, 3, 4, 40, 16)])
+def test_oas_passes_equal_direct_definition(shape, Lmode):
+    """Overlap-and-save forward over windows at hop L - n + 1, the error
+    propagation as overlap-and-add over g blocks, and the weight gradient
+    from windows and blocks: all equal the plain definitions."""
+    x, w, g = _rand(shape, 23 + sum(shape))
+    B, C, K, N, n = shape
+    L = oaa.fft_size(n) * (2 if Lmode == "double" else 1)
+    assert relerr(oas.forward(x, w, L), oracle.conv_forward(x, w)) <= 1e-13
+    assert relerr(oas.backward_data(g, w, N, L), oracle.conv_backward_data(g, w, N)) <= 1e-13
+    assert relerr(oas.backward_filter(x, g, n, L), oracle.conv_backward_filter(x, g, n)) <= 1e-13
+
+
+def test_oas_window_count_tiles_the_output():
+    """T = ceil(M / h) windows per side with h = L - n + 1: for the 128 x 128
+    layer with 16 x 16 kernels at L = 32, 7 windows against 8 blocks."""
+    assert oas.hop(16, 32) == 17 and oas.grid(113, 17) == 7 and oaa.block_grid(128, 16) == 8
+    x = np.zeros((1, 1, 20, 20))
+    assert oas.window_spectra(x, 5, 16).shape[2] == oas.grid(16, 12) == 2
+
+
+@pytest.mark.parametrize("n,L", [(1, 2), (3, 8), (4, 8), (5, 16), (16, 32)])
+def test_flipped_kernel_spectrum_is_phase_times_conjugate(n, L):
+    """For a real kernel, the spectrum of w flipped in both axes (padded at
+    [0, n)) is exp(-2 pi i (n-1)(u+v)/L) times the conjugate spectrum of w:
+    the identity that lets the error propagation reuse the kernel spectra."""
+    rng = np.random.default_rng(n + L)
+    w = rng.standard_normal((2, 3, n, n))
+    u = np.arange(L)[:, None]
+    v = np.arange(L // 2 + 1)[None, :]
+    phase = np.exp(-2j * np.pi * (n - 1) * (u + v) / L)
+    got = oas.kernel_spectra(w, L, flip=True)
+    ref = phase * np.conj(oas.kernel_spectra(w, L))
+    assert np.max(np.abs(got - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("shape", [(1, 3, 4, 32, 5), (2, 2, 3, 13, 4), (1, 1, 2, 10, 6), (2, 3, 2, 11, 1)])
+def test_oas_weight_gradient_with_conjugated_windows(shape):
+    """The same weight gradient with the conjugate on the window spectra:
+    the inverse then holds dw[u][v] at rows and columns (h + u) mod L,
+    (h + v) mod L (the orientation of the library's contraction)."""
+    x, _, g = _rand(shape, 5 + sum(shape))
+    B, C, K, N, n = shape
+    L = oaa.fft_size(n)
+    h = oas.hop(n, L)
+    dWh = np.einsum('bkpquv,bcpquv->kcuv', oas.block_spectra(g, n, L), np.conj(oas.window_spectra(x, n, L)))
+    c = np.fft.irfft2(dWh, s=(L, L))
+    idx = (h + np.arange(n)) % L
+    got = c[:, :, idx][:, :, :, idx]
+    assert relerr(got, oracle.conv_backward_filter(x, g, n)) <= 1e-13

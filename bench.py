@@ -213,6 +213,9 @@ def main():
     ap.add_argument("--tiling", default="auto",
                     help="auto: the library's block size (fewer, larger blocks where that cuts work); "
                          "paper: blocks of the kernel's size n; L:b an explicit transform side and block")
+    ap.add_argument("--method", default="oaa", choices=["oaa", "oas"],
+                    help="oaa: the paper's overlap-and-add tiling; oas: the output-tiled alternative "
+                         "(overlap-and-save forward, overlap-add of gradient blocks)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--stages-out", default=None, help="also write per-stage timings as JSON here")
@@ -258,7 +261,10 @@ def main():
     which = {"auto": binding.CONTRACTION_AUTO, "valu": binding.CONTRACTION_VALU,
              "mfma": binding.CONTRACTION_MFMA, "narrow": binding.CONTRACTION_NARROW}[args.contraction]
     tiling = args.tiling if args.tiling in ("auto", "paper") else tuple(int(v) for v in args.tiling.split(":"))
-    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which, tiling=tiling)
+    method = binding.METHOD_OVERLAP_SAVE if args.method == "oas" else binding.METHOD_OVERLAP_ADD
+    if method == binding.METHOD_OVERLAP_SAVE and isinstance(tiling, tuple):
+        tiling = (tiling[0], 0)
+    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=dev, contraction=which, tiling=tiling, method=method)
     geo = plan.geometry
     xd, wd, gd = (torch.from_numpy(a).to(dev) for a in (x, w, g))
     y = torch.empty((ly.B, ly.K, ly.M, ly.M), dtype=torch.float32, device=dev)
@@ -348,6 +354,7 @@ def main():
                                f"valid stride 1, forward + backward_data + backward_filter",
                    "B": ly.B, "C": ly.C, "K": ly.K, "N": ly.N, "n": ly.n,
                    "L": geo["L"], "block": geo["b"], "T": geo["T"], "split": geo["split"], "tiling": args.tiling,
+                   "method": args.method,
                    "contraction": args.contraction},
         "roofline": roof,
         "stages": per_stage,

@@ -66,14 +66,34 @@ typedef enum {
 typedef struct {
   int B, C, K, N, n;
   int M;      /* output side, N - n + 1                                      */
-  int T;      /* blocks per side, ceil(N / b)                                */
+  int T;      /* blocks per side: ceil(N / b), or ceil(M / b) for overlap-save */
   int P;      /* blocks per plane, T * T                                     */
   int L;      /* transform side (oaa_plan_create: smallest power of two
                  >= 2n - 1, at least 2)                                      */
   int F;      /* stored frequency bins per tile, L * (L/2 + 1)               */
   int split;  /* partial sums of the weight-gradient contraction             */
   int b;      /* block pitch: blocks are b x b (oaa_plan_create: b = n)      */
+  int method; /* oaa_method_t of the plan                                    */
 } oaa_geometry_t;
+
+/* How the passes are tiled (oaa_plan_create_method).
+ *
+ * OAA_METHOD_OVERLAP_ADD: the paper's method (Section 2). The forward pass
+ *   cuts x into b x b blocks, T = ceil(N / b) per side, and overlap-adds the
+ *   block results; the backward passes read g in windows of side up to 2b
+ *   that start every b (the adjoint of the overlap-add).
+ * OAA_METHOD_OVERLAP_SAVE: the alternative the paper names beside OaA
+ *   (Introduction), every pass tiled by the output side M with hop
+ *   h = L - n + 1 (reported as b), T = ceil(M / h) per side. The forward pass
+ *   transforms L x L windows of x starting every h and keeps rows and columns
+ *   [n-1, L) of each inverse (overlap-and-save); the error propagation cuts g
+ *   into h x h blocks and overlap-adds their results into dx (OaA applied to
+ *   that convolution); the weight gradient pairs the same windows and blocks.
+ *   The X and G regions then hold window and block spectra respectively. */
+typedef enum {
+  OAA_METHOD_OVERLAP_ADD = 0,
+  OAA_METHOD_OVERLAP_SAVE = 1
+} oaa_method_t;
 
 /* Workspace regions (see oaa_plan_region). Every spectrum is complex64
  * (re, im interleaved) and bin-major: bin f = u * (L/2 + 1) + v holds row
@@ -133,6 +153,14 @@ oaa_status_t oaa_plan_create(oaa_plan_t* plan, int B, int C, int K, int N, int n
  * and b by a work estimate of contraction and transforms. Larger blocks
  * mean fewer tiles: fewer spectra to transform, store and contract. */
 oaa_status_t oaa_plan_create_tiled(oaa_plan_t* plan, int B, int C, int K, int N, int n, int L, int b);
+
+/* Same, with a choice of method (oaa_method_t). For OAA_METHOD_OVERLAP_ADD
+ * this is oaa_plan_create_tiled. For OAA_METHOD_OVERLAP_SAVE, L is a power of
+ * two in [max(2, 2n-1 rounded up), 64], or 0 for the library's choice between
+ * that side and twice it; b must be 0 or L - n + 1 (the hop). An unknown
+ * method is OAA_ERR_INVALID_ARG. */
+oaa_status_t oaa_plan_create_method(oaa_plan_t* plan, int B, int C, int K, int N, int n, int L, int b,
+                                    oaa_method_t method);
 
 /* Release the host structure (and any timing events). NULL is a no-op.
  * Does not free the workspace. */

@@ -17,6 +17,7 @@ STATUS = {0: "OAA_OK", 1: "OAA_ERR_INVALID_ARG", 2: "OAA_ERR_UNSUPPORTED",
           3: "OAA_ERR_NO_WORKSPACE", 4: "OAA_ERR_NO_CACHE", 5: "OAA_ERR_HIP"}
 REGION_W_SPECTRUM, REGION_X_SPECTRUM, REGION_G_SPECTRUM, REGION_PRODUCT = 0, 1, 2, 3
 CONTRACTION_AUTO, CONTRACTION_VALU, CONTRACTION_MFMA, CONTRACTION_NARROW = 0, 1, 2, 3
+METHOD_OVERLAP_ADD, METHOD_OVERLAP_SAVE = 0, 1
 STAGES = ["w_spectrum", "x_spectrum", "g_spectrum", "fwd_product", "fwd_inverse",
           "bwd_data_product", "bwd_data_inverse", "bwd_filter_product", "bwd_filter_inverse"]
 
@@ -25,12 +26,15 @@ _c_int, _c_size, _vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
 
 
 class Geometry(ctypes.Structure):
-    _fields_ = [(k, ctypes.c_int) for k in ("B", "C", "K", "N", "n", "M", "T", "P", "L", "F", "split", "b")]
+    _fields_ = [(k, ctypes.c_int) for k in ("B", "C", "K", "N", "n", "M", "T", "P", "L", "F", "split", "b",
+                                            "method")]
 
 
 SIGNATURES = {
     "oaa_plan_create": (_c_int, [ctypes.POINTER(_vp), _c_int, _c_int, _c_int, _c_int, _c_int]),
     "oaa_plan_create_tiled": (_c_int, [ctypes.POINTER(_vp), _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int]),
+    "oaa_plan_create_method": (_c_int, [ctypes.POINTER(_vp), _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                        _c_int]),
     "oaa_plan_destroy": (_c_int, [_vp]),
     "oaa_plan_geometry": (_c_int, [_vp, ctypes.POINTER(Geometry)]),
     "oaa_plan_workspace_bytes": (_c_size, [_vp]),
@@ -93,6 +97,12 @@ def oaa_plan_create(B, C, K, N, n):
 def oaa_plan_create_tiled(B, C, K, N, n, L, b):
     h = _vp()
     _check(load().oaa_plan_create_tiled(ctypes.byref(h), B, C, K, N, n, L, b))
+    return h.value
+
+
+def oaa_plan_create_method(B, C, K, N, n, L, b, method):
+    h = _vp()
+    _check(load().oaa_plan_create_method(ctypes.byref(h), B, C, K, N, n, L, b, method))
     return h.value
 
 
@@ -164,11 +174,18 @@ class Plan:
     workspace tensor. Calls enqueue on torch's current stream of the tensors'
     device and return without synchronising."""
 
-    def __init__(self, B, C, K, N, n, device="cuda", contraction=CONTRACTION_AUTO, tiling="paper"):
+    def __init__(self, B, C, K, N, n, device="cuda", contraction=CONTRACTION_AUTO, tiling="paper",
+                 method=METHOD_OVERLAP_ADD):
         """tiling: "paper" (blocks of n, oaa_plan_create), "auto" (the
-        library's choice) or an (L, b) pair (oaa_plan_create_tiled)."""
+        library's choice) or an (L, b) pair (oaa_plan_create_tiled).
+        method=METHOD_OVERLAP_SAVE: the output-tiled passes
+        (oaa_plan_create_method); tiling "auto"/"paper" or (L, b) with b 0 or
+        L - n + 1."""
         import torch
-        if tiling == "paper":
+        if method != METHOD_OVERLAP_ADD:
+            L, b = (0, 0) if tiling in ("paper", "auto") else tiling
+            self.handle = oaa_plan_create_method(B, C, K, N, n, L, b, method)
+        elif tiling == "paper":
             self.handle = oaa_plan_create(B, C, K, N, n)
         elif tiling == "auto":
             self.handle = oaa_plan_create_tiled(B, C, K, N, n, 0, 0)

@@ -226,10 +226,11 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
   const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
   const unsigned rest = wg / p.nchunk;
-  const int strip = int(rest % T);
-  const unsigned plane = rest / T;
+  const int To = p.To, sh = p.shift;
+  const int strip = int(rest % To);
+  const unsigned plane = rest / To;
   const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
-  const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
+  const int q0 = chunk * p.TQ, nq = min(p.TQ, To - q0);
   const size_t tiles_per_ch = size_t(p.n_img) * T * T;
   const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
   const size_t ustride = size_t(V) * fstride;
@@ -245,7 +246,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
       const int qq = base % (nq + 1), rest2 = base / (nq + 1);
       const int v = rest2 % V, part = rest2 / V;
       const int Qt = q0 - 1 + qq, Pt = strip - part;
-      const bool live = Qt >= 0 && Pt >= 0 && (part == 0 || na > 0);
+      const bool live = Qt >= 0 && Qt < T && Pt >= 0 && Pt < T && (part == 0 || na > 0);
       const float2* col = in + size_t(live ? Pt : 0) * T + (live ? Qt : 0) + size_t(v) * fstride;
       const bool mir = v == 0 || v == L / 2;
       float re[HL], im[HL];
@@ -258,7 +259,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
       const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
 #pragma unroll
       for (int m = 0; m < HL; ++m) {
-        const int r = 2 * m + h;
+        const int r = (2 * m + h + sh) & (L - 1);
         const float2 val = make_float2(re[bitrev(m, HL)] * rs, im[bitrev(m, HL)] * is);
         if (part == 0) {
           if (r < b) zc[qq * TSc + v + r * V] = val;
@@ -273,7 +274,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
     const int qq = task % (nq + 1), rest2 = task / (nq + 1);
     const int v = rest2 % V, part = rest2 / V;
     const int Qt = q0 - 1 + qq, Pt = strip - part;
-    const bool live = Qt >= 0 && Pt >= 0 && (part == 0 || na > 0);
+    const bool live = Qt >= 0 && Qt < T && Pt >= 0 && Pt < T && (part == 0 || na > 0);
     const float2* col = in + size_t(live ? Pt : 0) * T + (live ? Qt : 0) + size_t(v) * fstride;
     // columns v = 0 and v = L/2 hold no products in rows u > L/2 (Hermitian
     // there): inverse of the rows [0, L/2] with rows 0, L/2 halved, twice
@@ -296,16 +297,21 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
     }
     fft_dif<L, +1, false>(re, im);
     const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
+    // row r of the inverse is row (r + shift) mod L of the tile
     if (part == 0) {
       float2* zt = zc + qq * TSc + v;
 #pragma unroll
-      for (int r = 0; r < L; ++r)
-        if (r < b) zt[r * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+      for (int r = 0; r < L; ++r) {
+        const int rt = (r + sh) & (L - 1);
+        if (rt < b) zt[rt * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+      }
     } else {
       float2* zt = za + qq * TSa + v;
 #pragma unroll
-      for (int r = 0; r < L; ++r)
-        if (r >= b && r < S) zt[(r - b) * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+      for (int r = 0; r < L; ++r) {
+        const int rt = (r + sh) & (L - 1);
+        if (rt >= b && rt < S) zt[(rt - b) * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+      }
     }
   }
   __syncthreads();
@@ -328,7 +334,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
       float* d0 = reinterpret_cast<float*>(const_cast<float2*>(zt));
 #pragma unroll
       for (int m = 0; m < HL; ++m) {
-        const int sx = 2 * m + h;
+        const int sx = (2 * m + h + sh) & (L - 1);
         if (sx < S) {
           d0[sx] = zr[bitrev(m, HL)] * scale;
           if (has1) d0[RS + sx] = zi[bitrev(m, HL)] * scale;
@@ -353,9 +359,10 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
     float* d0 = reinterpret_cast<float*>(const_cast<float2*>(zt));  // this task's own two rows
 #pragma unroll
     for (int s = 0; s < L; ++s) {
-      if (s < S) {
-        d0[s] = zr[bitrev(s, L)] * scale;
-        if (has1) d0[RS + s] = zi[bitrev(s, L)] * scale;
+      const int st = (s + sh) & (L - 1);  // column s of the inverse is column st of the tile
+      if (st < S) {
+        d0[st] = zr[bitrev(s, L)] * scale;
+        if (has1) d0[RS + st] = zi[bitrev(s, L)] * scale;
       }
     }
   }
@@ -388,6 +395,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
 template <int L>
 hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
+  if (p.To != p.T || p.shift != 0) return hipErrorInvalidValue;
   const int TS = odd_at_least((L / 2 + 1) * V);
   const size_t zb = size_t(TS) * 8;                 // column transforms of one tile
   const size_t ob = size_t(p.n) * (p.n | 1) * 4;    // output block of one tile
@@ -411,17 +419,17 @@ template <int L>
 hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   const int b = p.n, S = p.S, na = S - b;
-  if (na < 0 || S > L || 2 * b <= L) return hipErrorInvalidValue;
+  if (na < 0 || S > L || 2 * b <= L || p.To < p.T || p.shift < 0 || p.shift >= L) return hipErrorInvalidValue;
   const size_t per_tile = size_t(odd_at_least(b * V) + odd_at_least(na * V)) * 8;
-  int tq = std::min<int>(p.T, int(kLdsBudget / per_tile) - 1);
+  int tq = std::min<int>(p.To, int(kLdsBudget / per_tile) - 1);
   if (tq < 1) return hipErrorInvalidConfiguration;
-  const int nchunk = (p.T + tq - 1) / tq;
-  p.TQ = (p.T + nchunk - 1) / nchunk;
+  const int nchunk = (p.To + tq - 1) / tq;
+  p.TQ = (p.To + nchunk - 1) / nchunk;
   p.nchunk = nchunk;
   const long planes = long(p.n_img) * p.n_ch;
   const size_t lds = per_tile * (p.TQ + 1);
   const int tasks = (L >= 64 ? 2 : 1) * std::max(2 * (p.TQ + 1) * V, (p.TQ + 1) * ((b + 1) / 2 + (na + 1) / 2));
-  const long nwg = planes * p.T * p.nchunk;
+  const long nwg = planes * p.To * p.nchunk;
   hipLaunchKernelGGL(irfft2_overlap_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }

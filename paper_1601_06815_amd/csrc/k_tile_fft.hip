@@ -460,7 +460,7 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
   constexpr int RT = FULL ? L : L / 2;  // rows kept from the column transforms (>= n)
   extern __shared__ float smem[];
   const int tid = threadIdx.x, nthr = blockDim.x;
-  const int n = p.n, H = p.H;
+  const int n = p.n, H = p.H, org = p.origin;
   const int TS = odd_at_least((RT + 1) * V);
   const int OS = n | 1;  // obuf stride between tiles, odd
   float2* zbuf = reinterpret_cast<float2*>(smem);                   // [TQ][TS]
@@ -520,16 +520,17 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
       const int h = task & 1, base = task >> 1;
       const int q = base % nq, pr = base / nq;
       const int r0 = 2 * pr;
-      const float2* zt = zbuf + q * TS + r0 * V;
+      const float2* za = zbuf + q * TS + ((org + r0) & (L - 1)) * V;
+      const float2* zb = zbuf + q * TS + ((org + r0 + 1) & (L - 1)) * V;
       const bool has1 = r0 + 1 < n;
       float zr[HL], zi[HL];
-      irfft_pair_split<L>([&](int v) { return zt[v]; },
-                          [&](int v) { return has1 ? zt[V + v] : make_float2(0.f, 0.f); }, zr, zi, h);
+      irfft_pair_split<L>([&](int v) { return za[v]; },
+                          [&](int v) { return has1 ? zb[v] : make_float2(0.f, 0.f); }, zr, zi, h);
       float* o0 = obuf + (size_t(r0) * p.TQ + q) * OS;
       float* o1 = o0 + size_t(p.TQ) * OS;
 #pragma unroll
       for (int m = 0; m < HL; ++m) {
-        const int sx = 2 * m + h;
+        const int sx = (2 * m + h - org) & (L - 1);  // column 2m + h of the inverse
         if (sx < n) {
           o0[sx] = zr[bitrev(m, HL)] * scale;
           if (has1) o1[sx] = zi[bitrev(m, HL)] * scale;
@@ -543,13 +544,14 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
   for (int task = tid; task < (SPLIT ? 0 : npair * nq); task += nthr) {
     const int q = task % nq, pr = task / nq;
     const int r0 = 2 * pr;
-    const float2* zt = zbuf + q * TS + r0 * V;
+    const float2* za = zbuf + q * TS + ((org + r0) & (L - 1)) * V;
+    const float2* zb = zbuf + q * TS + ((org + r0 + 1) & (L - 1)) * V;
     const bool has1 = r0 + 1 < n;
     float2 A[V], Bv[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) {
-      A[v] = zt[v];
-      Bv[v] = has1 ? zt[V + v] : make_float2(0.f, 0.f);  // no row n for odd n
+      A[v] = za[v];
+      Bv[v] = has1 ? zb[v] : make_float2(0.f, 0.f);  // no row n for odd n
     }
     float zr[L], zi[L];
     irfft_pair<L>(A, Bv, zr, zi);
@@ -557,10 +559,11 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
     float* o1 = o0 + size_t(p.TQ) * OS;
 #pragma unroll
     for (int s = 0; s < (FULL ? L : L / 2); ++s) {
-      if (s < n) {
+      const int c = (s - org) & (L - 1);  // column s of the inverse is kept column c
+      if (c < n) {
         const int pos = bitrev(s, L);
-        o0[s] = zr[pos] * scale;
-        if (has1) o1[s] = zi[pos] * scale;
+        o0[c] = zr[pos] * scale;
+        if (has1) o1[c] = zi[pos] * scale;
       }
     }
   }
@@ -660,7 +663,9 @@ hipError_t launch_crop_LF(CropParams p, hipStream_t s) {
 // blocks of more than L/2 rows need every row of the column transforms
 template <int L>
 hipError_t launch_crop_L(const CropParams& p, hipStream_t s) {
-  if (p.n > L / 2) return launch_crop_LF<L, true>(p, s);
+  if (p.origin < 0 || p.origin >= L || p.n > L) return hipErrorInvalidValue;
+  // the kept rows [origin, origin + n) (mod L) within the first half, or all rows
+  if (p.origin + p.n > L / 2) return launch_crop_LF<L, true>(p, s);
   return launch_crop_LF<L, false>(p, s);
 }
 

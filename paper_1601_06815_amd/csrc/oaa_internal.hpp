@@ -31,8 +31,9 @@ struct TileFwdParams {
 };
 
 // Spectra (optionally the sum of `nsplit` partial spectra spaced
-// `split_stride` elements apart) -> inverse transform -> top-left n x n of
-// each tile written to block (P, Q) of dst[n_img][n_ch][H][H], clipped to H.
+// `split_stride` elements apart) -> inverse transform -> the n x n window of
+// each tile whose rows and columns start at `origin` (taken modulo L) written
+// to block (P, Q) of dst[n_img][n_ch][H][H] at (P n, Q n), clipped to H.
 struct CropParams {
   const float2* src;  // [nsplit][F][n_ch][n_img * T * T]
   int nsplit;
@@ -40,6 +41,7 @@ struct CropParams {
   float* dst;         // [n_img][n_ch][H][H]
   int n_img, n_ch;
   int H, n, T;
+  int origin;         // first kept row and column of a tile, in [0, L)
   int TQ, nchunk;
 };
 
@@ -64,6 +66,10 @@ struct FoldCropParams {
   int n_img, n_ch;
   int M, n, off, T;   // n: block pitch b (block side); off: n_kernel - 1
   int S;              // support of a block result, b + n_kernel - 1 (<= L)
+  int To;             // output blocks per side (T, or T + 1 when the last
+                      // tiles' overhang reaches past T b)
+  int shift;          // each tile is the inverse transform circularly shifted
+                      // down and right by `shift` (0 for the forward pass)
   int TQ, nchunk, SPW, ngroups;
 };
 

@@ -18,7 +18,9 @@
 
 struct oaa_plan_s {
   int B, C, K, N, n;
-  int b;  // block pitch (block side); the paper's tiling has b = n
+  int method;  // oaa_method_t
+  int b;  // block pitch (block side); the paper's tiling has b = n; the hop
+          // L - n + 1 for overlap-save
   int M, T, P, L, F;
   int split, kchunk;
   size_t off[4];
@@ -132,6 +134,23 @@ oaa_status_t run_filter_fft(oaa_plan_t p, const float* w, hipStream_t s) {
 }
 
 oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
+  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
+    // L x L windows of x starting every h = L - n + 1
+    oaa::WindowParams t{};
+    t.src = x;
+    t.dst = region(p, OAA_REGION_X_SPECTRUM);
+    t.n_img = p->B;
+    t.n_ch = p->C;
+    t.H = p->N;
+    t.n = p->b;
+    t.S = p->L;
+    t.off = 0;
+    t.T = p->T;
+    oaa_status_t st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input window spectra",
+                            [&] { return oaa::launch_window_rfft2(p->L, t, s); });
+    if (st == OAA_OK) p->x_valid = true;
+    return st;
+  }
   oaa::TileFwdParams t{};
   t.src = x;
   t.dst = region(p, OAA_REGION_X_SPECTRUM);
@@ -149,6 +168,23 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
 }
 
 oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
+  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
+    // h x h blocks of g, h = L - n + 1
+    oaa::TileFwdParams t{};
+    t.src = g;
+    t.dst = region(p, OAA_REGION_G_SPECTRUM);
+    t.n_img = p->B;
+    t.n_ch = p->K;
+    t.H = p->M;
+    t.pitch = p->b;
+    t.off = 0;
+    t.R = p->b;
+    t.T = p->T;
+    oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient block spectra",
+                            [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+    if (st == OAA_OK) p->g_valid = true;
+    return st;
+  }
   // window (P,Q) of the zero-framed gradient: g[P*n + r - (n-1)][Q*n + s - (n-1)],
   // r, s < 2n
   oaa::WindowParams t{};
@@ -221,6 +257,30 @@ void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   }
 }
 
+// Transform side for the output-tiled method: L0 (the smallest power of two
+// >= 2n-1) or 2 L0, with the work estimate of choose_tiling at the hop
+// L - n + 1 over the output side M.
+int choose_oas_side(int C, int K, int N, int n) {
+  const int L0 = pow2_at_least(2 * n - 1);
+  const int M = N - n + 1;
+  double best = 0;
+  int L = L0;
+  for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
+    int lg = 0;
+    while ((1 << lg) < Lc) ++lg;
+    const double eff = Lc <= 16 ? 1.0 : (Lc == 32 ? 1.5 : 3.0);
+    const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg) * 1.125;
+    const double con = 8.0 * C * K * oaa::unique_bins(Lc);
+    const double T = double((M + (Lc - n + 1) - 1) / (Lc - n + 1));
+    const double cost = T * T * (con + fft) * (Lc > L0 ? 1.1 : 1.0);
+    if (best == 0 || cost < best) {
+      best = cost;
+      L = Lc;
+    }
+  }
+  return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -245,27 +305,46 @@ oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n)
 }
 
 oaa_status_t oaa_plan_create_tiled(oaa_plan_t* out, int B, int C, int K, int N, int n, int L, int b) {
+  return oaa_plan_create_method(out, B, C, K, N, n, L, b, OAA_METHOD_OVERLAP_ADD);
+}
+
+oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N, int n, int L, int b,
+                                    oaa_method_t method) {
   if (!out) return fail(OAA_ERR_INVALID_ARG, "plan output pointer is NULL");
   *out = nullptr;
+  if (method != OAA_METHOD_OVERLAP_ADD && method != OAA_METHOD_OVERLAP_SAVE)
+    return fail(OAA_ERR_INVALID_ARG, "unknown method %d", (int)method);
   if (B < 1 || C < 1 || K < 1 || N < 1 || n < 1)
     return fail(OAA_ERR_INVALID_ARG, "dimensions must be positive (B=%d C=%d K=%d N=%d n=%d)", B, C, K, N, n);
   if (n > N) return fail(OAA_ERR_INVALID_ARG, "kernel side n=%d exceeds input side N=%d", n, N);
   if (n > 32) return fail(OAA_ERR_UNSUPPORTED, "kernel side n=%d > 32 (transform side would exceed 64)", n);
   if (L < 0 || b < 0) return fail(OAA_ERR_INVALID_ARG, "negative tiling (L=%d b=%d)", L, b);
-  if (L == 0 && b == 0) {
-    choose_tiling(B, C, K, N, n, L, b);
-  } else if (L == 0 || b == 0) {
-    return fail(OAA_ERR_INVALID_ARG, "give both L and b, or neither (L=%d b=%d)", L, b);
-  }
-  if (L < 2 || L > 64 || (L & (L - 1)))
-    return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
-  // block results (support b + n - 1) must fit the transform and may only
-  // reach the next block
-  if (b < (n > 1 ? n - 1 : 1) || b + n - 1 > L)
-    return fail(OAA_ERR_INVALID_ARG, "block pitch b=%d needs max(1, n-1) <= b <= L-n+1 (n=%d, L=%d)", b, n, L);
-
   const int M = N - n + 1;
-  const int T = (N + b - 1) / b;
+  int T = 0;
+  if (method == OAA_METHOD_OVERLAP_SAVE) {
+    if (L == 0) L = choose_oas_side(C, K, N, n);
+    if (L < 2 || L > 64 || (L & (L - 1)))
+      return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
+    if (L < 2 * n - 1)
+      return fail(OAA_ERR_INVALID_ARG, "overlap-save needs L >= 2n-1 (n=%d, L=%d)", n, L);
+    if (b != 0 && b != L - n + 1)
+      return fail(OAA_ERR_INVALID_ARG, "overlap-save hop b=%d must be 0 or L-n+1=%d", b, L - n + 1);
+    b = L - n + 1;
+    T = (M + b - 1) / b;
+  } else {
+    if (L == 0 && b == 0) {
+      choose_tiling(B, C, K, N, n, L, b);
+    } else if (L == 0 || b == 0) {
+      return fail(OAA_ERR_INVALID_ARG, "give both L and b, or neither (L=%d b=%d)", L, b);
+    }
+    if (L < 2 || L > 64 || (L & (L - 1)))
+      return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
+    // block results (support b + n - 1) must fit the transform and may only
+    // reach the next block
+    if (b < (n > 1 ? n - 1 : 1) || b + n - 1 > L)
+      return fail(OAA_ERR_INVALID_ARG, "block pitch b=%d needs max(1, n-1) <= b <= L-n+1 (n=%d, L=%d)", b, n, L);
+    T = (N + b - 1) / b;
+  }
   const long long P = (long long)T * T;
   const int F = L * (L / 2 + 1);
   const long long BP = (long long)B * P;
@@ -308,6 +387,7 @@ oaa_status_t oaa_plan_create_tiled(oaa_plan_t* out, int B, int C, int K, int N, 
   oaa_plan_s* p = new (std::nothrow) oaa_plan_s();
   if (!p) return fail(OAA_ERR_INVALID_ARG, "out of host memory");
   p->B = B; p->C = C; p->K = K; p->N = N; p->n = n; p->b = b;
+  p->method = (int)method;
   p->M = M; p->T = T; p->P = (int)P; p->L = L; p->F = F;
   p->split = (int)split;
   p->kchunk = (int)kchunk;
@@ -381,6 +461,7 @@ oaa_status_t oaa_plan_geometry(oaa_plan_t plan, oaa_geometry_t* out) {
   out->M = plan->M; out->T = plan->T; out->P = plan->P; out->L = plan->L; out->F = plan->F;
   out->b = plan->b;
   out->split = plan->split;
+  out->method = plan->method;
   return OAA_OK;
 }
 
@@ -444,11 +525,24 @@ oaa_status_t oaa_conv_forward(oaa_plan_t p, const float* x, const float* w, floa
   g.nsplit = 1; g.kchunk = p->C; g.c_sstride = 0;
   g.a_trans = true; g.a_conj = false; g.b_trans = false; g.b_conj = false;
   if ((st = run_gemm(p, g, OAA_STAGE_FWD_PRODUCT, s, "forward contraction"))) return st;
+  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
+    // rows and columns [n-1, L) of each window's inverse are its h x h outputs
+    oaa::CropParams c{};
+    c.src = region(p, OAA_REGION_PRODUCT);
+    c.nsplit = 1; c.split_stride = 0;
+    c.dst = y;
+    c.n_img = p->B; c.n_ch = p->K;
+    c.H = p->M; c.n = p->b; c.T = p->T;
+    c.origin = p->n - 1;
+    return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-save crop",
+                 [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+  }
   oaa::FoldCropParams o{};
   o.src = region(p, OAA_REGION_PRODUCT);
   o.dst = y;
   o.n_img = p->B; o.n_ch = p->K;
   o.M = p->M; o.n = p->b; o.off = p->n - 1; o.T = p->T;
+  o.To = p->T; o.shift = 0;
   o.S = p->b + p->n - 1;
   // the overlap-add in the frequency domain needs neighbours shifted by b not
   // to wrap into the block (2b <= L); larger blocks add their neighbours in space
@@ -482,12 +576,29 @@ oaa_status_t oaa_conv_backward_data(oaa_plan_t p, const float* g, const float* w
   gm.nsplit = 1; gm.kchunk = p->K; gm.c_sstride = 0;
   gm.a_trans = false; gm.a_conj = true; gm.b_trans = false; gm.b_conj = false;
   if ((st = run_gemm(p, gm, OAA_STAGE_BWD_DATA_PRODUCT, s, "backward-data contraction"))) return st;
+  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
+    // overlap-add of the gradient blocks' results into dx. The contraction
+    // used conj(W): each inverse is a circular correlation with support
+    // [-(n-1), h), i.e. the block's convolution with the flipped kernel
+    // circularly shifted up and left by n-1; the kernel shifts it back.
+    oaa::FoldCropParams o{};
+    o.src = region(p, OAA_REGION_PRODUCT);
+    o.dst = dx;
+    o.n_img = p->B; o.n_ch = p->C;
+    o.M = p->N; o.n = p->b; o.off = 0; o.T = p->T;
+    o.To = (p->N + p->b - 1) / p->b;
+    o.shift = p->n - 1;
+    o.S = p->L;
+    return timed(p, OAA_STAGE_BWD_DATA_INVERSE, s, "inverse transform + overlap-add",
+                 [&] { return oaa::launch_irfft2_overlap_crop(p->L, o, s); });
+  }
   oaa::CropParams c{};
   c.src = region(p, OAA_REGION_PRODUCT);
   c.nsplit = 1; c.split_stride = 0;
   c.dst = dx;
   c.n_img = p->B; c.n_ch = p->C;
   c.H = p->N; c.n = p->b; c.T = p->T;
+  c.origin = 0;
   return timed(p, OAA_STAGE_BWD_DATA_INVERSE, s, "inverse transform + block crop",
                [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
 }
@@ -524,6 +635,9 @@ oaa_status_t oaa_conv_backward_filter(oaa_plan_t p, const float* x, const float*
   c.dst = dw;
   c.n_img = p->K; c.n_ch = p->C;   // spectra [F][C][K], output planes dw[k][c]
   c.H = p->n; c.n = p->n; c.T = 1;
+  // overlap-save: the windows carry the conjugate, so dw[u][v] sits at rows
+  // and columns (h + u) mod L of the inverse
+  c.origin = p->method == OAA_METHOD_OVERLAP_SAVE ? p->b & (p->L - 1) : 0;
   return timed(p, OAA_STAGE_BWD_FILTER_INVERSE, s, "inverse transform of weight gradient",
                [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
 }

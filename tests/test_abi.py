@@ -239,3 +239,38 @@ def test_paper_sweep_configurations():
     i = sweep_configs("input")
     assert [c[4] for c in i] == list(range(8, 257, 8)) and all(c[5] == 5 for c in i)
     assert len(sweep_configs("all")) == len(k) + len(s) + len(i)
+
+
+@pytest.mark.parametrize("name,L,h,T", [("large128", 32, 17, 7), ("mid56", 16, 14, 4), ("first224", 16, 10, 22),
+                                       ("tiny", 16, 12, 3)])
+def test_overlap_save_geometry(lib, name, L, h, T):
+    """The output-tiled method: hop h = L - n + 1 reported as b, and
+    T = ceil(M / h) windows per side (the large layer: 7, against 8 blocks
+    of the overlap-add tiling)."""
+    ly = LAYERS[name]
+    handle = binding.oaa_plan_create_method(ly.B, ly.C, ly.K, ly.N, ly.n, L, 0, binding.METHOD_OVERLAP_SAVE)
+    try:
+        geo = binding.oaa_plan_geometry(handle)
+        assert (geo["L"], geo["b"], geo["T"], geo["P"], geo["method"]) == (L, h, T, T * T, 1)
+        assert geo["M"] == ly.M and T == -(-ly.M // h)
+    finally:
+        binding.oaa_plan_destroy(handle)
+    auto = binding.oaa_plan_create_method(ly.B, ly.C, ly.K, ly.N, ly.n, 0, 0, binding.METHOD_OVERLAP_SAVE)
+    try:
+        g2 = binding.oaa_plan_geometry(auto)
+        assert g2["b"] == g2["L"] - ly.n + 1 and g2["T"] == -(-ly.M // g2["b"])
+    finally:
+        binding.oaa_plan_destroy(auto)
+
+
+@pytest.mark.parametrize("dims,status", [
+    ((1, 1, 1, 16, 5, 8, 0, 1), 1),   # L < 2n - 1
+    ((1, 1, 1, 16, 5, 16, 11, 1), 1),  # b not the hop
+    ((1, 1, 1, 16, 5, 24, 0, 1), 2),   # L not a power of two
+    ((1, 1, 1, 16, 5, 16, 0, 7), 1),   # unknown method
+])
+def test_method_plan_validation(lib, dims, status):
+    h = ctypes.c_void_p()
+    st = lib.oaa_plan_create_method(ctypes.byref(h), *dims)
+    assert st == status and not h.value
+    assert lib.oaa_last_error_detail()

@@ -42,10 +42,10 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
-def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper"):
+def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper", method=binding.METHOD_OVERLAP_ADD):
     B, C, N, _ = x.shape
     K, _, n, _ = w.shape
-    plan = binding.Plan(B, C, K, N, n, device=DEV, contraction=contraction, tiling=tiling)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, contraction=contraction, tiling=tiling, method=method)
     xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
     y = plan.forward(xd, wd)
     dx = plan.backward_data(gd, wd)
@@ -54,8 +54,8 @@ def run_layer(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper"):
     return plan, y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
 
 
-def check_whole(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper"):
-    _, y, dx, dw = run_layer(x, w, g, contraction, tiling)
+def check_whole(x, w, g, contraction=binding.CONTRACTION_AUTO, tiling="paper", method=binding.METHOD_OVERLAP_ADD):
+    _, y, dx, dw = run_layer(x, w, g, contraction, tiling, method)
     N, n = x.shape[-1], w.shape[-1]
     e = (relerr(y, oracle.conv_forward(x, w)),
          relerr(dx, oracle.conv_backward_data(g, w, N)),
@@ -344,3 +344,91 @@ def test_autograd_function_matches_oracle(gpu_lib):
     assert relerr(yl.detach().cpu().numpy(), yr.detach().numpy()) <= TOL
     assert relerr(xd2.grad.cpu().numpy(), xr.grad.numpy()) <= TOL
     assert relerr(layer.weight.grad.cpu().numpy(), wr.grad.numpy()) <= TOL
+
+
+# ---------------------------------------------------------------------------
+# output-tiled method: overlap-and-save forward, overlap-add of gradient blocks
+
+OAS = binding.METHOD_OVERLAP_SAVE
+
+
+@pytest.mark.parametrize("double", [False, True], ids=["L0", "2L0"])
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+def test_overlap_save_small_layers(gpu_lib, shape, double):
+    B, C, K, N, n = shape
+    L = 2
+    while L < 2 * n - 1:
+        L *= 2
+    if double:
+        L *= 2
+    if L > 64:
+        pytest.skip("transform side above 64")
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=53 + sum(shape))
+    check_whole(x, w, g, tiling=(L, 0), method=OAS)
+
+
+@pytest.mark.parametrize("contraction", [binding.CONTRACTION_VALU, binding.CONTRACTION_MFMA, binding.CONTRACTION_NARROW],
+                         ids=["valu", "mfma", "narrow"])
+def test_overlap_save_contraction_engines(gpu_lib, contraction):
+    shape = (2, 3, 64, 30, 7) if contraction == binding.CONTRACTION_NARROW else (2, 40, 66, 21, 4)
+    B, C, K, N, n = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=61)
+    check_whole(x, w, g, contraction=contraction, tiling="auto", method=OAS)
+
+
+@pytest.mark.parametrize("name,batch,C,K", [("first224", 2, None, None), ("mid56", 2, None, None),
+                                            ("large128", 1, 16, 32)])
+def test_overlap_save_reduced_large_layers_whole(gpu_lib, name, batch, C, K):
+    ly = LAYERS[name]
+    ly = Layer(ly.name, batch, C or ly.C, K or ly.K, ly.N, ly.n, ly.x_dist, ly.w_var, ly.g_dist)
+    x, w, g = make_inputs(ly, seed=0)
+    check_whole(x, w, g, tiling="auto", method=OAS)
+
+
+@pytest.mark.parametrize("name", ["first224", "mid56", "large128"])
+def test_overlap_save_full_size_layers_sampled(gpu_lib, name):
+    """Full size, in the launch configuration bench.py --method oas times:
+    cached spectra reused (w, x, g NULL where the bench passes NULL)."""
+    ly = LAYERS[name]
+    x, w, g = make_inputs(ly, seed=0)
+    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=DEV, tiling="auto", method=OAS)
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    y = plan.forward(xd, wd)
+    dx = plan.backward_data(gd, None)
+    dw = plan.backward_filter(None, None)
+    torch.cuda.synchronize()
+    y, dx, dw = y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
+    rng = np.random.default_rng(2)
+    S = 48
+    B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
+    iy = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, K, M, M)]
+    ix = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, C, N, N)]
+    iw = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (K, C, n, n)]
+    e = (relerr(y[tuple(iy)], oracle.conv_forward_at(x, w, *iy)),
+         relerr(dx[tuple(ix)], oracle.conv_backward_data_at(g, w, N, *ix)),
+         relerr(dw[tuple(iw)], oracle.conv_backward_filter_at(x, g, n, *iw)))
+    print(f"{name} overlap-save sampled rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e} bwd_filter {e[2]:.2e}", flush=True)
+    assert max(e) <= TOL, e
+    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dw).all()
+
+
+def test_overlap_save_stage_spectra_match_oracle(gpu_lib):
+    """Window spectra of x and block spectra of g, as the kernels store them,
+    against the oracle's steps."""
+    from oracle import oas
+    B, C, K, N, n = 2, 3, 4, 23, 5
+    ly = Layer("t", B, C, K, N, n)
+    x, w, g = make_inputs(ly, seed=9)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(16, 0), method=OAS)
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    plan.forward(xd, wd)
+    plan.backward_data(gd, None)
+    torch.cuda.synchronize()
+    geo = plan.geometry
+    L, T, F = geo["L"], geo["T"], geo["F"]
+    V = L // 2 + 1
+    Xh = plan.region(binding.REGION_X_SPECTRUM).cpu().numpy().reshape(L, V, C, B, T, T)
+    Gh = plan.region(binding.REGION_G_SPECTRUM).cpu().numpy().reshape(L, V, K, B, T, T)
+    Xo = oas.window_spectra(x, n, L).transpose(4, 5, 1, 0, 2, 3)
+    Go = oas.block_spectra(g, n, L).transpose(4, 5, 1, 0, 2, 3)
+    assert relerr(Xh, Xo) <= TOL and relerr(Gh, Go) <= TOL

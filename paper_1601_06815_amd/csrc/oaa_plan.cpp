@@ -16,6 +16,15 @@
 
 #include "oaa_internal.hpp"
 
+// Weight-gradient split: enough partial products that the tiled contraction
+// has about this many tiles, three rounds of its 512 resident workgroups.
+// More partial sums balance the rounds better but cost the inverse one more
+// read of the whole weight-gradient spectrum each (overridable at build time
+// for tuning sweeps).
+#ifndef OAA_SPLIT_TILES
+#define OAA_SPLIT_TILES 1536
+#endif
+
 struct oaa_plan_s {
   int B, C, K, N, n;
   int method;  // oaa_method_t
@@ -361,7 +370,7 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   // split of the weight-gradient reduction over B*P, shared by every
   // contraction engine (the inverse adds the partial sums):
   //  * tiled engines: 96- or 128-row by 128-column tiles, two workgroups per
-  //    CU, at least eight rounds of 512 workgroups; chunks of 16 tiles;
+  //    CU, about OAA_SPLIT_TILES tiles; chunks of 16 tiles;
   //  * few input channels (the streaming engine): about 2048 workgroups of 64
   //    kernels, chunks of at least 1024 tiles, a multiple of 128.
   long long split, quantum;
@@ -374,7 +383,7 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   } else {
     const long long rows = ((C + 95) / 96) * 96 - C < ((C + 127) / 128) * 128 - C ? (C + 95) / 96 : (C + 127) / 128;
     const long long tiles = rows * ((K + 127) / 128) * F;
-    split = tiles >= 4096 ? 1 : (4096 + tiles - 1) / tiles;
+    split = tiles >= OAA_SPLIT_TILES ? 1 : (OAA_SPLIT_TILES + tiles - 1) / tiles;
     const long long max_split = (BP + 63) / 64;
     if (split > max_split) split = max_split;
     quantum = 16;

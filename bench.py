@@ -60,6 +60,17 @@ KERNEL_SOURCE = {
     "fwd_inverse": "k_fold_fft.hip", "bwd_data_inverse": "k_tile_fft.hip", "bwd_filter_inverse": "k_tile_fft.hip",
     "fwd_product": "k_cgemm.hip", "bwd_data_product": "k_cgemm.hip", "bwd_filter_product": "k_cgemm.hip",
 }
+# the output-tiled method crops the forward and overlap-adds the error propagation
+KERNEL_SOURCE_OAS = dict(KERNEL_SOURCE, fwd_inverse="k_tile_fft.hip", bwd_data_inverse="k_fold_fft.hip")
+
+
+def kernel_source(geo, stage):
+    return (KERNEL_SOURCE_OAS if geo.get("method") else KERNEL_SOURCE)[stage]
+
+
+def traffic_key(workload, geo, stage):
+    method = "/oas" if geo.get("method") else ""
+    return f"{workload}@{geo['L']}:{geo['b']}{method}/{stage}"
 
 
 SHARED_SOURCES = ("oaa_plan.cpp", "oaa_internal.hpp", "tile_common.hpp", "fft_core.hpp", "twiddle.hpp",
@@ -83,10 +94,10 @@ def measured_traffic(workload, geo, stage):
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path)).get(f"{workload}@{geo['L']}:{geo['b']}/{stage}")
+        rec = json.load(open(path)).get(traffic_key(workload, geo, stage))
     except (ValueError, OSError):
         return None
-    if not rec or rec.get("source_sha256") != source_digest(KERNEL_SOURCE[stage]):
+    if not rec or rec.get("source_sha256") != source_digest(kernel_source(geo, stage)):
         return None
     return rec.get("bytes_per_launch")
 
@@ -146,15 +157,17 @@ def _dispatch_values(run_dir, counter):
     return [per[d] for d in sorted(per)]
 
 
-def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, steps=2):
+def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, steps=2, method="oaa"):
     """HBM bytes per launch of each stage from FETCH_SIZE and WRITE_SIZE runs of
-    `bench.py --layer <layer> --steps 2 --warmup 1 --no-cpu-baseline`,
-    calibrated against runs of `bench.py --copy-calibration 1024`; prints the
-    table and records the figures in profiles/traffic.json."""
+    `bench.py --layer <layer> --method <method> --steps 2 --warmup 1
+    --no-cpu-baseline`, calibrated against runs of
+    `bench.py --copy-calibration 1024`; prints the table and records the
+    figures in profiles/traffic.json."""
     from paper_1601_06815_amd import binding
     from paper_1601_06815_amd.workloads import LAYERS
     ly = LAYERS[layer]
-    h = binding.oaa_plan_create_tiled(ly.B, ly.C, ly.K, ly.N, ly.n, 0, 0)
+    m = binding.METHOD_OVERLAP_SAVE if method == "oas" else binding.METHOD_OVERLAP_ADD
+    h = binding.oaa_plan_create_method(ly.B, ly.C, ly.K, ly.N, ly.n, 0, 0, m)
     geo = binding.oaa_plan_geometry(h)
     binding.oaa_plan_destroy(h)
     copy_bytes = 1024 * (1 << 20)
@@ -173,7 +186,8 @@ def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, ste
     db["_calibration"] = {"copy_bytes_each_way": copy_bytes, "fetch_factor": round(f_factor, 4),
                           "write_factor": round(w_factor, 4),
                           "note": "bytes = counter KiB x 1024 x factor; factors from a plain device copy"}
-    print(f"## {layer}, L={geo['L']} b={geo['b']} (mean over the last {steps} steps)")
+    name = "overlap-save, h" if geo.get("method") else "b"
+    print(f"## {layer}, L={geo['L']} {name}={geo['b']} (mean over the last {steps} steps)")
     print(f"{'stage':20s} {'kernel':48s} {'fetch MB':>9s} {'write MB':>9s} {'total MB':>9s} {'algo MB':>9s} {'ratio':>6s}")
     for i, stage in enumerate(STAGE_ORDER):
         fs = [fetch[j * n + i] for j in range(steps)]
@@ -184,9 +198,9 @@ def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, ste
         algo = work[stage]["bytes"]
         print(f"{stage:20s} {kern[:48]:48s} {fb / 1e6:9.1f} {wb / 1e6:9.1f} {(fb + wb) / 1e6:9.1f} "
               f"{algo / 1e6:9.1f} {(fb + wb) / algo:6.2f}")
-        db[f"{layer}@{geo['L']}:{geo['b']}/{stage}"] = {
+        db[traffic_key(layer, geo, stage)] = {
             "kernel": kern, "fetch_bytes": int(fb), "write_bytes": int(wb), "bytes_per_launch": int(fb + wb),
-            "source_sha256": source_digest(KERNEL_SOURCE[stage])}
+            "source_sha256": source_digest(kernel_source(geo, stage))}
     with open(path, "w") as f:
         json.dump(db, f, indent=1, sort_keys=True)
         f.write("\n")
@@ -227,7 +241,7 @@ def main():
                     help="host only: table of a rocprofv3 --kernel-trace --stats run")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(args.layer, *args.summarize_pmc)
+        summarize_pmc(args.layer, *args.summarize_pmc, method=args.method)
         return
     if args.summarize_stats:
         summarize_stats(args.summarize_stats)

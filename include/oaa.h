@@ -108,8 +108,12 @@ typedef enum {
                                 after backward_data: [F][C][B*P];
                                 after backward_filter: [split][F][C][K] partial sums.
                                 Bins (u, v) with u > L/2 and v in {0, L/2} are
-                                not written: they are the conjugates of bins
-                                (L-u, v), the spectra being Hermitian there. */
+                                the conjugates of bins (L-u, v), the spectra
+                                being Hermitian there. Nothing reads them: they
+                                are never written here, nor in the X and G
+                                regions when these hold window spectra (the G
+                                region with overlap-add, the X region with
+                                overlap-save) at L <= 32. */
 } oaa_region_t;
 
 /* Contraction implementation (the per-bin complex matrix product). */

@@ -23,6 +23,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_resource(const void* ba
   return __builtin_amdgcn_make_buffer_rsrc(pu, short(0), int(__builtin_amdgcn_readfirstlane(bytes)), 0x00020000);
 }
 
+__device__ __forceinline__ float buffer_load_f1(__amdgpu_buffer_rsrc_t rs, unsigned byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, byte_off, 0, 0));
+}
+
 __device__ __forceinline__ float2 buffer_load_f2(__amdgpu_buffer_rsrc_t rs, unsigned byte_off) {
   return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(rs, byte_off, 0, 0));
 }

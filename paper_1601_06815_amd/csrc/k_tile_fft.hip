@@ -397,6 +397,181 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
 }
 
 // ---------------------------------------------------------------------------
+// Windows -> spectra, several window rows per step (L <= 32).
+//
+// Windows of neighbouring window rows share S - n framed rows, and the row
+// transform of a framed row is the same for every window containing it. A
+// step stages the (rw - 1) n + S framed rows of rw window rows once,
+// transforms each of them once per window column, then runs the column
+// transforms of all rw x nq windows. When a workgroup holds whole rows of T
+// windows, the rw T windows of a step are consecutive tiles, and each
+// spectrum bin is written as one run of rw T complex values (the launcher
+// picks rw for runs of at least 16, 128 bytes).
+//
+// Transformed rows are stored packed, L/2 complex slots per row: slot 0 holds
+// the two real bins v = 0 and v = L/2 as (re, im), slots 1 .. L/2-1 the bins
+// in between. The column transform of slot 0 is one complex transform of the
+// two real columns v = 0 and v = L/2, separated afterwards by symmetry; it
+// stores their bins u <= L/2 only, since bins (L - u, v) of these columns
+// are their conjugates and nothing reads them. Every lane then stores about
+// L values.
+//
+// FULL: the window side is exactly L (L/2 under ZH), so no window entry
+// needs masking. PF: the next step's rows are prefetched into registers
+// (only worth its registers when a workgroup runs several steps).
+//
+// LDS: rows [NA][Wp] floats (staged framed rows), then zbuf [TQ][TS] float2,
+// NA = (RW - 1) n + S_MAX rounded up to even, TS >= NA L/2 odd.
+template <int L, bool ZH, bool FULL, bool PF>
+__global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(WindowParams p) {
+  constexpr int V = L / 2 + 1;
+  constexpr int HB = L / 2;                 // packed slots per transformed row
+  constexpr int S_MAX = ZH ? L / 2 : L;     // window side bound the transforms assume
+  extern __shared__ float smem[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int n = p.n, T = p.T, H = p.H, SW = p.S, RW = p.RW;
+  const int NA = ((RW - 1) * n + S_MAX + 1) & ~1;
+  const int TS = odd_at_least(NA * HB);
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
+  const int chunk = int(wg % p.nchunk);
+  const unsigned rest = wg / p.nchunk;
+  const int grp = int(rest % p.ngroups);
+  const unsigned plane = rest / p.ngroups;
+  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
+  const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
+  const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
+  const int W = (nq - 1) * n + SW;                  // staged columns
+  const int Wp = bank_stride((p.TQ - 1) * n + L);  // row reads stay inside the row
+  float* rows = smem;                                                                // [NA][Wp]
+  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(NA) * Wp));  // [TQ][TS]
+  const float* src = p.src + size_t(plane) * H * H;
+  const size_t tiles_per_ch = size_t(p.n_img) * T * T;
+  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
+  float2* out_base = p.dst + size_t(ch) * tiles_per_ch + size_t(img) * T * T + q0;
+  const int col0 = q0 * n - p.off;
+
+  // pass 1 of the step at window row P0: framed rows two at a time
+  auto row_pass = [&](int NR) {
+    for (int task = tid; task < ((NR + 1) / 2) * nq; task += nthr) {
+      const int q = task % nq, r0 = 2 * (task / nq);
+      const bool has_b = r0 + 1 < NR;
+      const float* row_a = rows + r0 * Wp + q * n;
+      const float* row_b = row_a + Wp;
+      float zr[L], zi[L];
+#pragma unroll
+      for (int s = 0; s < L; ++s) {
+        if (s < S_MAX) {
+          const float x0 = row_a[s], x1 = row_b[s];
+          const bool in = FULL || s < SW;
+          zr[s] = in ? x0 : 0.f;
+          zi[s] = in && has_b ? x1 : 0.f;
+        } else {
+          zr[s] = 0.f;
+          zi[s] = 0.f;
+        }
+      }
+      float2 X0[V], X1[V];
+      rfft_pair<L, ZH>(zr, zi, X0, X1);
+      float2* zt = zbuf + q * TS + r0 * HB;
+      zt[0] = make_float2(X0[0].x, X0[L / 2].x);
+      zt[HB] = make_float2(X1[0].x, X1[L / 2].x);
+#pragma unroll
+      for (int k = 1; k < HB; ++k) {
+        zt[k] = X0[k];
+        zt[HB + k] = X1[k];
+      }
+    }
+  };
+
+  // Order of a step, chosen for gfx9's single counter of outstanding vector
+  // memory operations (a wait for loads also waits for every earlier store):
+  // the loads of the next step's rows are issued first and written to LDS
+  // after the lane's first column transform, before its first spectrum
+  // store; those stores then drain during the next row pass.
+  RowsPrefetch<PF ? kWindowPrefetch : 1> pf;
+  constexpr bool use_pf = PF;
+  stage_rows32(rows, Wp, src, H, pb * n - p.off, col0, min(RW, pe - pb) * n - n + SW, W);
+  __syncthreads();
+  row_pass(min(RW, pe - pb) * n - n + SW);
+  __syncthreads();
+  for (int P0 = pb; P0 < pe; P0 += RW) {
+    const int rw = min(RW, pe - P0);
+    const bool next = P0 + RW < pe;
+    const int nNR = next ? (min(RW, pe - P0 - RW) - 1) * n + SW : 0;
+    if (next && use_pf) pf.load(src, H, (P0 + RW) * n - p.off, col0, nNR, W);
+    // pass 2: column transforms of the rw x nq windows; lanes run over the
+    // window columns, then the window rows, so that a store instruction
+    // covers consecutive tiles of one bin. With prefetch, every lane has at
+    // most one column task (launcher), and writes the next rows to LDS
+    // between its transform and its stores.
+    auto column_task = [&](int task, bool stage_next) {
+      const int q = task % nq, r2 = task / nq;
+      const int w = r2 % rw, k = r2 / rw;
+      const float2* zt = zbuf + q * TS + (w * n) * HB + k;
+      float re[L], im[L];
+#pragma unroll
+      for (int r = 0; r < L; ++r) {
+        if (r < S_MAX) {
+          const float2 z = zt[r * HB];
+          const bool in = FULL || r < SW;
+          re[r] = in ? z.x : 0.f;
+          im[r] = in ? z.y : 0.f;
+        } else {
+          re[r] = 0.f;
+          im[r] = 0.f;
+        }
+      }
+      fft_dif<L, -1, ZH>(re, im);
+      if (stage_next) pf.store(rows, Wp, nNR, W);
+      // bin (u, v) of this window at obase + u V fstride (wave-uniform) plus
+      // the lane's byte offset (v fstride + w T + q) * 8, below V fstride * 8
+      // < 2^32 (checked by the launcher)
+      float2* obase = out_base + size_t(P0) * T;
+      const unsigned lo = unsigned((size_t(k) * fstride + size_t(w) * T + q) * 8u);
+      if (k == 0) {
+        // Z = C0 + i C1 with C0, C1 the Hermitian spectra of columns 0, L/2:
+        // C0[u] = (Z[u] + conj Z[-u]) / 2, C1[u] = (Z[u] - conj Z[-u]) / (2i)
+        const unsigned lh = lo + unsigned(size_t(L / 2) * fstride * 8u);
+        float2* bu = obase;
+#pragma unroll
+        for (int u = 0; u <= L / 2; ++u) {
+          const int pu = bitrev(u, L), pm = bitrev((L - u) % L, L);
+          const float ar = re[pu], ai = im[pu], br = re[pm], bi = im[pm];
+          at_byte(bu, lo) = make_float2(0.5f * (ar + br), 0.5f * (ai - bi));
+          at_byte(bu, lh) = make_float2(0.5f * (ai + bi), 0.5f * (br - ar));
+          advance_uniform(bu, size_t(V) * fstride);
+        }
+      } else {
+        float2* bu = obase;
+#pragma unroll
+        for (int u = 0; u < L; ++u) {
+          const int pu = bitrev(u, L);
+          at_byte(bu, lo) = make_float2(re[pu], im[pu]);
+          advance_uniform(bu, size_t(V) * fstride);
+        }
+      }
+    };
+    const int ntask = HB * rw * nq;
+    if (next && use_pf) {
+      if (tid < ntask)
+        column_task(tid, true);
+      else
+        pf.store(rows, Wp, nNR, W);
+    } else {
+      for (int task = tid; task < ntask; task += nthr) column_task(task, false);
+    }
+    if (!next) break;
+    __syncthreads();  // rows of the next step staged; zbuf free
+    if (!use_pf) {
+      stage_rows32(rows, Wp, src, H, (P0 + RW) * n - p.off, col0, nNR, W);
+      __syncthreads();
+    }
+    row_pass(nNR);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Inverse column pass shared by the inverse kernels: for the tiles at
 // in[q], q < nq (bin f at in[q + f * fstride], plus nsplit - 1 partial sums
 // spaced split_stride apart), transform every column v and keep rows
@@ -614,6 +789,50 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   constexpr int ROWS = ZH ? L / 2 : L;
   constexpr int PAIRS = (ROWS + 1) / 2;
+  const long planes = long(p.n_img) * p.n_ch;
+  // 32-bit lane offsets: within a plane, and within one row u of the bins
+  const size_t fstride = size_t(p.n_ch) * p.n_img * p.T * p.T;
+  if (L <= 32 && OAA_WINDOW_ROWS && size_t(p.H) * p.H * 4 < (size_t(1) << 31) &&
+      size_t(V) * fstride * 8 < (size_t(1) << 32)) {
+    // whole rows of windows per workgroup, rw of them per step so that a
+    // step's windows make runs of at least 16 tiles, within the LDS limit
+    constexpr int HB = L / 2;
+    auto lds_rows = [&](int tq, int rw) {
+      const size_t na = size_t(((rw - 1) * p.n + ROWS + 1) & ~1);
+      const size_t wp = size_t(bank_stride((tq - 1) * p.n + L));
+      return even_floats(na * wp) * 4 + size_t(odd_at_least(int(na) * HB)) * tq * 8;
+    };
+    int nchunk = (p.T + OAA_WINDOW_TQ_MAX - 1) / OAA_WINDOW_TQ_MAX;
+    while (nchunk < p.T && lds_rows((p.T + nchunk - 1) / nchunk, 1) > kLdsRowsBudget) ++nchunk;
+    p.TQ = (p.T + nchunk - 1) / nchunk;
+    p.nchunk = (p.T + p.TQ - 1) / p.TQ;
+    int rw = 1;
+    if (p.nchunk == 1)
+      while (rw * p.T < 16 && rw < p.T && lds_rows(p.TQ, rw + 1) <= kLdsRowsBudget) ++rw;
+    p.RW = rw;
+    // the next step's (rw - 1) n + S rows of (TQ - 1) n + S columns in registers
+    const long staged = long((rw - 1) * p.n + p.S) * long((p.TQ - 1) * p.n + p.S);
+    const size_t lds = lds_rows(p.TQ, rw);
+    if (lds > kLdsRowsBudget) return hipErrorInvalidConfiguration;
+    int ng = 1;
+    if (planes < 2048) ng = int(std::min<long>((p.T + rw - 1) / rw, (2048 + planes - 1) / planes));
+    p.SPW = ((p.T + ng - 1) / ng + rw - 1) / rw * rw;
+    p.ngroups = (p.T + p.SPW - 1) / p.SPW;
+    const int na = ((rw - 1) * p.n + ROWS + 1) & ~1;
+    const int tasks = std::max(na / 2 * p.TQ, HB * rw * p.TQ);
+    const int nthr = pick_threads(tasks);
+    // register prefetch when a workgroup runs more than one step and the rows
+    // and column tasks fit the lanes; at L = 16 the prefetching variant's
+    // registers (about 190 against 76) cost more occupancy than it gains
+    p.PF = OAA_WINDOW_PREFETCH && L >= 32 && p.SPW > rw && staged <= long(kWindowPrefetch) * nthr && HB * rw * p.TQ <= nthr ? 1 : 0;
+    auto kern = p.S == ROWS ? (p.PF ? window_rows_rfft2_kernel<L, ZH, true, true> : window_rows_rfft2_kernel<L, ZH, true, false>)
+                            : (p.PF ? window_rows_rfft2_kernel<L, ZH, false, true> : window_rows_rfft2_kernel<L, ZH, false, false>);
+    const hipError_t e = allow_lds(kern, kLdsRowsBudget);
+    if (e != hipSuccess) return e;
+    const long nwg = planes * p.ngroups * p.nchunk;
+    hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(nthr), lds, s, p);
+    return hipGetLastError();
+  }
   const int TS = odd_at_least(2 * PAIRS * V);
   auto lds_for = [&](int tq) {
     const size_t Wp = size_t(bank_stride((tq - 1) * p.n + L));
@@ -623,9 +842,10 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   while (nchunk < p.T && lds_for((p.T + nchunk - 1) / nchunk) > kLdsBudget) ++nchunk;
   p.TQ = (p.T + nchunk - 1) / nchunk;
   p.nchunk = (p.T + p.TQ - 1) / p.TQ;
+  p.RW = 1;
+  p.PF = 0;
   const size_t lds = lds_for(p.TQ);
   if (lds > kLdsBudget) return hipErrorInvalidConfiguration;
-  const long planes = long(p.n_img) * p.n_ch;
   int ng = 1;
   if (planes < 2048) ng = int(std::min<long>(p.T, (2048 + planes - 1) / planes));
   p.SPW = (p.T + ng - 1) / ng;

@@ -3,12 +3,16 @@
 
 #include <hip/hip_runtime.h>
 
+#include "buffer_io.hpp"
 #include "fft_core.hpp"
 
 // Launch-shape defaults (tiles per workgroup along a block row, register
 // prefetch of the next rows); overridable at build time for tuning sweeps.
 #ifndef OAA_WINDOW_TQ_MAX
 #define OAA_WINDOW_TQ_MAX 64
+#endif
+#ifndef OAA_WINDOW_ROWS
+#define OAA_WINDOW_ROWS 1
 #endif
 #ifndef OAA_WINDOW_PREFETCH
 #define OAA_WINDOW_PREFETCH 1
@@ -46,6 +50,29 @@ constexpr int fft_waves(int want) { return L <= 32 ? want : 1; }
 
 constexpr int kMaxThreads = 256;
 constexpr size_t kLdsBudget = 60 * 1024;
+// LDS of the kernels that transform several window rows per step: two
+// workgroups per CU
+constexpr size_t kLdsRowsBudget = 80 * 1024;
+// registers per lane for the next step's rows in those kernels
+constexpr int kWindowPrefetch = 32;
+
+// Lets a kernel take up to `bytes` of dynamic LDS (beyond 64 KB) on the
+// current device; set once per device.
+template <class Kern>
+hipError_t allow_lds(Kern kern, size_t bytes) {
+  static int done[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (!done[dev]) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            int(bytes));
+    if (e != hipSuccess) return e;
+    done[dev] = 1;
+  }
+  return hipSuccess;
+}
 
 inline int pick_threads(int tasks) {
   int t = ((tasks + 63) / 64) * 64;
@@ -101,6 +128,111 @@ __device__ __forceinline__ void stage_rows(float* dst, int Wp, const float* src,
     }
   }
 }
+
+// Element at byte offset `boff` from a wave-uniform base: the compiler then
+// addresses with the base in scalar registers and a 32-bit lane offset, with
+// no 64-bit arithmetic per access.
+template <class T>
+__device__ __forceinline__ T& at_byte(T* base, unsigned boff) {
+  return *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + boff);
+}
+template <class T>
+__device__ __forceinline__ const T& at_byte(const T* base, unsigned boff) {
+  return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + boff);
+}
+
+// Advances a wave-uniform pointer by `step` elements. The empty asm keeps
+// the pointer in one scalar register pair: without it the compiler
+// precomputes the addresses of a whole unrolled loop and runs out of scalar
+// registers.
+template <class T>
+__device__ __forceinline__ void advance_uniform(T*& ptr, size_t step) {
+  const unsigned long long a = reinterpret_cast<unsigned long long>(ptr + step);
+  unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(a));
+  unsigned hi = __builtin_amdgcn_readfirstlane(unsigned(a >> 32));
+  asm volatile("" : "+s"(lo), "+s"(hi));
+  ptr = reinterpret_cast<T*>((static_cast<unsigned long long>(hi) << 32) | lo);
+}
+
+// stage_rows for planes of fewer than 2^30 pixels, with 32-bit offsets from
+// the plane base.
+__device__ __forceinline__ void stage_rows32(float* dst, int Wp, const float* plane, int H, int row0, int col0,
+                                             int R, int W) {
+  const int nthr = blockDim.x, tid = threadIdx.x;
+  const int Wt = W < nthr ? W : nthr;
+  const int rstep = nthr / Wt;
+  const int cl = tid % Wt, rl = tid / Wt;
+  if (rl >= rstep) return;
+  for (int c = cl; c < W; c += Wt) {
+    const int gc = col0 + c;
+    const bool col_ok = gc >= 0 && gc < H;
+    for (int rb = rl; rb < R; rb += kUnroll * rstep) {
+      float v[kUnroll];
+#pragma unroll
+      for (int j = 0; j < kUnroll; ++j) {
+        const int r = rb + j * rstep;
+        const int gr = row0 + r;
+        const bool ok = col_ok && r < R && gr >= 0 && gr < H;
+        const float t = at_byte(plane, ok ? unsigned(gr * H + gc) * 4u : 0u);
+        v[j] = ok ? t : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kUnroll; ++j) {
+        const int r = rb + j * rstep;
+        if (r < R) dst[r * Wp + c] = v[j];
+      }
+    }
+  }
+}
+
+// Register copy of rows [row0, row0 + R) x columns [col0, col0 + W) of an
+// H x H plane (zero outside), for planes of fewer than 2^29 pixels: element e
+// of the block in row-major order is held by lane e % lanes, so the loads are
+// coalesced along rows. Needs R * W <= MAXE * lanes and W <= lanes. Loads go
+// through a buffer resource over the plane: elements outside it read as zero
+// with no per-element mask kept until the data arrives.
+template <int MAXE>
+struct RowsPrefetch {
+  float v[MAXE];
+
+  __device__ __forceinline__ void load(const float* plane, int H, int row0, int col0, int R, int W) {
+    const __amdgpu_buffer_rsrc_t rs = buffer_resource(plane, unsigned(H) * unsigned(H) * 4u);
+    const int nthr = blockDim.x;
+    const int dr = nthr / W, dc = nthr % W;
+    int r = int(threadIdx.x) / W, c = int(threadIdx.x) % W;
+#pragma unroll
+    for (int j = 0; j < MAXE; ++j) {
+      const int gr = row0 + r, gc = col0 + c;
+      const bool ok = r < R && unsigned(gr) < unsigned(H) && unsigned(gc) < unsigned(H);
+      v[j] = buffer_load_f1(rs, ok ? unsigned(gr * H + gc) * 4u : kOutOfRange);
+      r += dr;
+      c += dc;
+      if (c >= W) {
+        c -= W;
+        ++r;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(float* dst, int Wp, int R, int W) const {
+    const int nthr = blockDim.x;
+    const int dr = nthr / W, dc = nthr % W;
+    int r = int(threadIdx.x) / W, c = int(threadIdx.x) % W;
+    // recomputed here rather than kept from load(): the empty asm stops the
+    // compiler from holding MAXE addresses in registers in between
+    asm volatile("" : "+v"(r), "+v"(c));
+#pragma unroll
+    for (int j = 0; j < MAXE; ++j) {
+      if (r < R) dst[r * Wp + c] = v[j];
+      r += dr;
+      c += dc;
+      if (c >= W) {
+        c -= W;
+        ++r;
+      }
+    }
+  }
+};
 
 // Register copy of rows [row0, row0+R) x columns [col0, col0+W) of an H x H
 // plane (zero outside), for W <= lanes: lane t holds column t % W of rows

@@ -30,9 +30,12 @@ using namespace tile;
 // One workgroup per (plane, block row, run of tile columns). LDS: zbuf
 // [TQ + 1][TS] float2: column transforms (rows [0, L/2]) of tiles q0-1 ..
 // q0+nq-1 of the block row, folded along u with the block row above; then
-// obuf [n][TQ][n + 1] floats: the block row's output, written to HBM row by
+// obuf [n][TQ n + 1] floats: the block row's output, written to HBM row by
 // row with consecutive lanes on consecutive pixels.
-template <int L>
+// O32: spectrum bins are addressed as 32-bit lane offsets from a wave-uniform
+// row base (V fstride * 8 < 2^32) and output pixels as 32-bit offsets from
+// the plane (M * M * 4 < 2^32), with no 64-bit arithmetic per access.
+template <int L, bool O32>
 __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irfft2_fold_crop_kernel(FoldCropParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int RT = L / 2 + 1;
@@ -42,7 +45,7 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
   const int TS = odd_at_least(RT * V);
   float2* zbuf = reinterpret_cast<float2*>(smem);
   float* obuf = smem + size_t(p.TQ + 1) * TS * 2;
-  const int OS = n | 1;  // obuf stride between tiles, odd
+  const int OWp = (p.TQ * n) | 1;  // obuf row stride, odd
   const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
   const int chunk = int(wg % p.nchunk);
   const unsigned rest = wg / p.nchunk;
@@ -93,18 +96,30 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
     const bool live = Qt >= 0;
     const bool up = live && strip > 0;
     const float2* cur = in + size_t(strip) * T + (live ? Qt : 0) + size_t(v) * fstride;
-    const float2* abv = cur - (up ? T : 0);
+    const float2* abv = up ? cur - T : cur;
     // Columns v = 0 and v = L/2 hold no products in rows u > L/2: there the
     // folded column h is Hermitian, so with g = h on rows [0, L/2] (rows 0 and
     // L/2 halved) and zero elsewhere, h = g + conj(g mirrored) and the
     // inverse of h is 2 Re(inverse of g).
     const bool mir = v == 0 || v == L / 2;
     const float edge = mir ? 0.5f : 1.f;
+    // lane offsets of this tile and of the one above (itself when there is
+    // none: both are read unconditionally, the unused one is zeroed)
+    const unsigned oc = unsigned((size_t(v) * fstride + size_t(strip) * T + (live ? Qt : 0)) * 8u);
+    const unsigned oa = up ? oc - unsigned(T) * 8u : oc;
+    const float2* bu = in;
     float re[L], im[L];
 #pragma unroll
     for (int u = 0; u < L; ++u) {
-      const float2 c = cur[u * ustride];
-      const float2 a = abv[u * ustride];
+      float2 c, a;
+      if (O32) {
+        c = at_byte(bu, oc);
+        a = at_byte(bu, oa);
+        advance_uniform(bu, ustride);
+      } else {
+        c = cur[u * ustride];
+        a = abv[u * ustride];
+      }
       const float2 f = cmad(live ? c : make_float2(0.f, 0.f), twiddle<L, +1>(n * u),
                             up ? a : make_float2(0.f, 0.f));
       if (u > L / 2) {
@@ -141,8 +156,8 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
       float zr[HL], zi[HL];
       irfft_pair_split<L>([&](int k) { return cmad(za[k], twiddle<L, +1>(n * k), zb[k]); },
                           [&](int k) { return cmad(za[V + k], twiddle<L, +1>(n * k), zb[V + k]); }, zr, zi, h);
-      float* o0 = obuf + (size_t(r0) * nq + q) * OS;
-      float* o1 = o0 + size_t(nq) * OS;
+      float* o0 = obuf + size_t(r0) * OWp + q * n;
+      float* o1 = o0 + OWp;
       const bool has1 = r0 + 1 < n;
 #pragma unroll
       for (int m = 0; m < HL; ++m) {
@@ -168,8 +183,8 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
     }
     float zr[L], zi[L];
     irfft_pair<L>(A, Bv, zr, zi);
-    float* o0 = obuf + (size_t(r0) * nq + q) * OS;
-    float* o1 = o0 + size_t(nq) * OS;
+    float* o0 = obuf + size_t(r0) * OWp + q * n;
+    float* o1 = o0 + OWp;
     const bool has1 = r0 + 1 < n;
 #pragma unroll
     for (int s = 0; s < L / 2; ++s) {
@@ -189,10 +204,166 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
   const int cb = max(0, -j0), ce = min(W, M - j0);
   const int wr = ce - cb;
   if (wr <= 0 || re_ <= rb) return;
-  for (int e = tid; e < (re_ - rb) * wr; e += nthr) {
-    const int r = rb + e / wr, c = cb + e % wr;
-    const int q = c / n, s = c - q * n;
-    out[size_t(i0 + r) * M + j0 + c] = obuf[(size_t(r) * nq + q) * OS + s];
+  // lanes over columns in rows of a power-of-two width (no division)
+  const int lw = 32 - __builtin_clz(unsigned(wr - 1) | 1u), cw = 1 << lw;
+  for (int e = tid; e < (re_ - rb) << lw; e += nthr) {
+    const int r = rb + (e >> lw), c = cb + (e & (cw - 1));
+    if (c >= ce) continue;
+    const float val = obuf[size_t(r) * OWp + c];
+    if (O32)
+      at_byte(out, unsigned((i0 + r) * M + j0 + c) * 4u) = val;
+    else
+      out[size_t(i0 + r) * M + j0 + c] = val;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward output, RB whole block rows per workgroup (L <= 32, 2b <= L).
+//
+// The R = RB T tiles of block rows P0 .. P0 + RB - 1 are consecutive, and so
+// are the tiles above them, so every load instruction reads runs of R
+// consecutive tiles of one bin (128 bytes from R = 16 on). Lane (t, k)
+// folds packed column k of tile t with the tile above it (e^{+b u}, in the
+// frequency domain) and inverts it; the row pass folds along v with the left
+// neighbour (e^{+b v}), inverts pairs of rows and crops to b x b; the block
+// rows are then written out row by row.
+//
+// Packed column k = 0 carries the real columns v = 0 and v = L/2 as
+// h0[u] + i h1[u], rows u > L/2 rebuilt from the conjugates of rows L - u
+// (those bins are not stored); both parts of its inverse are real.
+//
+// LDS: zrow [R][ZT] float2 (rows [0, b) of the folded column inverses, L/2
+// packed slots per row, ZT = b L/2 + 1), then obuf [RB b][T b + 1] floats.
+template <int L>
+__global__ void __launch_bounds__(kMaxThreads) irfft2_fold_runs_kernel(FoldCropParams p) {
+  constexpr int V = L / 2 + 1, HB = L / 2;
+  extern __shared__ float smem[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int b = p.n, T = p.T, M = p.M, RB = p.RB, R = RB * T;
+  const int ZT = b * HB + 1;
+  float2* zrow = reinterpret_cast<float2*>(smem);
+  const int OW = T * b, OWp = OW | 1;
+  float* obuf = smem + size_t(R) * ZT * 2;
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
+  const int grp = int(wg % p.ngroups);
+  const unsigned plane = wg / p.ngroups;
+  const int P0 = grp * RB, rbh = min(RB, T - P0);  // block rows of this workgroup
+  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
+  const size_t tiles_per_ch = size_t(p.n_img) * T * T;
+  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
+  const float2* in = p.src + size_t(ch) * tiles_per_ch + size_t(img) * T * T;
+  float* out = p.dst + size_t(plane) * M * M;
+  const float scale = 1.0f / float(L * L);
+  const float2 zero2 = make_float2(0.f, 0.f);
+
+  // column pass
+  {
+    const int t = tid % R, k = tid / R;
+    if (k < HB && t < rbh * T) {
+      const bool up = P0 + t / T > 0;
+      // bin (u, v) of tile P0 T + t at the wave-uniform row base in + u V
+      // fstride plus the lane offset (v fstride + P0 T + t) * 8, below
+      // V fstride * 8 < 2^32 (checked by the launcher); the tile above is T
+      // tiles earlier (itself when there is none, then zeroed)
+      const unsigned lo = unsigned((size_t(k) * fstride + size_t(P0) * T + t) * 8u);
+      const unsigned la = up ? lo - unsigned(T) * 8u : lo;
+      float re[L], im[L];
+      const float2* bu = in;
+      if (k == 0) {
+        const unsigned lh = unsigned(size_t(HB) * fstride * 8u);
+        float2 h0[V], h1[V];
+#pragma unroll
+        for (int u = 0; u <= L / 2; ++u) {
+          const float2 tw = twiddle<L, +1>(b * u);
+          const float2 c0 = at_byte(bu, lo), a0 = at_byte(bu, la);
+          const float2 c1 = at_byte(bu, lo + lh), a1 = at_byte(bu, la + lh);
+          h0[u] = cmad(c0, tw, up ? a0 : zero2);
+          h1[u] = cmad(c1, tw, up ? a1 : zero2);
+          advance_uniform(bu, size_t(V) * fstride);
+        }
+        // z[u] = h0[u] + i h1[u], h[L - u] = conj h[u]
+#pragma unroll
+        for (int u = 0; u < L; ++u) {
+          const int m = u <= L / 2 ? u : L - u;
+          const float sgn = u <= L / 2 ? 1.f : -1.f;
+          re[u] = h0[m].x - sgn * h1[m].y;
+          im[u] = sgn * h0[m].y + h1[m].x;
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < L; ++u) {
+          const float2 c = at_byte(bu, lo), a = at_byte(bu, la);
+          const float2 f = cmad(c, twiddle<L, +1>(b * u), up ? a : zero2);
+          re[u] = f.x;
+          im[u] = f.y;
+          advance_uniform(bu, size_t(V) * fstride);
+        }
+      }
+      fft_dif<L, +1, false>(re, im);
+      float2* zt = zrow + size_t(t) * ZT + k;
+#pragma unroll
+      for (int r = 0; r < L / 2; ++r) {
+        const int pos = bitrev(r, L);
+        if (r < b) zt[r * HB] = make_float2(re[pos], im[pos]);
+      }
+    }
+  }
+  __syncthreads();
+  // row pass: fold along v with the left neighbour, inverse row transforms
+  // of row pairs, crop to the block
+  const int npair = (b + 1) / 2;
+  for (int task = tid; task < rbh * T * npair; task += nthr) {
+    const int tt = task % (rbh * T), pr = task / (rbh * T);
+    const int i = tt / T, q = tt % T;
+    const int r0 = 2 * pr;
+    const bool has1 = r0 + 1 < b;
+    const bool left = q > 0;
+    const float2* za = zrow + size_t(tt) * ZT + r0 * HB;
+    const float2* zl = zrow + size_t(left ? tt - 1 : tt) * ZT + r0 * HB;
+    const int rb1 = has1 ? HB : 0;  // row r0 + 1, or r0 again when b is odd
+    float2 A[V], Bv[V];
+    {
+      const float2 a0 = za[0], b0 = za[rb1];
+      const float2 l0 = left ? zl[0] : zero2, m0 = left ? zl[rb1] : zero2;
+      // slot 0: (bin 0, bin L/2) of a row, both real; e^{+b v} is 1 at v = 0
+      // and (-1)^b at v = L/2
+      const float sg = (b & 1) ? -1.f : 1.f;
+      A[0] = make_float2(a0.x + l0.x, 0.f);
+      A[L / 2] = make_float2(a0.y + sg * l0.y, 0.f);
+      Bv[0] = make_float2(b0.x + m0.x, 0.f);
+      Bv[L / 2] = make_float2(b0.y + sg * m0.y, 0.f);
+    }
+#pragma unroll
+    for (int v = 1; v < HB; ++v) {
+      const float2 tw = twiddle<L, +1>(b * v);
+      A[v] = cmad(za[v], tw, left ? zl[v] : zero2);
+      Bv[v] = cmad(za[rb1 + v], tw, left ? zl[rb1 + v] : zero2);
+    }
+    float zr[L], zi[L];
+    irfft_pair<L>(A, Bv, zr, zi);
+    float* o0 = obuf + size_t(i * b + r0) * OWp + q * b;
+    float* o1 = o0 + OWp;
+#pragma unroll
+    for (int s2 = 0; s2 < L / 2; ++s2) {
+      if (s2 < b) {
+        const int pos = bitrev(s2, L);
+        o0[s2] = zr[pos] * scale;
+        if (has1) o1[s2] = zi[pos] * scale;
+      }
+    }
+  }
+  __syncthreads();
+  // plane rows P0 b - off + [0, rbh b), clipped to [0, M); lanes over columns
+  // in rows of a power-of-two width (no division)
+  const int i0 = P0 * b - p.off, j0 = -p.off;
+  const int rb = max(0, -i0), re_ = min(rbh * b, M - i0);
+  const int cb = max(0, -j0), ce = min(OW, M - j0);
+  const int wr = ce - cb;
+  if (wr <= 0 || re_ <= rb) return;
+  const int lw = 32 - __builtin_clz(unsigned(wr - 1) | 1u), cw = 1 << lw;
+  for (int e = tid; e < (re_ - rb) << lw; e += nthr) {
+    const int r = rb + (e >> lw), c = cb + (e & (cw - 1));
+    if (c < ce) at_byte(out, unsigned((i0 + r) * M + j0 + c) * 4u) = obuf[size_t(r) * OWp + c];
   }
 }
 
@@ -396,9 +567,31 @@ template <int L>
 hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   if (p.To != p.T || p.shift != 0) return hipErrorInvalidValue;
+  const long planes = long(p.n_img) * p.n_ch;
+  // Runs of whole block rows for L = 16 and 32 (at L <= 8 the transforms are
+  // too short to repay the packed columns), with 32-bit lane offsets.
+  if (L >= 16 && L <= 32 && OAA_FOLD_RUNS && 2 * p.n <= L && size_t(p.M) * p.M * 4 < (size_t(1) << 32) &&
+      size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32)) {
+    // whole block rows, RB of them per workgroup: runs of at least 16 tiles
+    // where the lanes allow, every column task on a lane of its own
+    constexpr int HB = L / 2;
+    const int rb = std::min(std::max(1, (16 + p.T - 1) / p.T), std::max(1, kMaxThreads / (p.T * HB)));
+    const int R = rb * p.T;
+    const size_t lds = size_t(R) * (p.n * HB + 1) * 8 + size_t(rb * p.n) * ((p.T * p.n) | 1) * 4;
+    if (R * HB <= kMaxThreads && lds <= kLdsRowsBudget) {
+      p.RB = rb;
+      p.ngroups = (p.T + rb - 1) / rb;
+      auto kern = irfft2_fold_runs_kernel<L>;
+      const hipError_t e = allow_lds(kern, kLdsRowsBudget);
+      if (e != hipSuccess) return e;
+      const int nthr = pick_threads(std::max(R * HB, R * ((p.n + 1) / 2)));
+      hipLaunchKernelGGL(kern, dim3(unsigned(planes * p.ngroups)), dim3(nthr), lds, s, p);
+      return hipGetLastError();
+    }
+  }
   const int TS = odd_at_least((L / 2 + 1) * V);
   const size_t zb = size_t(TS) * 8;                 // column transforms of one tile
-  const size_t ob = size_t(p.n) * (p.n | 1) * 4;    // output block of one tile
+  const size_t ob = size_t(p.n) * (p.n + 1) * 4;    // output block of one tile (and padding)
   int tq = std::min<int>(std::min<int>(p.T, OAA_FOLD_TQ_MAX),
                          kLdsBudget > zb ? int((kLdsBudget - zb) / (zb + ob)) : 0);
   if (tq < 1) return hipErrorInvalidConfiguration;
@@ -407,11 +600,13 @@ hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   p.nchunk = nchunk;
   p.SPW = 1;
   p.ngroups = p.T;
-  const long planes = long(p.n_img) * p.n_ch;
-  const size_t lds = zb * (p.TQ + 1) + ob * p.TQ;
+  const size_t lds = zb * (p.TQ + 1) + size_t(p.n) * ((p.TQ * p.n) | 1) * 4;
   const int tasks = (L >= 64 ? 2 : 1) * std::max((p.TQ + 1) * V, ((p.n + 1) / 2) * p.TQ);
   const long nwg = planes * p.T * p.nchunk;
-  hipLaunchKernelGGL(irfft2_fold_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
+  const bool o32 = size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32) &&
+                   size_t(p.M) * p.M * 4 < (size_t(1) << 32);
+  auto kern = o32 ? irfft2_fold_crop_kernel<L, true> : irfft2_fold_crop_kernel<L, false>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }
 

@@ -17,6 +17,9 @@
 #ifndef OAA_WINDOW_PREFETCH
 #define OAA_WINDOW_PREFETCH 1
 #endif
+#ifndef OAA_FOLD_RUNS
+#define OAA_FOLD_RUNS 1
+#endif
 #ifndef OAA_FOLD_TQ_MAX
 #define OAA_FOLD_TQ_MAX 64
 #endif

@@ -144,6 +144,31 @@ def test_tiled_layers_all_passes(gpu_lib, shape):
     check_whole(x, w, g, tiling=(L, b))
 
 
+FOLD_RUNS = [  # (B, C, K, N, n, L): blocks of L/2, where the forward inverse takes several
+    # whole block rows per workgroup (runs of consecutive tiles)
+    (2, 3, 512, 64, 5, 32),    # T = 4: four block rows per workgroup
+    (1, 2, 1024, 100, 7, 32),  # T = 7: two block rows, the last workgroup with one
+    (1, 2, 1024, 128, 5, 16),  # T = 16: one block row
+    (4, 2, 256, 50, 3, 8),     # T = 13 at L = 8 (the per-block-row kernel)
+    (8, 2, 128, 128, 9, 32),   # T = 8, two block rows (the large-kernel layer's tiling)
+    (2, 2, 8, 45, 4, 16),      # T = 6 on few planes, ragged output
+]
+
+
+@pytest.mark.parametrize("shape", FOLD_RUNS, ids=lambda s: "x".join(map(str, s)))
+def test_forward_block_row_runs(gpu_lib, shape):
+    """Forward pass through the overlap-add inverse on runs of block rows
+    against the oracle."""
+    B, C, K, N, n, L = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=41 + sum(shape))
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, L // 2))
+    y = plan.forward(to_dev(x), to_dev(w))
+    torch.cuda.synchronize()
+    e = relerr(y.cpu().numpy(), oracle.conv_forward(x, w))
+    print(f"block-row runs {shape}: rel err fwd {e:.2e}", flush=True)
+    assert e <= TOL, e
+
+
 FFTCONV = [  # (B, C, K, N, n, L): one block per plane, L >= N + n - 1 (the paper's FFTconv)
     (1, 3, 4, 32, 5, 64),
     (2, 2, 3, 13, 4, 16),

@@ -32,6 +32,10 @@
 #ifndef OAA_GEMM_NB
 #define OAA_GEMM_NB 2
 #endif
+// Matrix-core step of a slice after which the next slice goes to LDS (0..3).
+#ifndef OAA_GEMM_STORE_STEP
+#define OAA_GEMM_STORE_STEP 2
+#endif
 
 namespace oaa {
 
@@ -386,8 +390,17 @@ __global__ void __launch_bounds__(kThreads, OAA_WAVES_GEMM) cgemm_mfma_kernel(Ge
       Br[j] = *reinterpret_cast<const floatx4*>(&Bsr[buf][wn + 16 * j + lr][4 * lk]);
       Bi[j] = *reinterpret_cast<const floatx4*>(&Bsi[buf][wn + 16 * j + lr][4 * lk]);
     }
+    // The wave issues its matrix-core products at raised priority, so that
+    // the arbiter keeps them flowing while the other waves of the SIMD load
+    // and store; the next slice goes to LDS half way through (the buffer it
+    // overwrites was released by the previous barrier).
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
+      if (s == OAA_GEMM_STORE_STEP && more) {
+        sa.store(Asr[buf ^ 1], Asi[buf ^ 1], AC);
+        sb.store(Bsr[buf ^ 1], Bsi[buf ^ 1], BC);
+      }
       float as[MB], bs[NB];
 #pragma unroll
       for (int i = 0; i < MB; ++i) as[i] = Ar[i][s] + Ai[i][s];
@@ -411,10 +424,7 @@ __global__ void __launch_bounds__(kThreads, OAA_WAVES_GEMM) cgemm_mfma_kernel(Ge
         for (int j = 0; j < NB; ++j)
           p2[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(Ai[i][s], Bi[j][s], p2[i][j], 0, 0, 0);
     }
-    if (more) {
-      sa.store(Asr[buf ^ 1], Asi[buf ^ 1], AC);
-      sb.store(Bsr[buf ^ 1], Bsi[buf ^ 1], BC);
-    }
+    __builtin_amdgcn_s_setprio(0);
     if (ck + kKC >= cur.ke) {
       // 16 x 16 result block: lane holds rows 4*(lane/16) + r, r < 4, of column
       // lane % 16; each bin's matrix is under 2^28 elements (32-bit offsets)

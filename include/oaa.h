@@ -110,10 +110,8 @@ typedef enum {
                                 Bins (u, v) with u > L/2 and v in {0, L/2} are
                                 the conjugates of bins (L-u, v), the spectra
                                 being Hermitian there. Nothing reads them: they
-                                are never written here, nor in the X and G
-                                regions when these hold window spectra (the G
-                                region with overlap-add, the X region with
-                                overlap-save) at L <= 32. */
+                                are never written here, and the X and G
+                                regions may omit them too. */
 } oaa_region_t;
 
 /* Contraction implementation (the per-bin complex matrix product). */

@@ -16,6 +16,17 @@
 
 #include "oaa_internal.hpp"
 
+// Block tiles (the input with overlap-add, the gradient with overlap-save)
+// go through the window transform (window side = pitch = b) where its
+// several-rows-per-step kernel pays: fewer than 16 blocks per row (the block
+// transform's runs of one block row are shorter than 128 bytes), and at
+// L = 32 only for blocks of exactly L/2 (other sides take its masked,
+// register-heavy variant).
+#ifndef OAA_BLOCKS_AS_WINDOWS
+#define OAA_BLOCKS_AS_WINDOWS 1
+#endif
+
+
 // Weight-gradient split: enough partial products that the tiled contraction
 // has about this many tiles, three rounds of its 512 resident workgroups.
 // More partial sums balance the rounds better but cost the inverse one more
@@ -48,6 +59,10 @@ struct oaa_plan_s {
   };
   std::vector<Rec> records;
 };
+
+bool blocks_as_windows(const oaa_plan_s* p) {
+  return OAA_BLOCKS_AS_WINDOWS && p->T < 16 && (p->L <= 16 || 2 * p->b == p->L);
+}
 
 namespace {
 
@@ -160,18 +175,35 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
     if (st == OAA_OK) p->x_valid = true;
     return st;
   }
-  oaa::TileFwdParams t{};
-  t.src = x;
-  t.dst = region(p, OAA_REGION_X_SPECTRUM);
-  t.n_img = p->B;
-  t.n_ch = p->C;
-  t.H = p->N;
-  t.pitch = p->b;
-  t.off = 0;
-  t.R = p->b;
-  t.T = p->T;
-  oaa_status_t st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
-                          [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+  oaa_status_t st;
+  if (blocks_as_windows(p)) {
+    // b x b blocks as windows of side b at pitch b
+    oaa::WindowParams t{};
+    t.src = x;
+    t.dst = region(p, OAA_REGION_X_SPECTRUM);
+    t.n_img = p->B;
+    t.n_ch = p->C;
+    t.H = p->N;
+    t.n = p->b;
+    t.S = p->b;
+    t.off = 0;
+    t.T = p->T;
+    st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
+               [&] { return oaa::launch_window_rfft2(p->L, t, s); });
+  } else {
+    oaa::TileFwdParams t{};
+    t.src = x;
+    t.dst = region(p, OAA_REGION_X_SPECTRUM);
+    t.n_img = p->B;
+    t.n_ch = p->C;
+    t.H = p->N;
+    t.pitch = p->b;
+    t.off = 0;
+    t.R = p->b;
+    t.T = p->T;
+    st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
+               [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+  }
   if (st == OAA_OK) p->x_valid = true;
   return st;
 }
@@ -179,18 +211,34 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
 oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // h x h blocks of g, h = L - n + 1
-    oaa::TileFwdParams t{};
-    t.src = g;
-    t.dst = region(p, OAA_REGION_G_SPECTRUM);
-    t.n_img = p->B;
-    t.n_ch = p->K;
-    t.H = p->M;
-    t.pitch = p->b;
-    t.off = 0;
-    t.R = p->b;
-    t.T = p->T;
-    oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient block spectra",
-                            [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+    oaa_status_t st;
+    if (blocks_as_windows(p)) {
+      oaa::WindowParams t{};
+      t.src = g;
+      t.dst = region(p, OAA_REGION_G_SPECTRUM);
+      t.n_img = p->B;
+      t.n_ch = p->K;
+      t.H = p->M;
+      t.n = p->b;
+      t.S = p->b;
+      t.off = 0;
+      t.T = p->T;
+      st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient block spectra",
+                 [&] { return oaa::launch_window_rfft2(p->L, t, s); });
+    } else {
+      oaa::TileFwdParams t{};
+      t.src = g;
+      t.dst = region(p, OAA_REGION_G_SPECTRUM);
+      t.n_img = p->B;
+      t.n_ch = p->K;
+      t.H = p->M;
+      t.pitch = p->b;
+      t.off = 0;
+      t.R = p->b;
+      t.T = p->T;
+      st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient block spectra",
+                 [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+    }
     if (st == OAA_OK) p->g_valid = true;
     return st;
   }

@@ -625,6 +625,17 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
   }
 }
 
+// x / d for 0 <= x < 2^16 and 0 < d < 2^16 without a division: for d >= 2,
+// m = floor((2^32 - 1) / d) + 1 lies in (2^32 / d, 2^32 / d + 1], so x m / 2^32
+// exceeds x / d by less than x / 2^32 < 1 / d and its floor is x / d. d = 1
+// (where m would be 2^32) is taken apart.
+struct SmallDiv {
+  int d;
+  unsigned m;
+  __device__ __forceinline__ explicit SmallDiv(int d_) : d(d_), m(d_ > 1 ? 0xffffffffu / unsigned(d_) + 1u : 0u) {}
+  __device__ __forceinline__ int operator()(int x) const { return d > 1 ? int(__umulhi(unsigned(x), m)) : x; }
+};
+
 // ---------------------------------------------------------------------------
 // Inverse + top-left n x n crop, scattered to the blocks of the output planes.
 // A workgroup takes TQ consecutive tiles of one channel (they may span block
@@ -744,10 +755,11 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
   }
   __syncthreads();
   // row r of every tile, tiles in order: neighbouring tiles of a block row
-  // are neighbours in the output row
+  // are neighbours in the output row (n * nq * n < 2^16: launcher)
+  const SmallDiv div_n(n), div_nq(nq);
   for (int e = tid; e < n * nq * n; e += nthr) {
-    const int s = e % n, rest = e / n;
-    const int q = rest % nq, r = rest / nq;
+    const int rest = div_n(e), s = e - rest * n;
+    const int r = div_nq(rest), q = rest - r * nq;
     const int lim = tbase[2 * p.TQ + q];
     if (r < (lim >> 16) && s < (lim & 0xffff)) {
       float* o = p.dst + (size_t(tbase[p.TQ + q]) * p.n_ch + ch) * H * H;
@@ -870,6 +882,7 @@ hipError_t launch_crop_LF(CropParams p, hipStream_t s) {
   const long want = (long(p.n_ch) * tiles + 2047) / 2048;
   if (want < tq) tq = std::max<long>(want, 1);
   if (tq > tiles) tq = tiles;
+  if (long(p.n) * p.n * tq >= 65536) tq = std::max<long>(1, 65535 / (long(p.n) * p.n));
   const long nchunk = (tiles + tq - 1) / tq;
   p.TQ = int((tiles + nchunk - 1) / nchunk);
   p.nchunk = int(nchunk);

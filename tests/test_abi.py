@@ -10,6 +10,8 @@ import ctypes
 import os
 import re
 
+import numpy as np
+
 import pytest
 
 from paper_1601_06815_amd import binding, build
@@ -274,3 +276,15 @@ def test_method_plan_validation(lib, dims, status):
     st = lib.oaa_plan_create_method(ctypes.byref(h), *dims)
     assert st == status and not h.value
     assert lib.oaa_last_error_detail()
+
+
+def test_small_division_by_reciprocal_is_exact():
+    """The inverse kernels divide small lane indices x < 2^16 by a divisor
+    d < 2^16 as floor(x m / 2^32) with m = floor((2^32 - 1) / d) + 1 (d >= 2;
+    d = 1 is taken apart, m would be 2^32): exact for every such x."""
+    x = np.arange(1 << 16, dtype=np.uint64)
+    for d in list(range(2, 1025)) + [4095, 4096, 4097, 65535]:
+        m = np.uint64(0xFFFFFFFF // d + 1)
+        assert m < (1 << 32)
+        assert np.array_equal((x * m) >> np.uint64(32), x // np.uint64(d)), d
+    assert (0xFFFFFFFF // 1 + 1) & 0xFFFFFFFF == 0  # why d = 1 needs its own path

@@ -42,10 +42,12 @@ def stage_work(ly, geo):
     # products (Gauss), i.e. 6 real flops, where the textbook count is 8
     Fu = (L // 2 + 1) ** 2 + (L // 2 - 1) ** 2
     prod_flops = 6.0 * BP * C * K * Fu
+    # the transforms' outputs count the same unique bins (the others are
+    # conjugates that no later stage reads)
     return {
-        "w_spectrum": dict(bytes=K * C * n * n * 4 + F * C * K * cplx),
-        "x_spectrum": dict(bytes=B * C * N * N * 4 + F * C * BP * cplx),
-        "g_spectrum": dict(bytes=B * K * M * M * 4 + F * K * BP * cplx),
+        "w_spectrum": dict(bytes=K * C * n * n * 4 + Fu * C * K * cplx),
+        "x_spectrum": dict(bytes=B * C * N * N * 4 + Fu * C * BP * cplx),
+        "g_spectrum": dict(bytes=B * K * M * M * 4 + Fu * K * BP * cplx),
         "fwd_product": dict(flops=prod_flops, bytes=(Fu * C * K + Fu * C * BP + Fu * K * BP) * cplx),
         "fwd_inverse": dict(bytes=Fu * K * BP * cplx + B * K * M * M * 4),
         "bwd_data_product": dict(flops=prod_flops, bytes=(Fu * C * K + Fu * K * BP + Fu * C * BP) * cplx),
@@ -133,7 +135,7 @@ def cpu_baseline(ly, x, w, g, budget_s=20.0):
 
 STAGE_ORDER = ["w_spectrum", "x_spectrum", "fwd_product", "fwd_inverse", "g_spectrum", "bwd_data_product",
                "bwd_data_inverse", "bwd_filter_product", "bwd_filter_inverse"]
-LIB_KERNELS = ("tile_rfft2_kernel", "window_rfft2_kernel", "irfft2_", "cgemm_", "narrow_")
+LIB_KERNELS = ("tile_rfft2_kernel", "window_rfft2_kernel", "window_rows_rfft2_kernel", "irfft2_", "cgemm_", "narrow_")
 
 
 def _short_kernel(name):

@@ -113,8 +113,8 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
     for (int u = 0; u < L; ++u) {
       float2 c, a;
       if (O32) {
-        c = at_byte(bu, oc);
-        a = at_byte(bu, oa);
+        c = load_at(bu, oc);
+        a = load_at(bu, oa);
         advance_uniform(bu, ustride);
       } else {
         c = cur[u * ustride];
@@ -211,7 +211,7 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_FOLD)) irf
     if (c >= ce) continue;
     const float val = obuf[size_t(r) * OWp + c];
     if (O32)
-      at_byte(out, unsigned((i0 + r) * M + j0 + c) * 4u) = val;
+      store_at(out, unsigned((i0 + r) * M + j0 + c) * 4u, val);
     else
       out[size_t(i0 + r) * M + j0 + c] = val;
   }
@@ -275,8 +275,8 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_runs_kernel(FoldCropP
 #pragma unroll
         for (int u = 0; u <= L / 2; ++u) {
           const float2 tw = twiddle<L, +1>(b * u);
-          const float2 c0 = at_byte(bu, lo), a0 = at_byte(bu, la);
-          const float2 c1 = at_byte(bu, lo + lh), a1 = at_byte(bu, la + lh);
+          const float2 c0 = load_at(bu, lo), a0 = load_at(bu, la);
+          const float2 c1 = load_at(bu, lo + lh), a1 = load_at(bu, la + lh);
           h0[u] = cmad(c0, tw, up ? a0 : zero2);
           h1[u] = cmad(c1, tw, up ? a1 : zero2);
           advance_uniform(bu, size_t(V) * fstride);
@@ -292,7 +292,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_runs_kernel(FoldCropP
       } else {
 #pragma unroll
         for (int u = 0; u < L; ++u) {
-          const float2 c = at_byte(bu, lo), a = at_byte(bu, la);
+          const float2 c = load_at(bu, lo), a = load_at(bu, la);
           const float2 f = cmad(c, twiddle<L, +1>(b * u), up ? a : zero2);
           re[u] = f.x;
           im[u] = f.y;
@@ -363,7 +363,7 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_runs_kernel(FoldCropP
   const int lw = 32 - __builtin_clz(unsigned(wr - 1) | 1u), cw = 1 << lw;
   for (int e = tid; e < (re_ - rb) << lw; e += nthr) {
     const int r = rb + (e >> lw), c = cb + (e & (cw - 1));
-    if (c < ce) at_byte(out, unsigned((i0 + r) * M + j0 + c) * 4u) = obuf[size_t(r) * OWp + c];
+    if (c < ce) store_at(out, unsigned((i0 + r) * M + j0 + c) * 4u, obuf[size_t(r) * OWp + c]);
   }
 }
 

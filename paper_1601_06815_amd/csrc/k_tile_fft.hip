@@ -537,8 +537,8 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
         for (int u = 0; u <= L / 2; ++u) {
           const int pu = bitrev(u, L), pm = bitrev((L - u) % L, L);
           const float ar = re[pu], ai = im[pu], br = re[pm], bi = im[pm];
-          at_byte(bu, lo) = make_float2(0.5f * (ar + br), 0.5f * (ai - bi));
-          at_byte(bu, lh) = make_float2(0.5f * (ai + bi), 0.5f * (br - ar));
+          store_at(bu, lo, make_float2(0.5f * (ar + br), 0.5f * (ai - bi)));
+          store_at(bu, lh, make_float2(0.5f * (ai + bi), 0.5f * (br - ar)));
           advance_uniform(bu, size_t(V) * fstride);
         }
       } else {
@@ -546,7 +546,7 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
 #pragma unroll
         for (int u = 0; u < L; ++u) {
           const int pu = bitrev(u, L);
-          at_byte(bu, lo) = make_float2(re[pu], im[pu]);
+          store_at(bu, lo, make_float2(re[pu], im[pu]));
           advance_uniform(bu, size_t(V) * fstride);
         }
       }

@@ -132,16 +132,28 @@ __device__ __forceinline__ void stage_rows(float* dst, int Wp, const float* src,
   }
 }
 
-// Element at byte offset `boff` from a wave-uniform base: the compiler then
-// addresses with the base in scalar registers and a 32-bit lane offset, with
-// no 64-bit arithmetic per access.
+// Loads and stores of global memory at byte offset `boff` from a
+// wave-uniform base: the compiler then addresses with the base in scalar
+// registers and a 32-bit lane offset, with no 64-bit arithmetic per access.
+// The global address space is spelled out, since a generic pointer (one
+// rebuilt from integers, say) would compile to flat accesses, which also
+// count as LDS operations in the wave's wait counters.
 template <class T>
-__device__ __forceinline__ T& at_byte(T* base, unsigned boff) {
-  return *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + boff);
+using global_t = __attribute__((address_space(1))) T;
+typedef float f2_native __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float2 load_at(const float2* base, unsigned boff) {
+  const f2_native t = *(const global_t<f2_native>*)((const global_t<char>*)(base) + boff);
+  return make_float2(t.x, t.y);
 }
-template <class T>
-__device__ __forceinline__ const T& at_byte(const T* base, unsigned boff) {
-  return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + boff);
+__device__ __forceinline__ float load_at(const float* base, unsigned boff) {
+  return *(const global_t<float>*)((const global_t<char>*)(base) + boff);
+}
+__device__ __forceinline__ void store_at(float2* base, unsigned boff, float2 v) {
+  *(global_t<f2_native>*)((global_t<char>*)(base) + boff) = f2_native{v.x, v.y};
+}
+__device__ __forceinline__ void store_at(float* base, unsigned boff, float v) {
+  *(global_t<float>*)((global_t<char>*)(base) + boff) = v;
 }
 
 // Advances a wave-uniform pointer by `step` elements. The empty asm keeps
@@ -176,7 +188,7 @@ __device__ __forceinline__ void stage_rows32(float* dst, int Wp, const float* pl
         const int r = rb + j * rstep;
         const int gr = row0 + r;
         const bool ok = col_ok && r < R && gr >= 0 && gr < H;
-        const float t = at_byte(plane, ok ? unsigned(gr * H + gc) * 4u : 0u);
+        const float t = load_at(plane, ok ? unsigned(gr * H + gc) * 4u : 0u);
         v[j] = ok ? t : 0.f;
       }
 #pragma unroll

@@ -576,7 +576,9 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
 // in[q], q < nq (bin f at in[q + f * fstride], plus nsplit - 1 partial sums
 // spaced split_stride apart), transform every column v and keep rows
 // [0, ROWS) at zbuf[q * TS + r * V + v].
-template <int L, int ROWS>
+// O32: bins addressed as 32-bit lane offsets (v fstride + q) * 8 from
+// wave-uniform row bases (the caller checks V fstride * 8 < 2^32).
+template <int L, int ROWS, bool O32>
 __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride, int nsplit,
                                                 size_t split_stride, int nq, int TS, float2* zbuf) {
   constexpr int V = L / 2 + 1;
@@ -584,18 +586,23 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
   for (int task = threadIdx.x; task < V * nq; task += blockDim.x) {
     const int q = task % nq, v = task / nq;
     const float2* col = in + q + size_t(v) * fstride;
+    const unsigned lo = unsigned((size_t(v) * fstride + q) * 8u);
     float re[L], im[L];
+    const float2* bu = in;
 #pragma unroll
     for (int u = 0; u < L; ++u) {
-      const float2 z = col[u * ustride];
+      const float2 z = O32 ? load_at(bu, lo) : col[u * ustride];
+      if (O32) advance_uniform(bu, ustride);
       re[u] = z.x;
       im[u] = z.y;
     }
     for (int s = 1; s < nsplit; ++s) {
       const float2* cs = col + s * split_stride;
+      const float2* bs = in + s * split_stride;
 #pragma unroll
       for (int u = 0; u < L; ++u) {
-        const float2 z = cs[u * ustride];
+        const float2 z = O32 ? load_at(bs, lo) : cs[u * ustride];
+        if (O32) advance_uniform(bs, ustride);
         re[u] += z.x;
         im[u] += z.y;
       }
@@ -640,7 +647,7 @@ struct SmallDiv {
 // Inverse + top-left n x n crop, scattered to the blocks of the output planes.
 // A workgroup takes TQ consecutive tiles of one channel (they may span block
 // rows and images), so its spectrum reads are contiguous.
-template <int L, bool FULL>
+template <int L, bool FULL, bool O32>
 __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irfft2_crop_kernel(CropParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int RT = FULL ? L : L / 2;  // rows kept from the column transforms (>= n)
@@ -724,7 +731,7 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_CROP)) irf
       }
     }
   } else {
-    inverse_columns<L, RT>(p.src + size_t(ch) * tiles + t0, fstride, p.nsplit, p.split_stride, nq, TS, zbuf);
+    inverse_columns<L, RT, O32>(p.src + size_t(ch) * tiles + t0, fstride, p.nsplit, p.split_stride, nq, TS, zbuf);
   }
   __syncthreads();
   for (int task = tid; task < (SPLIT ? 0 : npair * nq); task += nthr) {
@@ -889,7 +896,9 @@ hipError_t launch_crop_LF(CropParams p, hipStream_t s) {
   const size_t lds = per_tile * p.TQ;
   const int tasks = (L >= 64 ? 2 : 1) * std::max(V * p.TQ, ((p.n + 1) / 2) * p.TQ);
   const long nwg = long(p.n_ch) * p.nchunk;
-  hipLaunchKernelGGL((irfft2_crop_kernel<L, FULL>), dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
+  const bool o32 = OAA_CROP_O32 && size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32);
+  auto kern = o32 ? irfft2_crop_kernel<L, FULL, true> : irfft2_crop_kernel<L, FULL, false>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }
 

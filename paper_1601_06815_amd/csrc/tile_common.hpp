@@ -26,6 +26,9 @@
 #ifndef OAA_FWD_TQ_MAX
 #define OAA_FWD_TQ_MAX 64
 #endif
+#ifndef OAA_CROP_O32
+#define OAA_CROP_O32 1
+#endif
 #ifndef OAA_CROP_TQ_MAX
 #define OAA_CROP_TQ_MAX 64
 #endif

@@ -379,7 +379,9 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_fold_runs_kernel(FoldCropP
 // floats of a row); then every output pixel of the block row is the sum, in
 // a fixed order, of its tile's value and the overhangs of the left, upper and
 // upper-left neighbours.
-template <int L>
+// O32: bins read at 32-bit lane offsets from wave-uniform row bases and
+// output pixels written at 32-bit offsets from the plane (launcher checks).
+template <int L, bool O32>
 __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCropParams p) {
   constexpr int V = L / 2 + 1;
   extern __shared__ float smem[];
@@ -447,6 +449,8 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
     const int Qt = q0 - 1 + qq, Pt = strip - part;
     const bool live = Qt >= 0 && Qt < T && Pt >= 0 && Pt < T && (part == 0 || na > 0);
     const float2* col = in + size_t(live ? Pt : 0) * T + (live ? Qt : 0) + size_t(v) * fstride;
+    const unsigned lo = unsigned((size_t(v) * fstride + size_t(live ? Pt : 0) * T + (live ? Qt : 0)) * 8u);
+    const float2* bu = in;
     // columns v = 0 and v = L/2 hold no products in rows u > L/2 (Hermitian
     // there): inverse of the rows [0, L/2] with rows 0, L/2 halved, twice
     // the real part
@@ -454,7 +458,8 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
     float re[L], im[L];
 #pragma unroll
     for (int u = 0; u < L; ++u) {
-      const float2 z = col[u * ustride];
+      const float2 z = O32 ? load_at(bu, lo) : col[u * ustride];
+      if (O32) advance_uniform(bu, ustride);
       float zr = live ? z.x : 0.f, zi = live ? z.y : 0.f;
       if (u > L / 2) {
         zr = mir ? 0.f : zr;
@@ -545,9 +550,14 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
   const int cb = max(0, -j0), ce = min(W, M - j0);
   const int wr = ce - cb;
   if (wr <= 0 || re_ <= rb) return;
-  for (int e = tid; e < (re_ - rb) * wr; e += nthr) {
-    const int r = rb + e / wr, c = cb + e % wr;
-    const int q = c / b, s = c - q * b;
+  // lanes over columns in rows of a power-of-two width; column / b by a
+  // reciprocal multiply (c < TQ b, which the LDS budget keeps below 2^13)
+  const int lw = 32 - __builtin_clz(unsigned(wr - 1) | 1u), cw = 1 << lw;
+  const SmallDiv div_b(b);
+  for (int e = tid; e < (re_ - rb) << lw; e += nthr) {
+    const int r = rb + (e >> lw), c = cb + (e & (cw - 1));
+    if (c >= ce) continue;
+    const int q = div_b(c), s = c - q * b;
     const float* own = sc + (q + 1) * SSc + r * RS;
     const float* left = sc + q * SSc + r * RS;
     float v = own[s];
@@ -556,7 +566,10 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
       v += sa[(q + 1) * SSa + r * RS + s];
       if (s < na) v += sa[q * SSa + r * RS + b + s];
     }
-    out[size_t(i0 + r) * M + j0 + c] = v;
+    if (O32)
+      store_at(out, unsigned((i0 + r) * M + j0 + c) * 4u, v);
+    else
+      out[size_t(i0 + r) * M + j0 + c] = v;
   }
 }
 
@@ -625,7 +638,10 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
   const size_t lds = per_tile * (p.TQ + 1);
   const int tasks = (L >= 64 ? 2 : 1) * std::max(2 * (p.TQ + 1) * V, (p.TQ + 1) * ((b + 1) / 2 + (na + 1) / 2));
   const long nwg = planes * p.To * p.nchunk;
-  hipLaunchKernelGGL(irfft2_overlap_crop_kernel<L>, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
+  const bool o32 = size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32) &&
+                   size_t(p.M) * p.M * 4 < (size_t(1) << 32);
+  auto kern = o32 ? irfft2_overlap_crop_kernel<L, true> : irfft2_overlap_crop_kernel<L, false>;
+  hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(pick_threads(tasks)), lds, s, p);
   return hipGetLastError();
 }
 

@@ -632,16 +632,6 @@ __device__ __forceinline__ void inverse_columns(const float2* in, size_t fstride
   }
 }
 
-// x / d for 0 <= x < 2^16 and 0 < d < 2^16 without a division: for d >= 2,
-// m = floor((2^32 - 1) / d) + 1 lies in (2^32 / d, 2^32 / d + 1], so x m / 2^32
-// exceeds x / d by less than x / 2^32 < 1 / d and its floor is x / d. d = 1
-// (where m would be 2^32) is taken apart.
-struct SmallDiv {
-  int d;
-  unsigned m;
-  __device__ __forceinline__ explicit SmallDiv(int d_) : d(d_), m(d_ > 1 ? 0xffffffffu / unsigned(d_) + 1u : 0u) {}
-  __device__ __forceinline__ int operator()(int x) const { return d > 1 ? int(__umulhi(unsigned(x), m)) : x; }
-};
 
 // ---------------------------------------------------------------------------
 // Inverse + top-left n x n crop, scattered to the blocks of the output planes.

@@ -159,6 +159,17 @@ __device__ __forceinline__ void store_at(float* base, unsigned boff, float v) {
   *(global_t<float>*)((global_t<char>*)(base) + boff) = v;
 }
 
+// x / d for 0 <= x < 2^16 and 0 < d < 2^16 without a division: for d >= 2,
+// m = floor((2^32 - 1) / d) + 1 lies in (2^32 / d, 2^32 / d + 1], so x m / 2^32
+// exceeds x / d by less than x / 2^32 < 1 / d and its floor is x / d. d = 1
+// (where m would be 2^32) is taken apart.
+struct SmallDiv {
+  int d;
+  unsigned m;
+  __device__ __forceinline__ explicit SmallDiv(int d_) : d(d_), m(d_ > 1 ? 0xffffffffu / unsigned(d_) + 1u : 0u) {}
+  __device__ __forceinline__ int operator()(int x) const { return d > 1 ? int(__umulhi(unsigned(x), m)) : x; }
+};
+
 // Advances a wave-uniform pointer by `step` elements. The empty asm keeps
 // the pointer in one scalar register pair: without it the compiler
 // precomputes the addresses of a whole unrolled loop and runs out of scalar

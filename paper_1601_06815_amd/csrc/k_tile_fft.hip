@@ -817,7 +817,7 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     p.nchunk = (p.T + p.TQ - 1) / p.TQ;
     int rw = 1;
     if (p.nchunk == 1)
-      while (rw * p.T < 16 && rw < p.T && lds_rows(p.TQ, rw + 1) <= kLdsRowsBudget) ++rw;
+      while (rw * p.T < OAA_WINDOW_MIN_RUN && rw < p.T && lds_rows(p.TQ, rw + 1) <= kLdsRowsBudget) ++rw;
     p.RW = rw;
     // the next step's (rw - 1) n + S rows of (TQ - 1) n + S columns in registers
     const long staged = long((rw - 1) * p.n + p.S) * long((p.TQ - 1) * p.n + p.S);

@@ -14,6 +14,10 @@
 #ifndef OAA_WINDOW_ROWS
 #define OAA_WINDOW_ROWS 1
 #endif
+// Consecutive tiles a step of the several-rows window transform aims for.
+#ifndef OAA_WINDOW_MIN_RUN
+#define OAA_WINDOW_MIN_RUN 16
+#endif
 #ifndef OAA_WINDOW_PREFETCH
 #define OAA_WINDOW_PREFETCH 1
 #endif

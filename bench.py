@@ -301,6 +301,20 @@ def config_report(args):
             st = plan.stage_times()
             plan.set_timing(False)
             med, mean10 = float(np.median(ts)), float(np.mean(ts[:10]))
+            # the same pass replayed from a HIP graph (launch overheads removed)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                call()
+            graph.replay()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(20):
+                graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ms_graph = e0.elapsed_time(e1) / 20
+            del graph
             stages = {}
             for sname, (ms, cnt) in st.items():
                 if not cnt or sname not in PASS_STAGES[pas]:
@@ -316,6 +330,7 @@ def config_report(args):
                 stages[sname] = {"ms": sm, "share": sm / med, "bound": bound, "frac": frac}
             cpu_ms, cpu_note = oracle_pass_ms(ly, x, w, g, pas, args.cpu_budget / 4)
             row = {"layer": name, "pass": pas, "L": geo["L"], "b": geo["b"], "ms_median": med, "ms_mean10": mean10,
+                   "ms_graph": ms_graph,
                    "tflops_direct_eq": ly.direct_flops() / (med * 1e-3) / 1e12, "stages": stages,
                    "oracle_ms": cpu_ms, "oracle_sample": cpu_note, "speedup_vs_oracle": cpu_ms / med}
             rows.append(row)
@@ -323,9 +338,9 @@ def config_report(args):
         del plan
         torch.cuda.empty_cache()
 
-    print("| layer | pass | (L, b) | ms median | ms mean of 10 | direct-eq TFLOP/s | stages: share, roofline fraction "
-          "| fp64 oracle ms (host) | GPU / oracle |")
-    print("|---|---|---|---|---|---|---|---|---|")
+    print("| layer | pass | (L, b) | ms median | ms mean of 10 | ms graph replay | direct-eq TFLOP/s "
+          "| stages: share, roofline fraction | fp64 oracle ms (host) | GPU / oracle |")
+    print("|---|---|---|---|---|---|---|---|---|---|")
     for r in rows:
         # layers whose data stays in L2 and whose stages last a few
         # microseconds are bound by launch latency: no roofline fraction
@@ -335,7 +350,7 @@ def config_report(args):
         if small:
             st += " (latency-bound)"
         print(f"| {r['layer']} | {r['pass']} | ({r['L']}, {r['b']}) | {r['ms_median']:.4f} | {r['ms_mean10']:.4f} "
-              f"| {r['tflops_direct_eq']:.2f} | {st} | {r['oracle_ms']:.1f} ({r['oracle_sample']}) "
+              f"| {r['ms_graph']:.4f} | {r['tflops_direct_eq']:.2f} | {st} | {r['oracle_ms']:.1f} ({r['oracle_sample']}) "
               f"| {r['speedup_vs_oracle']:.0f}× |")
     r8 = next(r for r in rows if r["layer"] == "plane224_n8")
     xs = r8["stages"].get("x_spectrum", {"share": 0.0})["share"]
@@ -452,6 +467,22 @@ def main():
     ms_step = ms_total / args.steps
     print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
 
+    # the same step captured once in a HIP graph and replayed (no per-stage
+    # events): what a training loop that replays its step would see
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    graph.replay()
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_graph = ev0.elapsed_time(ev1) / args.steps
+    del graph
+    print(f"[bench] graph replays: {ms_graph:.3f} ms/step", file=sys.stderr, flush=True)
+
     direct = 3 * ly.direct_flops()
     value = direct / (ms_step * 1e-3) / 1e12
     work = stage_work(ly, geo)
@@ -513,6 +544,7 @@ def main():
                    "method": args.method,
                    "contraction": args.contraction},
         "roofline": roof,
+        "graph_ms_per_step": ms_graph,
         "stages": per_stage,
         "sampled_rel_err": err,
     }

@@ -322,6 +322,46 @@ def test_zero_inputs_give_exact_zeros(gpu_lib):
     assert not y.any() and not dx.any() and not dw.any()
 
 
+def test_graph_capture_replays_match_eager(gpu_lib):
+    """A training step (forward, backward-data with cached kernel spectra,
+    backward-filter with cached input and gradient spectra) captured in a
+    HIP graph: several replays, with eager work on the outputs in between,
+    each equal bit for bit to the eager step."""
+    B, C, K, N, n = 2, 8, 70, 41, 5
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=53)
+    plan = binding.Plan(B, C, K, N, n, device=DEV)
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    M = N - n + 1
+    y = torch.empty((B, K, M, M), dtype=torch.float32, device=DEV)
+    dx, dw = torch.empty_like(xd), torch.empty_like(wd)
+
+    def step():
+        plan.forward(xd, wd, y)
+        plan.backward_data(gd, None, dx)
+        plan.backward_filter(None, None, dw)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    ref = (y.clone(), dx.clone(), dw.clone())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for i in range(4):
+        y.fill_(float(i + 1))
+        dx.mul_(0.5)
+        dw.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref[0]) and torch.equal(dx, ref[1]) and torch.equal(dw, ref[2]), i
+    e = relerr(y.cpu().numpy(), oracle.conv_forward(x, w))
+    assert e <= TOL, e
+
+
 def test_named_stream_is_used(gpu_lib):
     B, C, K, N, n = 2, 3, 4, 32, 5
     x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=8)

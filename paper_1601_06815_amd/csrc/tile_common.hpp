@@ -60,9 +60,10 @@ constexpr int fft_waves(int want) { return L <= 32 ? want : 1; }
 
 constexpr int kMaxThreads = 256;
 constexpr size_t kLdsBudget = 60 * 1024;
-// LDS of the kernels that transform several window rows per step: two
-// workgroups per CU
-constexpr size_t kLdsRowsBudget = 80 * 1024;
+// LDS of the kernels that transform several window rows per step, for two
+// workgroups per CU. Measured: 77056 bytes per workgroup keeps two resident,
+// 80128 bytes leaves one (the window transform ran twice as long).
+constexpr size_t kLdsRowsBudget = 76 * 1024;
 // registers per lane for the next step's rows in those kernels
 constexpr int kWindowPrefetch = 32;
 

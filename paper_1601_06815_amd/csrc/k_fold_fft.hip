@@ -629,7 +629,7 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
   const int b = p.n, S = p.S, na = S - b;
   if (na < 0 || S > L || 2 * b <= L || p.To < p.T || p.shift < 0 || p.shift >= L) return hipErrorInvalidValue;
   const size_t per_tile = size_t(odd_at_least(b * V) + odd_at_least(na * V)) * 8;
-  int tq = std::min<int>(p.To, int(kLdsBudget / per_tile) - 1);
+  int tq = std::min<int>(std::min<int>(p.To, OAA_OVERLAP_TQ_MAX), int(kLdsBudget / per_tile) - 1);
   if (tq < 1) return hipErrorInvalidConfiguration;
   const int nchunk = (p.To + tq - 1) / tq;
   p.TQ = (p.To + nchunk - 1) / nchunk;

@@ -27,6 +27,9 @@
 #ifndef OAA_FOLD_TQ_MAX
 #define OAA_FOLD_TQ_MAX 64
 #endif
+#ifndef OAA_OVERLAP_TQ_MAX
+#define OAA_OVERLAP_TQ_MAX 64
+#endif
 #ifndef OAA_FWD_TQ_MAX
 #define OAA_FWD_TQ_MAX 64
 #endif
@@ -35,6 +38,9 @@
 #endif
 #ifndef OAA_CROP_TQ_MAX
 #define OAA_CROP_TQ_MAX 64
+#endif
+#ifndef OAA_CROP_TQ_SMALL
+#define OAA_CROP_TQ_SMALL 16
 #endif
 
 // Minimum waves per SIMD asked of the register allocator, per transform
@@ -60,10 +66,9 @@ constexpr int fft_waves(int want) { return L <= 32 ? want : 1; }
 
 constexpr int kMaxThreads = 256;
 constexpr size_t kLdsBudget = 60 * 1024;
-// LDS of the kernels that transform several window rows per step, for two
-// workgroups per CU. Measured: 77056 bytes per workgroup keeps two resident,
-// 80128 bytes leaves one (the window transform ran twice as long).
-constexpr size_t kLdsRowsBudget = 76 * 1024;
+// LDS of the kernels that transform several window rows per step: two
+// workgroups per CU
+constexpr size_t kLdsRowsBudget = 80 * 1024;
 // registers per lane for the next step's rows in those kernels
 constexpr int kWindowPrefetch = 32;
 

@@ -574,6 +574,163 @@ __global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_crop_kernel(FoldCr
 }
 
 // ---------------------------------------------------------------------------
+// Same result as irfft2_overlap_crop_kernel (2b > L, L <= 32). A workgroup
+// takes SPW consecutive block rows of a plane and walks down them, RB per
+// step.
+//
+// A step inverts the tiles of tile rows P .. P + RB - 1 (RB T consecutive
+// tiles, so every load instruction reads runs of RB T tiles of one bin) and
+// keeps rows and columns [0, S) of each inverse. Output block (P, Q) sums its
+// own tile, the overhang of its left neighbour, and the overhangs of the two
+// tiles above it: from LDS inside the step, and for the step's first block
+// row from a carry that the previous step left: the overhang rows of its last
+// tile row, already summed along the row. A workgroup that does not start at
+// block row 0 first inverts the tile row above its first block row, for the
+// carry alone. Each tile is thus loaded and inverted once, plus once more
+// per group boundary; the per-block-row kernel does both twice.
+//
+// LDS: zb [RB T][TSz] float2, TSz = S V rounded up to odd (column inverses,
+// rows [0, S) at stride V; after the row inverses row r of tile t holds S
+// reals from float 2 (t TSz + r V)), then carry [2][S - b][To b] floats.
+// Bins are read at 32-bit lane offsets and output pixels written at 32-bit
+// offsets (the launcher checks both fit).
+template <int L>
+__global__ void __launch_bounds__(kMaxThreads) irfft2_overlap_rows_kernel(FoldCropParams p) {
+  constexpr int V = L / 2 + 1;
+  extern __shared__ float smem[];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int b = p.n, S = p.S, na = S - b, T = p.T, To = p.To, M = p.M, RB = p.RB, sh = p.shift;
+  const int TSz = odd_at_least(S * V), CW = To * b;
+  float2* zb = reinterpret_cast<float2*>(smem);
+  const float* zr = smem;  // the same array, read as real rows
+  float* carry = smem + size_t(RB) * T * TSz * 2;
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
+  const int grp = int(wg % p.ngroups);
+  const unsigned plane = wg / p.ngroups;
+  const int Pb = grp * p.SPW, Pe = min(To, Pb + p.SPW);  // output block rows of this workgroup
+  const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
+  const size_t tiles_per_ch = size_t(p.n_img) * T * T;
+  const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
+  const size_t ustride = size_t(V) * fstride;
+  const float2* in = p.src + size_t(ch) * tiles_per_ch + size_t(img) * T * T;
+  float* out = p.dst + size_t(plane) * M * M;
+  const float scale = 1.0f / float(L * L);
+  // lanes over output columns in rows of a power-of-two width; divisions by
+  // b through a reciprocal multiply (operands below To b and RB b, < 2^16)
+  const int lw = 32 - __builtin_clz(unsigned(CW - 1) | 1u), cw = 1 << lw;
+  const SmallDiv div_b(b);
+  // real value at row r, column s of tile (row pl of the step, column q)
+  auto at = [&](int pl, int q, int r, int s) { return zr[2 * ((pl * T + q) * TSz + r * V) + s]; };
+  // overhang rows [b, S) of tile row pl at output column c = q b + s: its own
+  // tile and the left neighbour's overhang columns
+  auto overhang = [&](int pl, int q, int s, int rr) {
+    float v = q < T ? at(pl, q, b + rr, s) : 0.f;
+    if (s < na && q > 0) v += at(pl, q - 1, b + rr, b + s);
+    return v;
+  };
+  for (int e = tid; e < na * CW; e += nthr) carry[e] = 0.f;  // nothing above block row 0
+  int cur = 0;
+  // step at tile row P0: tile rows P0 .. P0 + tr - 1, output block rows
+  // P0 .. P0 + orow - 1; the first step of a later group is the tile row
+  // above the group (Pb - 1), with no output rows
+  for (int P0 = Pb > 0 ? Pb - 1 : 0; P0 < Pe;) {
+    const bool halo = P0 < Pb;
+    const int tr = halo ? 1 : max(0, min(RB, T - P0));  // tile rows of this step
+    const int orow = halo ? 0 : min(RB, Pe - P0);       // output block rows of this step
+    const int nt = tr * T;
+    // column inverses; columns v = 0 and v = L/2 hold no bins in rows
+    // u > L/2 (Hermitian there): inverse of rows [0, L/2] with rows 0 and L/2
+    // halved, twice the real part
+    for (int task = tid; task < nt * V; task += nthr) {
+      const int t = task % nt, v = task / nt;
+      const unsigned lo = unsigned((size_t(v) * fstride + size_t(P0) * T + t) * 8u);
+      const bool mir = v == 0 || v == L / 2;
+      const float2* bu = in;
+      float re[L], im[L];
+#pragma unroll
+      for (int u = 0; u < L; ++u) {
+        float2 z = make_float2(0.f, 0.f);
+        if (u <= L / 2 || !mir) z = load_at(bu, lo);
+        advance_uniform(bu, ustride);
+        if (u == 0 || u == L / 2) {
+          z.x *= mir ? 0.5f : 1.f;
+          z.y *= mir ? 0.5f : 1.f;
+        }
+        re[u] = z.x;
+        im[u] = z.y;
+      }
+      fft_dif<L, +1, false>(re, im);
+      const float rs = mir ? 2.f : 1.f, is = mir ? 0.f : 1.f;
+      float2* zt = zb + t * TSz + v;
+      // row r of the inverse is row (r + shift) mod L of the tile
+#pragma unroll
+      for (int r = 0; r < L; ++r) {
+        const int rt = (r + sh) & (L - 1);
+        if (rt < S) zt[rt * V] = make_float2(re[bitrev(r, L)] * rs, im[bitrev(r, L)] * is);
+      }
+    }
+    __syncthreads();
+    // row inverses of row pairs, written over the pair's own spectrum rows
+    const int ps = (S + 1) / 2;
+    for (int task = tid; task < nt * ps; task += nthr) {
+      const int t = task % nt, r0 = 2 * (task / nt);
+      const bool has1 = r0 + 1 < S;
+      float2* zt = zb + t * TSz + r0 * V;
+      float2 A[V], Bv[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        A[v] = zt[v];
+        Bv[v] = has1 ? zt[V + v] : make_float2(0.f, 0.f);
+      }
+      float xr[L], xi[L];
+      irfft_pair<L>(A, Bv, xr, xi);
+      float* d0 = reinterpret_cast<float*>(zt);
+#pragma unroll
+      for (int s2 = 0; s2 < L; ++s2) {
+        const int st = (s2 + sh) & (L - 1);  // column s2 of the inverse is column st of the tile
+        if (st < S) {
+          d0[st] = xr[bitrev(s2, L)] * scale;
+          if (has1) d0[2 * V + st] = xi[bitrev(s2, L)] * scale;
+        }
+      }
+    }
+    __syncthreads();
+    // output block rows P0 .. P0 + orow - 1: pixel (P b - off + rr, c - off)
+    const float* cin = carry + cur * na * CW;
+    for (int e = tid; e < (orow * b) << lw; e += nthr) {
+      const int r = e >> lw, c = e & (cw - 1);
+      if (c >= CW) continue;
+      const int pl = div_b(r), rr = r - pl * b;
+      const int q = div_b(c), s = c - q * b;
+      const int i = (P0 + pl) * b - p.off + rr, j = c - p.off;
+      if (i < 0 || i >= M || j < 0 || j >= M) continue;
+      float v = 0.f;
+      if (pl < tr) {
+        if (q < T) v = at(pl, q, rr, s);
+        if (s < na && q > 0) v += at(pl, q - 1, rr, b + s);
+      }
+      if (rr < na) v += pl == 0 ? cin[rr * CW + c] : (pl - 1 < tr ? overhang(pl - 1, q, s, rr) : 0.f);
+      store_at(out, unsigned(i * M + j) * 4u, v);
+    }
+    // carry of the next step: the overhang rows of this step's last tile row
+    // (the next step starts right below it whenever there is one)
+    const int next = halo ? Pb : P0 + RB;
+    if (next < Pe) {
+      float* cn = carry + (cur ^ 1) * na * CW;
+      for (int e = tid; e < na << lw; e += nthr) {
+        const int rr = e >> lw, c = e & (cw - 1);
+        if (c >= CW) continue;
+        const int q = div_b(c), s = c - q * b;
+        cn[rr * CW + c] = tr > 0 ? overhang(tr - 1, q, s, rr) : 0.f;
+      }
+      cur ^= 1;
+    }
+    __syncthreads();
+    P0 = next;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 
 template <int L>
@@ -628,13 +785,39 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
   constexpr int V = L / 2 + 1;
   const int b = p.n, S = p.S, na = S - b;
   if (na < 0 || S > L || 2 * b <= L || p.To < p.T || p.shift < 0 || p.shift >= L) return hipErrorInvalidValue;
+  const long planes = long(p.n_img) * p.n_ch;
+  // a workgroup per plane, RB block rows per step: runs of at least 16 tiles
+  // where LDS allows (L >= 4: below, the rows are too short to matter)
+  if (L >= 4 && L <= 32 && OAA_OVERLAP_ROWS && p.To <= p.T + 1 && size_t(p.M) * p.M * 4 < (size_t(1) << 32) &&
+      size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32) && long(p.To) * b < 65536) {
+    const size_t tsz = size_t(odd_at_least(S * V)) * 8;
+    const size_t cbytes = size_t(2) * na * p.To * b * 4;
+    auto lds_for = [&](int rb) { return size_t(rb) * p.T * tsz + cbytes; };
+    int rb = std::min(std::max(1, (16 + p.T - 1) / p.T), p.To);
+    while (rb > 1 && lds_for(rb) > kLdsBudget) --rb;
+    // measured: faster with several block rows per step, or at L <= 16 with
+    // enough planes to fill the GPU; one L = 32 row per step is slower than
+    // the per-block-row kernel, which keeps more workgroups in flight
+    if ((rb >= 2 || (L <= 16 && planes >= 1024)) && lds_for(rb) <= kLdsBudget && long(rb) * b < 65536) {
+      p.RB = rb;
+      // groups of block rows so that there are about OAA_OVERLAP_MIN_WG
+      // workgroups (one tile row more is inverted per group)
+      const int steps = (p.To + rb - 1) / rb;
+      const long ng = std::min<long>(steps, std::max<long>(1, (OAA_OVERLAP_MIN_WG + planes - 1) / planes));
+      p.SPW = int((steps + ng - 1) / ng) * rb;
+      p.ngroups = (p.To + p.SPW - 1) / p.SPW;
+      const int nt = rb * p.T;
+      const int nthr = pick_threads(std::max(nt * V, nt * ((S + 1) / 2)));
+      hipLaunchKernelGGL(irfft2_overlap_rows_kernel<L>, dim3(unsigned(planes * p.ngroups)), dim3(nthr), lds_for(rb), s, p);
+      return hipGetLastError();
+    }
+  }
   const size_t per_tile = size_t(odd_at_least(b * V) + odd_at_least(na * V)) * 8;
   int tq = std::min<int>(std::min<int>(p.To, OAA_OVERLAP_TQ_MAX), int(kLdsBudget / per_tile) - 1);
   if (tq < 1) return hipErrorInvalidConfiguration;
   const int nchunk = (p.To + tq - 1) / tq;
   p.TQ = (p.To + nchunk - 1) / nchunk;
   p.nchunk = nchunk;
-  const long planes = long(p.n_img) * p.n_ch;
   const size_t lds = per_tile * (p.TQ + 1);
   const int tasks = (L >= 64 ? 2 : 1) * std::max(2 * (p.TQ + 1) * V, (p.TQ + 1) * ((b + 1) / 2 + (na + 1) / 2));
   const long nwg = planes * p.To * p.nchunk;

@@ -73,7 +73,7 @@ struct FoldCropParams {
   int shift;          // each tile is the inverse transform circularly shifted
                       // down and right by `shift` (0 for the forward pass)
   int TQ, nchunk, SPW, ngroups;
-  int RB;             // block rows per step of the walking kernel (launcher)
+  int RB;             // block rows per workgroup or per step (set by the launcher)
 };
 
 // Batched complex matrix product, one problem per frequency bin f:

@@ -27,6 +27,12 @@
 #ifndef OAA_FOLD_TQ_MAX
 #define OAA_FOLD_TQ_MAX 64
 #endif
+#ifndef OAA_OVERLAP_ROWS
+#define OAA_OVERLAP_ROWS 1
+#endif
+#ifndef OAA_OVERLAP_MIN_WG
+#define OAA_OVERLAP_MIN_WG 4096
+#endif
 #ifndef OAA_OVERLAP_TQ_MAX
 #define OAA_OVERLAP_TQ_MAX 64
 #endif

@@ -169,6 +169,44 @@ def test_forward_block_row_runs(gpu_lib, shape):
     assert e <= TOL, e
 
 
+OVERLAP_WALK = [  # (B, C, K, N, n, L, b), 2b > L: the forward inverse walks down groups of
+    # block rows (several per step, or one at L <= 16 on many planes), each group after the
+    # first starting from the tile row above it
+    (1, 2, 1200, 60, 5, 16, 12),   # T = 5: four block rows per step, groups of 4 and 1
+    (1, 2, 1100, 72, 7, 16, 10),   # T = 8: two per step, four groups of one step each
+    (2, 1, 600, 100, 3, 8, 6),     # T = 17 at L = 8: one per step, four groups
+    (1, 3, 40, 70, 9, 32, 20),     # L = 32, T = 4: three per step (LDS), groups of 3 and 1
+    (1, 1, 1030, 47, 4, 16, 11),   # T = 5, ragged output
+]
+
+
+@pytest.mark.parametrize("shape", OVERLAP_WALK, ids=lambda s: "x".join(map(str, s)))
+def test_forward_overlap_walk(gpu_lib, shape):
+    """Forward pass through the walking overlap-add inverse against the oracle."""
+    B, C, K, N, n, L, b = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=43 + sum(shape))
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    y = plan.forward(to_dev(x), to_dev(w))
+    torch.cuda.synchronize()
+    e = relerr(y.cpu().numpy(), oracle.conv_forward(x, w))
+    print(f"overlap walk {shape}: rel err fwd {e:.2e}", flush=True)
+    assert e <= TOL, e
+
+
+def test_overlap_save_backward_data_walk(gpu_lib):
+    """Overlap-save error propagation on many planes: the overlap-add of the
+    gradient blocks walks groups of block rows, with one output block row more
+    than tile rows (To = T + 1), the last group holding that row alone."""
+    B, C, K, N, n = 1, 1030, 2, 100, 5
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=47)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(16, 0), method=binding.METHOD_OVERLAP_SAVE)
+    dx = plan.backward_data(to_dev(g), to_dev(w))
+    torch.cuda.synchronize()
+    e = relerr(dx.cpu().numpy(), oracle.conv_backward_data(g, w, N))
+    print(f"overlap-save backward data walk: rel err {e:.2e}", flush=True)
+    assert e <= TOL, e
+
+
 FFTCONV = [  # (B, C, K, N, n, L): one block per plane, L >= N + n - 1 (the paper's FFTconv)
     (1, 3, 4, 32, 5, 64),
     (2, 2, 3, 13, 4, 16),

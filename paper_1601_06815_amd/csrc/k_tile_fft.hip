@@ -488,7 +488,7 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
   // the loads of the next step's rows are issued first and written to LDS
   // after the lane's first column transform, before its first spectrum
   // store; those stores then drain during the next row pass.
-  RowsPrefetch<PF ? kWindowPrefetch : 1> pf;
+  RowsPrefetch<PF ? window_prefetch<L>() : 1> pf;
   constexpr bool use_pf = PF;
   stage_rows32(rows, Wp, src, H, pb * n - p.off, col0, min(RW, pe - pb) * n - n + SW, W);
   __syncthreads();
@@ -831,9 +831,9 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     const int tasks = std::max(na / 2 * p.TQ, HB * rw * p.TQ);
     const int nthr = pick_threads(tasks);
     // register prefetch when a workgroup runs more than one step and the rows
-    // and column tasks fit the lanes; at L = 16 the prefetching variant's
-    // registers (about 190 against 76) cost more occupancy than it gains
-    p.PF = OAA_WINDOW_PREFETCH && L >= 32 && p.SPW > rw && staged <= long(kWindowPrefetch) * nthr && HB * rw * p.TQ <= nthr ? 1 : 0;
+    // and column tasks fit the lanes (at L = 16 with 20 values per lane:
+    // 127 registers, four waves per SIMD; 32 values took about 190)
+    p.PF = OAA_WINDOW_PREFETCH && L >= 16 && p.SPW > rw && staged <= long(window_prefetch<L>()) * nthr && HB * rw * p.TQ <= nthr ? 1 : 0;
     auto kern = p.S == ROWS ? (p.PF ? window_rows_rfft2_kernel<L, ZH, true, true> : window_rows_rfft2_kernel<L, ZH, true, false>)
                             : (p.PF ? window_rows_rfft2_kernel<L, ZH, false, true> : window_rows_rfft2_kernel<L, ZH, false, false>);
     const hipError_t e = allow_lds(kern, kLdsRowsBudget);

@@ -77,6 +77,8 @@ constexpr size_t kLdsBudget = 60 * 1024;
 constexpr size_t kLdsRowsBudget = 80 * 1024;
 // registers per lane for the next step's rows in those kernels
 constexpr int kWindowPrefetch = 32;
+template <int L>
+constexpr int window_prefetch() { return L <= 16 ? 20 : kWindowPrefetch; }
 
 // Lets a kernel take up to `bytes` of dynamic LDS (beyond 64 KB) on the
 // current device; set once per device.

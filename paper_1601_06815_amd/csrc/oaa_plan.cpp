@@ -28,12 +28,13 @@
 
 
 // Weight-gradient split: enough partial products that the tiled contraction
-// has about this many tiles, three rounds of its 512 resident workgroups.
-// More partial sums balance the rounds better but cost the inverse one more
-// read of the whole weight-gradient spectrum each (overridable at build time
-// for tuning sweeps).
+// has at least this many tiles, a little over two rounds of its 512 resident
+// workgroups. More partial sums balance the rounds better but cost the
+// inverse one more read of the whole weight-gradient spectrum each: measured,
+// 1152 gives the large layer 2 partial sums (1 was slower) and the 56 x 56
+// layer 8 (11 cost 0.03 ms more; overridable at build time for sweeps).
 #ifndef OAA_SPLIT_TILES
-#define OAA_SPLIT_TILES 1536
+#define OAA_SPLIT_TILES 1152
 #endif
 
 struct oaa_plan_s {

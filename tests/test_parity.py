@@ -207,6 +207,25 @@ def test_overlap_save_backward_data_walk(gpu_lib):
     assert e <= TOL, e
 
 
+WIDE = [  # (B, C, K, N, n, tiling): planes wider than one workgroup's run of tiles, so every
+    # transform splits a block row into chunks and the walking kernels take many steps
+    (1, 2, 3, 1024, 3, "paper"),     # L = 8, b = 3: T = 342
+    (1, 2, 3, 1024, 3, "auto"),
+    (1, 3, 2, 700, 16, "auto"),      # L = 32: T = 44
+    (1, 2, 2, 900, 9, (32, 24)),     # blocks over L/2 on a wide plane
+    (2, 1, 2, 400, 32, "paper"),     # the largest kernel side (L = 64)
+]
+
+
+@pytest.mark.parametrize("shape", WIDE, ids=lambda s: "x".join(map(str, s)))
+def test_wide_planes_all_passes(gpu_lib, shape):
+    """Maximum plane sizes of the transform kernels' launch shapes: all three
+    passes compared whole against the oracle."""
+    B, C, K, N, n, tiling = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=61 + B + C + K + N + n)
+    check_whole(x, w, g, tiling=tiling)
+
+
 FFTCONV = [  # (B, C, K, N, n, L): one block per plane, L >= N + n - 1 (the paper's FFTconv)
     (1, 3, 4, 32, 5, 64),
     (2, 2, 3, 13, 4, 16),

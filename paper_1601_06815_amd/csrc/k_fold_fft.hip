@@ -740,7 +740,7 @@ hipError_t launch_fold_crop_L(FoldCropParams p, hipStream_t s) {
   const long planes = long(p.n_img) * p.n_ch;
   // Runs of whole block rows for L = 16 and 32 (at L <= 8 the transforms are
   // too short to repay the packed columns), with 32-bit lane offsets.
-  if (L >= 16 && L <= 32 && OAA_FOLD_RUNS && 2 * p.n <= L && size_t(p.M) * p.M * 4 < (size_t(1) << 32) &&
+  if constexpr (L >= 16 && L <= 32) if (OAA_FOLD_RUNS && 2 * p.n <= L && size_t(p.M) * p.M * 4 < (size_t(1) << 32) &&
       size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32)) {
     // whole block rows, RB of them per workgroup: runs of at least 16 tiles
     // where the lanes allow, every column task on a lane of its own
@@ -788,7 +788,7 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
   const long planes = long(p.n_img) * p.n_ch;
   // a workgroup per plane, RB block rows per step: runs of at least 16 tiles
   // where LDS allows (L >= 4: below, the rows are too short to matter)
-  if (L >= 4 && L <= 32 && OAA_OVERLAP_ROWS && p.To <= p.T + 1 && size_t(p.M) * p.M * 4 < (size_t(1) << 32) &&
+  if constexpr (L >= 4 && L <= 32) if (OAA_OVERLAP_ROWS && p.To <= p.T + 1 && size_t(p.M) * p.M * 4 < (size_t(1) << 32) &&
       size_t(V) * size_t(p.n_ch) * p.n_img * p.T * p.T * 8 < (size_t(1) << 32) && long(p.To) * b < 65536) {
     const size_t tsz = size_t(odd_at_least(S * V)) * 8;
     const size_t cbytes = size_t(2) * na * p.To * b * 4;

@@ -801,7 +801,7 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   const long planes = long(p.n_img) * p.n_ch;
   // 32-bit lane offsets: within a plane, and within one row u of the bins
   const size_t fstride = size_t(p.n_ch) * p.n_img * p.T * p.T;
-  if (L <= 32 && OAA_WINDOW_ROWS && size_t(p.H) * p.H * 4 < (size_t(1) << 31) &&
+  if constexpr (L <= 32) if (OAA_WINDOW_ROWS && size_t(p.H) * p.H * 4 < (size_t(1) << 31) &&
       size_t(V) * fstride * 8 < (size_t(1) << 32)) {
     // whole rows of windows per workgroup, rw of them per step so that a
     // step's windows make runs of at least 16 tiles, within the LDS limit

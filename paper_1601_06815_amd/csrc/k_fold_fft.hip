@@ -795,10 +795,11 @@ hipError_t launch_overlap_crop_L(FoldCropParams p, hipStream_t s) {
     auto lds_for = [&](int rb) { return size_t(rb) * p.T * tsz + cbytes; };
     int rb = std::min(std::max(1, (16 + p.T - 1) / p.T), p.To);
     while (rb > 1 && lds_for(rb) > kLdsBudget) --rb;
-    // measured: faster with several block rows per step, or at L <= 16 with
-    // enough planes to fill the GPU; one L = 32 row per step is slower than
-    // the per-block-row kernel, which keeps more workgroups in flight
-    if ((rb >= 2 || (L <= 16 && planes >= 1024)) && lds_for(rb) <= kLdsBudget && long(rb) * b < 65536) {
+    // measured: faster on enough planes to fill the GPU, with several block
+    // rows per step or at L <= 16; one L = 32 row per step, or a few hundred
+    // planes (the paper's single-image sweeps), run faster through the
+    // per-block-row kernel, which keeps more workgroups in flight
+    if (planes >= 1024 && (rb >= 2 || L <= 16) && lds_for(rb) <= kLdsBudget && long(rb) * b < 65536) {
       p.RB = rb;
       // groups of block rows so that there are about OAA_OVERLAP_MIN_WG
       // workgroups (one tile row more is inverted per group)

@@ -169,13 +169,13 @@ def test_forward_block_row_runs(gpu_lib, shape):
     assert e <= TOL, e
 
 
-OVERLAP_WALK = [  # (B, C, K, N, n, L, b), 2b > L: the forward inverse walks down groups of
-    # block rows (several per step, or one at L <= 16 on many planes), each group after the
-    # first starting from the tile row above it
+OVERLAP_WALK = [  # (B, C, K, N, n, L, b), 2b > L, at least 1024 planes: the forward inverse
+    # walks down groups of block rows (several per step, or one at L <= 16), each group after
+    # the first starting from the tile row above it
     (1, 2, 1200, 60, 5, 16, 12),   # T = 5: four block rows per step, groups of 4 and 1
     (1, 2, 1100, 72, 7, 16, 10),   # T = 8: two per step, four groups of one step each
     (2, 1, 600, 100, 3, 8, 6),     # T = 17 at L = 8: one per step, four groups
-    (1, 3, 40, 70, 9, 32, 20),     # L = 32, T = 4: three per step (LDS), groups of 3 and 1
+    (1, 3, 1100, 44, 9, 32, 20),   # L = 32, T = 3: the whole plane in one step
     (1, 1, 1030, 47, 4, 16, 11),   # T = 5, ragged output
 ]
 

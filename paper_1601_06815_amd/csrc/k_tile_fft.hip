@@ -873,11 +873,12 @@ hipError_t launch_crop_LF(CropParams p, hipStream_t s) {
   // column transforms, output block and three tile descriptors per tile
   const size_t per_tile = size_t(TS) * 8 + size_t(p.n) * (p.n | 1) * 4 + 3 * 4;
   const long tiles = long(p.n_img) * p.T * p.T;
-  // runs of consecutive tiles (128-byte reads) as LDS allows, shortened to
-  // keep about 2048 workgroups when there are few tiles (the weight gradient).
-  // For L <= 16 a shorter run is faster: the smaller workgroups leave room
-  // for more of them per CU (measured at both L = 16 layers).
-  long tq = std::min<long>(long(kLdsBudget / per_tile), L <= 16 ? OAA_CROP_TQ_SMALL : OAA_CROP_TQ_MAX);
+  // runs of consecutive tiles (128-byte reads) within OAA_CROP_LDS bytes of
+  // LDS, so that several workgroups share a CU (fewer, longer runs measured
+  // slower), shortened to keep about 2048 workgroups when there are few tiles
+  // (the weight gradient)
+  long tq = std::min<long>(long(std::min<size_t>(kLdsBudget, OAA_CROP_LDS) / per_tile), OAA_CROP_TQ_MAX);
+  if (tq < 1) tq = 1;
   const long want = (long(p.n_ch) * tiles + 2047) / 2048;
   if (want < tq) tq = std::max<long>(want, 1);
   if (tq > tiles) tq = tiles;

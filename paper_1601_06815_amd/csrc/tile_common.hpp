@@ -45,8 +45,9 @@
 #ifndef OAA_CROP_TQ_MAX
 #define OAA_CROP_TQ_MAX 64
 #endif
-#ifndef OAA_CROP_TQ_SMALL
-#define OAA_CROP_TQ_SMALL 16
+// LDS per workgroup of the inverse with crop (40 KB: four per CU)
+#ifndef OAA_CROP_LDS
+#define OAA_CROP_LDS 40960
 #endif
 
 // Minimum waves per SIMD asked of the register allocator, per transform

@@ -418,11 +418,15 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
 //
 // FULL: the window side is exactly L (L/2 under ZH), so no window entry
 // needs masking. PF: the next step's rows are prefetched into registers
-// (only worth its registers when a workgroup runs several steps).
+// (only worth its registers when a workgroup runs several steps). DIRECT:
+// the row transforms read the plane straight from memory instead of from
+// staged rows (for workgroups of a single step, whose LDS then holds only
+// zbuf, so more of them share a CU).
 //
-// LDS: rows [NA][Wp] floats (staged framed rows), then zbuf [TQ][TS] float2,
-// NA = (RW - 1) n + S_MAX rounded up to even, TS >= NA L/2 odd.
-template <int L, bool ZH, bool FULL, bool PF>
+// LDS: rows [NA][Wp] floats (staged framed rows; none under DIRECT), then
+// zbuf [TQ][TS] float2, NA = (RW - 1) n + S_MAX rounded up to even,
+// TS >= NA L/2 odd.
+template <int L, bool ZH, bool FULL, bool PF, bool DIRECT>
 __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(WindowParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int HB = L / 2;                 // packed slots per transformed row
@@ -443,25 +447,41 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
   const int W = (nq - 1) * n + SW;                  // staged columns
   const int Wp = bank_stride((p.TQ - 1) * n + L);  // row reads stay inside the row
   float* rows = smem;                                                                // [NA][Wp]
-  float2* zbuf = reinterpret_cast<float2*>(smem + even_floats(size_t(NA) * Wp));  // [TQ][TS]
+  float2* zbuf = reinterpret_cast<float2*>(smem + (DIRECT ? 0 : even_floats(size_t(NA) * Wp)));  // [TQ][TS]
   const float* src = p.src + size_t(plane) * H * H;
   const size_t tiles_per_ch = size_t(p.n_img) * T * T;
   const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
   float2* out_base = p.dst + size_t(ch) * tiles_per_ch + size_t(img) * T * T + q0;
   const int col0 = q0 * n - p.off;
 
-  // pass 1 of the step at window row P0: framed rows two at a time
-  auto row_pass = [&](int NR) {
+  // pass 1 of the step whose first framed row is plane row `prow0`: framed
+  // rows two at a time
+  auto row_pass = [&](int NR, int prow0) {
     for (int task = tid; task < ((NR + 1) / 2) * nq; task += nthr) {
       const int q = task % nq, r0 = 2 * (task / nq);
       const bool has_b = r0 + 1 < NR;
       const float* row_a = rows + r0 * Wp + q * n;
       const float* row_b = row_a + Wp;
+      // DIRECT: plane rows prow0 + r0 and the next, columns col0 + q n + s,
+      // through a buffer resource over the plane (elements outside it,
+      // offset kOutOfRange, read as zero)
+      const int ga = prow0 + r0, gc = col0 + q * n;
+      const __amdgpu_buffer_rsrc_t rs = buffer_resource(src, unsigned(H) * unsigned(H) * 4u);  // (unused unless DIRECT)
       float zr[L], zi[L];
 #pragma unroll
       for (int s = 0; s < L; ++s) {
         if (s < S_MAX) {
-          const float x0 = row_a[s], x1 = row_b[s];
+          float x0, x1;
+          if (DIRECT) {
+            const bool cok = unsigned(gc + s) < unsigned(H) && (FULL || s < SW);
+            const bool aok = cok && unsigned(ga) < unsigned(H);
+            const bool bok = cok && has_b && unsigned(ga + 1) < unsigned(H);
+            x0 = buffer_load_f1(rs, aok ? unsigned(ga * H + gc + s) * 4u : kOutOfRange);
+            x1 = buffer_load_f1(rs, bok ? unsigned((ga + 1) * H + gc + s) * 4u : kOutOfRange);
+          } else {
+            x0 = row_a[s];
+            x1 = row_b[s];
+          }
           const bool in = FULL || s < SW;
           zr[s] = in ? x0 : 0.f;
           zi[s] = in && has_b ? x1 : 0.f;
@@ -490,9 +510,11 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
   // store; those stores then drain during the next row pass.
   RowsPrefetch<PF ? window_prefetch<L>() : 1> pf;
   constexpr bool use_pf = PF;
-  stage_rows32(rows, Wp, src, H, pb * n - p.off, col0, min(RW, pe - pb) * n - n + SW, W);
-  __syncthreads();
-  row_pass(min(RW, pe - pb) * n - n + SW);
+  if (!DIRECT) {
+    stage_rows32(rows, Wp, src, H, pb * n - p.off, col0, min(RW, pe - pb) * n - n + SW, W);
+    __syncthreads();
+  }
+  row_pass(min(RW, pe - pb) * n - n + SW, pb * n - p.off);
   __syncthreads();
   for (int P0 = pb; P0 < pe; P0 += RW) {
     const int rw = min(RW, pe - P0);
@@ -562,11 +584,11 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
     }
     if (!next) break;
     __syncthreads();  // rows of the next step staged; zbuf free
-    if (!use_pf) {
+    if (!use_pf && !DIRECT) {
       stage_rows32(rows, Wp, src, H, (P0 + RW) * n - p.off, col0, nNR, W);
       __syncthreads();
     }
-    row_pass(nNR);
+    row_pass(nNR, (P0 + RW) * n - p.off);
     __syncthreads();
   }
 }
@@ -834,12 +856,21 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     // and column tasks fit the lanes (at L = 16 with 20 values per lane:
     // 127 registers, four waves per SIMD; 32 values took about 190)
     p.PF = OAA_WINDOW_PREFETCH && L >= 16 && p.SPW > rw && staged <= long(window_prefetch<L>()) * nthr && HB * rw * p.TQ <= nthr ? 1 : 0;
-    auto kern = p.S == ROWS ? (p.PF ? window_rows_rfft2_kernel<L, ZH, true, true> : window_rows_rfft2_kernel<L, ZH, true, false>)
-                            : (p.PF ? window_rows_rfft2_kernel<L, ZH, false, true> : window_rows_rfft2_kernel<L, ZH, false, false>);
+    // one step per workgroup: the row transforms read the plane directly,
+    // and the workgroup's LDS is zbuf alone
+    const bool direct = OAA_WINDOW_DIRECT && p.nchunk == 1 && p.SPW == rw && !p.PF;
+    const bool full = p.S == ROWS;
+    auto kern = direct ? (full ? window_rows_rfft2_kernel<L, ZH, true, false, true>
+                               : window_rows_rfft2_kernel<L, ZH, false, false, true>)
+                : full ? (p.PF ? window_rows_rfft2_kernel<L, ZH, true, true, false>
+                               : window_rows_rfft2_kernel<L, ZH, true, false, false>)
+                       : (p.PF ? window_rows_rfft2_kernel<L, ZH, false, true, false>
+                               : window_rows_rfft2_kernel<L, ZH, false, false, false>);
     const hipError_t e = allow_lds(kern, kLdsRowsBudget);
     if (e != hipSuccess) return e;
+    const size_t zbytes = size_t(odd_at_least(na * HB)) * p.TQ * 8;
     const long nwg = planes * p.ngroups * p.nchunk;
-    hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(nthr), lds, s, p);
+    hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(nthr), direct ? zbytes : lds, s, p);
     return hipGetLastError();
   }
   const int TS = odd_at_least(2 * PAIRS * V);

@@ -21,6 +21,9 @@
 #ifndef OAA_WINDOW_PREFETCH
 #define OAA_WINDOW_PREFETCH 1
 #endif
+#ifndef OAA_WINDOW_DIRECT
+#define OAA_WINDOW_DIRECT 1
+#endif
 #ifndef OAA_FOLD_RUNS
 #define OAA_FOLD_RUNS 1
 #endif

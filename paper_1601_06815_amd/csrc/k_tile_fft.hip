@@ -401,12 +401,17 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
 //
 // Windows of neighbouring window rows share S - n framed rows, and the row
 // transform of a framed row is the same for every window containing it. A
-// step stages the (rw - 1) n + S framed rows of rw window rows once,
-// transforms each of them once per window column, then runs the column
-// transforms of all rw x nq windows. When a workgroup holds whole rows of T
-// windows, the rw T windows of a step are consecutive tiles, and each
-// spectrum bin is written as one run of rw T complex values (the launcher
-// picks rw for runs of at least 16, 128 bytes).
+// step transforms the (rw - 1) n + S framed rows of rw window rows once per
+// window column, then runs the column transforms of all rw x nq windows.
+// When a workgroup holds whole rows of T windows, the rw T windows of a step
+// are consecutive tiles, and each spectrum bin is written as one run of rw T
+// complex values (the launcher picks rw for runs of at least 16, 128 bytes).
+//
+// The row transforms read the plane from memory through a buffer resource
+// over it (elements outside the plane read as zero, so the framing and the
+// zero padding cost no branches); LDS holds only the transformed rows, and
+// more workgroups share a CU. (Staging the rows in LDS first, with the next
+// step's rows prefetched into registers, measured slower.)
 //
 // Transformed rows are stored packed, L/2 complex slots per row: slot 0 holds
 // the two real bins v = 0 and v = L/2 as (re, im), slots 1 .. L/2-1 the bins
@@ -417,16 +422,11 @@ __global__ void __launch_bounds__(kMaxThreads, fft_waves<L>(OAA_WAVES_WINDOW)) w
 // L values.
 //
 // FULL: the window side is exactly L (L/2 under ZH), so no window entry
-// needs masking. PF: the next step's rows are prefetched into registers
-// (only worth its registers when a workgroup runs several steps). DIRECT:
-// the row transforms read the plane straight from memory instead of from
-// staged rows (for workgroups of a single step, whose LDS then holds only
-// zbuf, so more of them share a CU).
+// needs masking.
 //
-// LDS: rows [NA][Wp] floats (staged framed rows; none under DIRECT), then
-// zbuf [TQ][TS] float2, NA = (RW - 1) n + S_MAX rounded up to even,
-// TS >= NA L/2 odd.
-template <int L, bool ZH, bool FULL, bool PF, bool DIRECT>
+// LDS: zbuf [TQ][TS] float2, TS >= NA L/2 odd, NA = (RW - 1) n + S_MAX
+// rounded up to even.
+template <int L, bool ZH, bool FULL>
 __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(WindowParams p) {
   constexpr int V = L / 2 + 1;
   constexpr int HB = L / 2;                 // packed slots per transformed row
@@ -444,47 +444,32 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
   const int img = int(plane / p.n_ch), ch = int(plane % p.n_ch);
   const int q0 = chunk * p.TQ, nq = min(p.TQ, T - q0);
   const int pb = grp * p.SPW, pe = min(T, pb + p.SPW);
-  const int W = (nq - 1) * n + SW;                  // staged columns
-  const int Wp = bank_stride((p.TQ - 1) * n + L);  // row reads stay inside the row
-  float* rows = smem;                                                                // [NA][Wp]
-  float2* zbuf = reinterpret_cast<float2*>(smem + (DIRECT ? 0 : even_floats(size_t(NA) * Wp)));  // [TQ][TS]
+  float2* zbuf = reinterpret_cast<float2*>(smem);  // [TQ][TS]
   const float* src = p.src + size_t(plane) * H * H;
+  const __amdgpu_buffer_rsrc_t rs = buffer_resource(src, unsigned(H) * unsigned(H) * 4u);
   const size_t tiles_per_ch = size_t(p.n_img) * T * T;
   const size_t fstride = size_t(p.n_ch) * tiles_per_ch;
   float2* out_base = p.dst + size_t(ch) * tiles_per_ch + size_t(img) * T * T + q0;
   const int col0 = q0 * n - p.off;
 
-  // pass 1 of the step whose first framed row is plane row `prow0`: framed
-  // rows two at a time
-  auto row_pass = [&](int NR, int prow0) {
+  for (int P0 = pb; P0 < pe; P0 += RW) {
+    const int rw = min(RW, pe - P0);
+    // pass 1: the step's framed rows two at a time, plane rows prow0 + r0
+    // and prow0 + r0 + 1, columns col0 + q n + s
+    const int NR = (rw - 1) * n + SW, prow0 = P0 * n - p.off;
     for (int task = tid; task < ((NR + 1) / 2) * nq; task += nthr) {
       const int q = task % nq, r0 = 2 * (task / nq);
       const bool has_b = r0 + 1 < NR;
-      const float* row_a = rows + r0 * Wp + q * n;
-      const float* row_b = row_a + Wp;
-      // DIRECT: plane rows prow0 + r0 and the next, columns col0 + q n + s,
-      // through a buffer resource over the plane (elements outside it,
-      // offset kOutOfRange, read as zero)
       const int ga = prow0 + r0, gc = col0 + q * n;
-      const __amdgpu_buffer_rsrc_t rs = buffer_resource(src, unsigned(H) * unsigned(H) * 4u);  // (unused unless DIRECT)
       float zr[L], zi[L];
 #pragma unroll
       for (int s = 0; s < L; ++s) {
         if (s < S_MAX) {
-          float x0, x1;
-          if (DIRECT) {
-            const bool cok = unsigned(gc + s) < unsigned(H) && (FULL || s < SW);
-            const bool aok = cok && unsigned(ga) < unsigned(H);
-            const bool bok = cok && has_b && unsigned(ga + 1) < unsigned(H);
-            x0 = buffer_load_f1(rs, aok ? unsigned(ga * H + gc + s) * 4u : kOutOfRange);
-            x1 = buffer_load_f1(rs, bok ? unsigned((ga + 1) * H + gc + s) * 4u : kOutOfRange);
-          } else {
-            x0 = row_a[s];
-            x1 = row_b[s];
-          }
-          const bool in = FULL || s < SW;
-          zr[s] = in ? x0 : 0.f;
-          zi[s] = in && has_b ? x1 : 0.f;
+          const bool cok = unsigned(gc + s) < unsigned(H) && (FULL || s < SW);
+          const bool aok = cok && unsigned(ga) < unsigned(H);
+          const bool bok = cok && has_b && unsigned(ga + 1) < unsigned(H);
+          zr[s] = buffer_load_f1(rs, aok ? unsigned(ga * H + gc + s) * 4u : kOutOfRange);
+          zi[s] = buffer_load_f1(rs, bok ? unsigned((ga + 1) * H + gc + s) * 4u : kOutOfRange);
         } else {
           zr[s] = 0.f;
           zi[s] = 0.f;
@@ -501,32 +486,11 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
         zt[HB + k] = X1[k];
       }
     }
-  };
-
-  // Order of a step, chosen for gfx9's single counter of outstanding vector
-  // memory operations (a wait for loads also waits for every earlier store):
-  // the loads of the next step's rows are issued first and written to LDS
-  // after the lane's first column transform, before its first spectrum
-  // store; those stores then drain during the next row pass.
-  RowsPrefetch<PF ? window_prefetch<L>() : 1> pf;
-  constexpr bool use_pf = PF;
-  if (!DIRECT) {
-    stage_rows32(rows, Wp, src, H, pb * n - p.off, col0, min(RW, pe - pb) * n - n + SW, W);
     __syncthreads();
-  }
-  row_pass(min(RW, pe - pb) * n - n + SW, pb * n - p.off);
-  __syncthreads();
-  for (int P0 = pb; P0 < pe; P0 += RW) {
-    const int rw = min(RW, pe - P0);
-    const bool next = P0 + RW < pe;
-    const int nNR = next ? (min(RW, pe - P0 - RW) - 1) * n + SW : 0;
-    if (next && use_pf) pf.load(src, H, (P0 + RW) * n - p.off, col0, nNR, W);
     // pass 2: column transforms of the rw x nq windows; lanes run over the
     // window columns, then the window rows, so that a store instruction
-    // covers consecutive tiles of one bin. With prefetch, every lane has at
-    // most one column task (launcher), and writes the next rows to LDS
-    // between its transform and its stores.
-    auto column_task = [&](int task, bool stage_next) {
+    // covers consecutive tiles of one bin
+    for (int task = tid; task < HB * rw * nq; task += nthr) {
       const int q = task % nq, r2 = task / nq;
       const int w = r2 % rw, k = r2 / rw;
       const float2* zt = zbuf + q * TS + (w * n) * HB + k;
@@ -544,7 +508,6 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
         }
       }
       fft_dif<L, -1, ZH>(re, im);
-      if (stage_next) pf.store(rows, Wp, nNR, W);
       // bin (u, v) of this window at obase + u V fstride (wave-uniform) plus
       // the lane's byte offset (v fstride + w T + q) * 8, below V fstride * 8
       // < 2^32 (checked by the launcher)
@@ -572,24 +535,8 @@ __global__ void __launch_bounds__(kMaxThreads, 2) window_rows_rfft2_kernel(Windo
           advance_uniform(bu, size_t(V) * fstride);
         }
       }
-    };
-    const int ntask = HB * rw * nq;
-    if (next && use_pf) {
-      if (tid < ntask)
-        column_task(tid, true);
-      else
-        pf.store(rows, Wp, nNR, W);
-    } else {
-      for (int task = tid; task < ntask; task += nthr) column_task(task, false);
     }
-    if (!next) break;
-    __syncthreads();  // rows of the next step staged; zbuf free
-    if (!use_pf && !DIRECT) {
-      stage_rows32(rows, Wp, src, H, (P0 + RW) * n - p.off, col0, nNR, W);
-      __syncthreads();
-    }
-    row_pass(nNR, (P0 + RW) * n - p.off);
-    __syncthreads();
+    __syncthreads();  // zbuf free for the next step
   }
 }
 
@@ -829,9 +776,8 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     // step's windows make runs of at least 16 tiles, within the LDS limit
     constexpr int HB = L / 2;
     auto lds_rows = [&](int tq, int rw) {
-      const size_t na = size_t(((rw - 1) * p.n + ROWS + 1) & ~1);
-      const size_t wp = size_t(bank_stride((tq - 1) * p.n + L));
-      return even_floats(na * wp) * 4 + size_t(odd_at_least(int(na) * HB)) * tq * 8;
+      const int na = ((rw - 1) * p.n + ROWS + 1) & ~1;
+      return size_t(odd_at_least(na * HB)) * tq * 8;
     };
     int nchunk = (p.T + OAA_WINDOW_TQ_MAX - 1) / OAA_WINDOW_TQ_MAX;
     while (nchunk < p.T && lds_rows((p.T + nchunk - 1) / nchunk, 1) > kLdsRowsBudget) ++nchunk;
@@ -841,8 +787,6 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     if (p.nchunk == 1)
       while (rw * p.T < OAA_WINDOW_MIN_RUN && rw < p.T && lds_rows(p.TQ, rw + 1) <= kLdsRowsBudget) ++rw;
     p.RW = rw;
-    // the next step's (rw - 1) n + S rows of (TQ - 1) n + S columns in registers
-    const long staged = long((rw - 1) * p.n + p.S) * long((p.TQ - 1) * p.n + p.S);
     const size_t lds = lds_rows(p.TQ, rw);
     if (lds > kLdsRowsBudget) return hipErrorInvalidConfiguration;
     int ng = 1;
@@ -850,27 +794,12 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     p.SPW = ((p.T + ng - 1) / ng + rw - 1) / rw * rw;
     p.ngroups = (p.T + p.SPW - 1) / p.SPW;
     const int na = ((rw - 1) * p.n + ROWS + 1) & ~1;
-    const int tasks = std::max(na / 2 * p.TQ, HB * rw * p.TQ);
-    const int nthr = pick_threads(tasks);
-    // register prefetch when a workgroup runs more than one step and the rows
-    // and column tasks fit the lanes (at L = 16 with 20 values per lane:
-    // 127 registers, four waves per SIMD; 32 values took about 190)
-    p.PF = OAA_WINDOW_PREFETCH && L >= 16 && p.SPW > rw && staged <= long(window_prefetch<L>()) * nthr && HB * rw * p.TQ <= nthr ? 1 : 0;
-    // one step per workgroup: the row transforms read the plane directly,
-    // and the workgroup's LDS is zbuf alone
-    const bool direct = OAA_WINDOW_DIRECT && p.nchunk == 1 && p.SPW == rw && !p.PF;
-    const bool full = p.S == ROWS;
-    auto kern = direct ? (full ? window_rows_rfft2_kernel<L, ZH, true, false, true>
-                               : window_rows_rfft2_kernel<L, ZH, false, false, true>)
-                : full ? (p.PF ? window_rows_rfft2_kernel<L, ZH, true, true, false>
-                               : window_rows_rfft2_kernel<L, ZH, true, false, false>)
-                       : (p.PF ? window_rows_rfft2_kernel<L, ZH, false, true, false>
-                               : window_rows_rfft2_kernel<L, ZH, false, false, false>);
+    const int nthr = pick_threads(std::max(na / 2 * p.TQ, HB * rw * p.TQ));
+    auto kern = p.S == ROWS ? window_rows_rfft2_kernel<L, ZH, true> : window_rows_rfft2_kernel<L, ZH, false>;
     const hipError_t e = allow_lds(kern, kLdsRowsBudget);
     if (e != hipSuccess) return e;
-    const size_t zbytes = size_t(odd_at_least(na * HB)) * p.TQ * 8;
     const long nwg = planes * p.ngroups * p.nchunk;
-    hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(nthr), direct ? zbytes : lds, s, p);
+    hipLaunchKernelGGL(kern, dim3(unsigned(nwg)), dim3(nthr), lds, s, p);
     return hipGetLastError();
   }
   const int TS = odd_at_least(2 * PAIRS * V);
@@ -883,7 +812,6 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
   p.TQ = (p.T + nchunk - 1) / nchunk;
   p.nchunk = (p.T + p.TQ - 1) / p.TQ;
   p.RW = 1;
-  p.PF = 0;
   const size_t lds = lds_for(p.TQ);
   if (lds > kLdsBudget) return hipErrorInvalidConfiguration;
   int ng = 1;

@@ -57,7 +57,6 @@ struct WindowParams {
   int TQ, nchunk;    // window columns per workgroup, ceil(T / TQ)
   int SPW, ngroups;  // window rows per workgroup, ceil(T / SPW)
   int RW;            // window rows transformed together (set by the launcher)
-  int PF;            // 1: the next rows are loaded into registers (launcher)
 };
 
 // Forward output through folded tile spectra: output block (P, Q) covers

@@ -21,9 +21,6 @@
 #ifndef OAA_WINDOW_PREFETCH
 #define OAA_WINDOW_PREFETCH 1
 #endif
-#ifndef OAA_WINDOW_DIRECT
-#define OAA_WINDOW_DIRECT 1
-#endif
 #ifndef OAA_FOLD_RUNS
 #define OAA_FOLD_RUNS 1
 #endif
@@ -76,14 +73,9 @@ constexpr int fft_waves(int want) { return L <= 32 ? want : 1; }
 
 constexpr int kMaxThreads = 256;
 constexpr size_t kLdsBudget = 60 * 1024;
-// LDS of the kernels that transform several window rows per step: two
-// workgroups per CU
+// LDS of the kernels that transform several window rows per step (at most:
+// two workgroups per CU)
 constexpr size_t kLdsRowsBudget = 80 * 1024;
-// registers per lane for the next step's rows in those kernels
-constexpr int kWindowPrefetch = 32;
-template <int L>
-constexpr int window_prefetch() { return L <= 16 ? 20 : kWindowPrefetch; }
-
 // Lets a kernel take up to `bytes` of dynamic LDS (beyond 64 KB) on the
 // current device; set once per device.
 template <class Kern>
@@ -204,86 +196,6 @@ __device__ __forceinline__ void advance_uniform(T*& ptr, size_t step) {
   asm volatile("" : "+s"(lo), "+s"(hi));
   ptr = reinterpret_cast<T*>((static_cast<unsigned long long>(hi) << 32) | lo);
 }
-
-// stage_rows for planes of fewer than 2^30 pixels, with 32-bit offsets from
-// the plane base.
-__device__ __forceinline__ void stage_rows32(float* dst, int Wp, const float* plane, int H, int row0, int col0,
-                                             int R, int W) {
-  const int nthr = blockDim.x, tid = threadIdx.x;
-  const int Wt = W < nthr ? W : nthr;
-  const int rstep = nthr / Wt;
-  const int cl = tid % Wt, rl = tid / Wt;
-  if (rl >= rstep) return;
-  for (int c = cl; c < W; c += Wt) {
-    const int gc = col0 + c;
-    const bool col_ok = gc >= 0 && gc < H;
-    for (int rb = rl; rb < R; rb += kUnroll * rstep) {
-      float v[kUnroll];
-#pragma unroll
-      for (int j = 0; j < kUnroll; ++j) {
-        const int r = rb + j * rstep;
-        const int gr = row0 + r;
-        const bool ok = col_ok && r < R && gr >= 0 && gr < H;
-        const float t = load_at(plane, ok ? unsigned(gr * H + gc) * 4u : 0u);
-        v[j] = ok ? t : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < kUnroll; ++j) {
-        const int r = rb + j * rstep;
-        if (r < R) dst[r * Wp + c] = v[j];
-      }
-    }
-  }
-}
-
-// Register copy of rows [row0, row0 + R) x columns [col0, col0 + W) of an
-// H x H plane (zero outside), for planes of fewer than 2^29 pixels: element e
-// of the block in row-major order is held by lane e % lanes, so the loads are
-// coalesced along rows. Needs R * W <= MAXE * lanes and W <= lanes. Loads go
-// through a buffer resource over the plane: elements outside it read as zero
-// with no per-element mask kept until the data arrives.
-template <int MAXE>
-struct RowsPrefetch {
-  float v[MAXE];
-
-  __device__ __forceinline__ void load(const float* plane, int H, int row0, int col0, int R, int W) {
-    const __amdgpu_buffer_rsrc_t rs = buffer_resource(plane, unsigned(H) * unsigned(H) * 4u);
-    const int nthr = blockDim.x;
-    const int dr = nthr / W, dc = nthr % W;
-    int r = int(threadIdx.x) / W, c = int(threadIdx.x) % W;
-#pragma unroll
-    for (int j = 0; j < MAXE; ++j) {
-      const int gr = row0 + r, gc = col0 + c;
-      const bool ok = r < R && unsigned(gr) < unsigned(H) && unsigned(gc) < unsigned(H);
-      v[j] = buffer_load_f1(rs, ok ? unsigned(gr * H + gc) * 4u : kOutOfRange);
-      r += dr;
-      c += dc;
-      if (c >= W) {
-        c -= W;
-        ++r;
-      }
-    }
-  }
-
-  __device__ __forceinline__ void store(float* dst, int Wp, int R, int W) const {
-    const int nthr = blockDim.x;
-    const int dr = nthr / W, dc = nthr % W;
-    int r = int(threadIdx.x) / W, c = int(threadIdx.x) % W;
-    // recomputed here rather than kept from load(): the empty asm stops the
-    // compiler from holding MAXE addresses in registers in between
-    asm volatile("" : "+v"(r), "+v"(c));
-#pragma unroll
-    for (int j = 0; j < MAXE; ++j) {
-      if (r < R) dst[r * Wp + c] = v[j];
-      r += dr;
-      c += dc;
-      if (c >= W) {
-        c -= W;
-        ++r;
-      }
-    }
-  }
-};
 
 // Register copy of rows [row0, row0+R) x columns [col0, col0+W) of an H x H
 // plane (zero outside), for W <= lanes: lane t holds column t % W of rows

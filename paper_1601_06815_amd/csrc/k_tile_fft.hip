@@ -783,9 +783,20 @@ hipError_t launch_window_L(WindowParams p, hipStream_t s) {
     while (nchunk < p.T && lds_rows((p.T + nchunk - 1) / nchunk, 1) > kLdsRowsBudget) ++nchunk;
     p.TQ = (p.T + nchunk - 1) / nchunk;
     p.nchunk = (p.T + p.TQ - 1) / p.TQ;
+    // window rows per step: the fewest whose run of rw T tiles is a multiple
+    // of 16 (whole 128-byte lines, e.g. two rows of 8), else as many as lengthen
+    // the run towards OAA_WINDOW_MIN_RUN, while the LDS of a workgroup stays
+    // within OAA_WINDOW_GROW_LDS
     int rw = 1;
-    if (p.nchunk == 1)
-      while (rw * p.T < OAA_WINDOW_MIN_RUN && rw < p.T && lds_rows(p.TQ, rw + 1) <= kLdsRowsBudget) ++rw;
+    if (p.nchunk == 1) {
+      int ra = 0;
+      for (int r = 1; r <= p.T && r * p.T <= 64 && !ra; ++r)
+        if ((r * p.T) % 16 == 0) ra = r;
+      if (ra && lds_rows(p.TQ, ra) <= OAA_WINDOW_GROW_LDS)
+        rw = ra;
+      else
+        while (rw * p.T < OAA_WINDOW_MIN_RUN && rw < p.T && lds_rows(p.TQ, rw + 1) <= OAA_WINDOW_GROW_LDS) ++rw;
+    }
     p.RW = rw;
     const size_t lds = lds_rows(p.TQ, rw);
     if (lds > kLdsRowsBudget) return hipErrorInvalidConfiguration;

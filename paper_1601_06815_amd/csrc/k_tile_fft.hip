@@ -7,8 +7,11 @@
 // coalesced loads; pass 1 (one lane per pair of tile rows) transforms rows,
 // pass 2 (one lane per tile column) transforms columns and writes the spectra
 // bin-major with consecutive tiles at consecutive addresses.
-// Gradient windows: one workgroup walks down the block rows of a plane with
-// a ring of 2n input rows in LDS, reading each row of g once.
+// Gradient windows (and input blocks taken as windows of side and pitch b):
+// one workgroup walks down the window rows of a plane, several per step for
+// L <= 32 with the rows read straight from memory (window_rows_rfft2_kernel),
+// one per step with a ring of 2n input rows in LDS for L = 64
+// (window_rfft2_kernel).
 // Inverse with crop (error propagation, weight gradient): the two passes in
 // the opposite order, keeping the top-left n x n of every tile. The forward
 // inverse with overlap-add is in k_fold_fft.hip.

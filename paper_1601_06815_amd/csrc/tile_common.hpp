@@ -17,13 +17,14 @@
 // Consecutive tiles a step of the several-rows window transform aims for
 // where no run of whole 128-byte lines is within reach, and the LDS per
 // workgroup it may grow to for them (measured: runs of 69 tiles at first224
-// cut its gradient windows from 1.17 to 0.92 ms; at large128, runs of 24
-// tiles were slower than the line-aligned runs of 16).
+// cut its gradient windows from 1.17 to 0.92 ms, runs of 28 the overlap-save
+// input windows at large128 from 0.33 to 0.30 ms; at large128's T = 8,
+// runs of 24 tiles were slower than the line-aligned runs of 16).
 #ifndef OAA_WINDOW_MIN_RUN
 #define OAA_WINDOW_MIN_RUN 48
 #endif
 #ifndef OAA_WINDOW_GROW_LDS
-#define OAA_WINDOW_GROW_LDS 65536
+#define OAA_WINDOW_GROW_LDS 81920
 #endif
 #ifndef OAA_WINDOW_PREFETCH
 #define OAA_WINDOW_PREFETCH 1

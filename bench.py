@@ -29,30 +29,37 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
 PROFILE_DIR = os.path.join(ROOT, "profiles")
+PARITY_TOL = 2e-5              # max|err| / max|ref| against the fp64 oracle
 
 
 def stage_work(ly, geo):
-    """Algorithmic bytes (HBM) and flops per launch of each stage."""
+    """Algorithmic bytes (HBM) and flops per launch of each stage.
+
+    Contractions: "flops" is the method's own count, 8 real flops per
+    complex multiply-add over all F = L(L/2+1) stored bins of every tile,
+    8 B P C K F per launch; "flops_exec" is what the matrix-core engine
+    executes, 6 real flops per complex multiply-add (Gauss's three real
+    products) over the unique_bins(L) bins that are not conjugates of
+    others."""
     B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
     F, P, S, L = geo["F"], geo["P"], geo["split"], geo["L"]
     BP = B * P
     cplx = 8
-    # the contractions compute the bins that are not conjugates of others;
-    # the matrix-core engine forms each complex multiply-add from three real
-    # products (Gauss), i.e. 6 real flops, where the textbook count is 8
     Fu = (L // 2 + 1) ** 2 + (L // 2 - 1) ** 2
-    prod_flops = 6.0 * BP * C * K * Fu
+    alg_flops = 8.0 * BP * C * K * F
+    exec_flops = 6.0 * BP * C * K * Fu
     # the transforms' outputs count the same unique bins (the others are
     # conjugates that no later stage reads)
+    prod = dict(flops=alg_flops, flops_exec=exec_flops)
     return {
         "w_spectrum": dict(bytes=K * C * n * n * 4 + Fu * C * K * cplx),
         "x_spectrum": dict(bytes=B * C * N * N * 4 + Fu * C * BP * cplx),
         "g_spectrum": dict(bytes=B * K * M * M * 4 + Fu * K * BP * cplx),
-        "fwd_product": dict(flops=prod_flops, bytes=(Fu * C * K + Fu * C * BP + Fu * K * BP) * cplx),
+        "fwd_product": dict(prod, bytes=(Fu * C * K + Fu * C * BP + Fu * K * BP) * cplx),
         "fwd_inverse": dict(bytes=Fu * K * BP * cplx + B * K * M * M * 4),
-        "bwd_data_product": dict(flops=prod_flops, bytes=(Fu * C * K + Fu * K * BP + Fu * C * BP) * cplx),
+        "bwd_data_product": dict(prod, bytes=(Fu * C * K + Fu * K * BP + Fu * C * BP) * cplx),
         "bwd_data_inverse": dict(bytes=Fu * C * BP * cplx + B * C * N * N * 4),
-        "bwd_filter_product": dict(flops=prod_flops, bytes=(Fu * C * BP + Fu * K * BP + S * Fu * C * K) * cplx),
+        "bwd_filter_product": dict(prod, bytes=(Fu * C * BP + Fu * K * BP + S * Fu * C * K) * cplx),
         "bwd_filter_inverse": dict(bytes=S * Fu * C * K * cplx + K * C * n * n * 4),
     }
 
@@ -88,11 +95,10 @@ def source_digest(fname):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, geo, stage):
-    """HBM bytes per launch from committed rocprofv3 counter runs of the same
-    workload and tiling, or None if absent or taken on a different version of
-    the kernel's source."""
-    path = os.path.join(PROFILE_DIR, "traffic.json")
+def _profile_record(fname, workload, geo, stage):
+    """A committed per-stage counter record (profiles/<fname>), or None if
+    absent or taken on a different version of the kernel's source."""
+    path = os.path.join(PROFILE_DIR, fname)
     if not os.path.exists(path):
         return None
     try:
@@ -101,7 +107,23 @@ def measured_traffic(workload, geo, stage):
         return None
     if not rec or rec.get("source_sha256") != source_digest(kernel_source(geo, stage)):
         return None
-    return rec.get("bytes_per_launch")
+    return rec
+
+
+def measured_traffic(workload, geo, stage):
+    """HBM bytes per launch from committed rocprofv3 counter runs of the same
+    workload and tiling, or None if absent or stale."""
+    rec = _profile_record("traffic.json", workload, geo, stage)
+    return None if rec is None else rec.get("bytes_per_launch")
+
+
+def measured_mfma(workload, geo, stage):
+    """Matrix-core counters of a contraction stage (busy fraction and fp32
+    MFMA flops per launch) from committed rocprofv3 runs, or None."""
+    rec = _profile_record("mfma.json", workload, geo, stage)
+    if rec is None:
+        return None
+    return {k: rec[k] for k in ("mfma_busy", "mfma_f32_flops", "mfma_xf32_flops", "mfma_bf16_flops") if k in rec}
 
 
 def cpu_baseline(ly, x, w, g, budget_s=20.0):
@@ -206,6 +228,62 @@ def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, ste
     with open(path, "w") as f:
         json.dump(db, f, indent=1, sort_keys=True)
         f.write("\n")
+
+
+def summarize_counters(layer, run_dir, steps=2, method="oaa"):
+    """Per-stage values of every counter in a rocprofv3 --pmc run of
+    `bench.py --layer <layer> --method <method> --steps 2 --warmup 1
+    --no-cpu-baseline` (mean over the last `steps` steps). For the
+    contractions, the matrix-core figures (MfmaUtil: busy cycles of the
+    MFMA units over active cycles of all SIMDs; MfmaFlopsF32 and the XF32 /
+    BF16 MFMA op counts) are recorded in profiles/mfma.json."""
+    import csv
+    import glob
+    from paper_1601_06815_amd import binding
+    from paper_1601_06815_amd.workloads import LAYERS
+    ly = LAYERS[layer]
+    m = binding.METHOD_OVERLAP_SAVE if method == "oas" else binding.METHOD_OVERLAP_ADD
+    h = binding.oaa_plan_create_method(ly.B, ly.C, ly.K, ly.N, ly.n, 0, 0, m)
+    geo = binding.oaa_plan_geometry(h)
+    binding.oaa_plan_destroy(h)
+    rows = list(csv.DictReader(open(glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"),
+                                              recursive=True)[0])))
+    names = sorted({r["Counter_Name"] for r in rows})
+    per = {}
+    for r in rows:
+        d = int(r["Dispatch_Id"])
+        k = _short_kernel(r["Kernel_Name"])
+        if not k.startswith(LIB_KERNELS):
+            continue
+        e = per.setdefault(d, {"kernel": k})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    disp = [per[d] for d in sorted(per)]
+    n = len(STAGE_ORDER)
+    disp = disp[-steps * n:]
+    work = stage_work(ly, geo)
+    name = "overlap-save, h" if geo.get("method") else "b"
+    print(f"## {layer}, L={geo['L']} {name}={geo['b']} (mean over the last {steps} steps)")
+    print(f"{'stage':20s} {'kernel':44s} " + " ".join(f"{c[:24]:>24s}" for c in names))
+    path = os.path.join(PROFILE_DIR, "mfma.json")
+    db = json.load(open(path)) if os.path.exists(path) else {}
+    for i, stage in enumerate(STAGE_ORDER):
+        ds = [disp[j * n + i] for j in range(steps)]
+        mean = {c: sum(d.get(c, 0.0) for d in ds) / steps for c in names}
+        print(f"{stage:20s} {ds[0]['kernel'][:44]:44s} " + " ".join(f"{mean[c]:24.4g}" for c in names))
+        if "flops" in work[stage] and "MfmaUtil" in mean:
+            rec = {"kernel": ds[0]["kernel"], "mfma_busy": round(mean["MfmaUtil"] / 100.0, 4),
+                   "source_sha256": source_digest(kernel_source(geo, stage))}
+            if "MfmaFlopsF32" in mean:
+                rec["mfma_f32_flops"] = mean["MfmaFlopsF32"]
+            for c, key in (("SQ_INSTS_VALU_MFMA_MOPS_XF32", "mfma_xf32_flops"),
+                           ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "mfma_bf16_flops")):
+                if c in mean:
+                    rec[key] = mean[c] * 512
+            db[traffic_key(layer, geo, stage)] = rec
+    if any("MfmaUtil" in d for d in disp):
+        with open(path, "w") as f:
+            json.dump(db, f, indent=1, sort_keys=True)
+            f.write("\n")
 
 
 def summarize_stats(run_dir):
@@ -321,13 +399,15 @@ def config_report(args):
                     continue
                 sm = ms / cnt
                 wk = work[sname]
+                frac_exec = None
                 if "flops" in wk and min(ly.C, ly.K) >= 64:
                     frac = wk["flops"] / (sm * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS
+                    frac_exec = wk["flops_exec"] / (sm * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS
                     bound = "mfma"
                 else:
                     frac = wk["bytes"] / (sm * 1e-3) / 1e9 / HBM_PEAK_GBS
                     bound = "hbm"
-                stages[sname] = {"ms": sm, "share": sm / med, "bound": bound, "frac": frac}
+                stages[sname] = {"ms": sm, "share": sm / med, "bound": bound, "frac": frac, "frac_exec": frac_exec}
             cpu_ms, cpu_note = oracle_pass_ms(ly, x, w, g, pas, args.cpu_budget / 4)
             row = {"layer": name, "pass": pas, "L": geo["L"], "b": geo["b"], "ms_median": med, "ms_mean10": mean10,
                    "ms_graph": ms_graph,
@@ -346,6 +426,7 @@ def config_report(args):
         # microseconds are bound by launch latency: no roofline fraction
         small = LAYERS[r["layer"]].direct_flops() < 1e9
         st = "; ".join(f"{k} {v['share'] * 100:.0f} %" + ("" if small else f", {v['frac'] * 100:.0f} % {v['bound']}")
+                       + ("" if small or v.get("frac_exec") is None else f" ({v['frac_exec'] * 100:.0f} % executed)")
                        for k, v in r["stages"].items())
         if small:
             st += " (latency-bound)"
@@ -391,6 +472,9 @@ def main():
                     help="per config and pass: ms, direct-equivalent TFLOP/s, stage shares and roofline fractions, "
                          "oracle host time (a table, not the JSON line)")
     ap.add_argument("--report-out", default=None, help="with --report: also write the rows as JSON here")
+    ap.add_argument("--summarize-counters", metavar="DIR",
+                    help="host only: per-stage counter values of --layer from a rocprofv3 --pmc run "
+                         "(records matrix-core figures in profiles/mfma.json)")
     ap.add_argument("--summarize-stats", metavar="DIR",
                     help="host only: table of a rocprofv3 --kernel-trace --stats run")
     args = ap.parse_args()
@@ -399,6 +483,9 @@ def main():
         return
     if args.summarize_stats:
         summarize_stats(args.summarize_stats)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.layer, args.summarize_counters, method=args.method)
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -495,10 +582,15 @@ def main():
     wk = work[dom]
     if "flops" in wk:
         achieved = wk["flops"] / avg_s / 1e12
+        executed = wk["flops_exec"] / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / FP32_MFMA_PEAK_TFLOPS,
-                "flops_counted": "6 per complex multiply-add (three real MFMA products)",
-                "complex_equiv_tflops": achieved * 8.0 / 6.0}
+                "flops_counted": "8 B P C K F: 8 real flops per complex multiply-add over all L(L/2+1) "
+                                 "stored bins of every tile",
+                "executed": {"achieved": executed, "frac": executed / FP32_MFMA_PEAK_TFLOPS,
+                             "flops_counted": "6 real flops per complex multiply-add (three real matrix-core "
+                                              "products) over the bins that are not conjugates of others"},
+                "counters": measured_mfma(ly.name, geo, dom)}
     else:
         achieved = wk["bytes"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -512,17 +604,24 @@ def main():
         st["gbs_algorithmic"] = wk["bytes"] / s / 1e9
         if "flops" in wk:
             st["tflops"] = wk["flops"] / s / 1e12
+            st["tflops_executed"] = wk["flops_exec"] / s / 1e12
 
     # sampled parity of the timed outputs against the oracle
     import oracle
     rng = np.random.default_rng(0)
-    iy = [rng.integers(0, s, 16) for s in (ly.B, ly.K, ly.M, ly.M)]
-    iw = [rng.integers(0, s, 16) for s in (ly.K, ly.C, ly.n, ly.n)]
-    yh, dwh = y.cpu().numpy(), dw.cpu().numpy()
-    ry = oracle.conv_forward_at(x, w, *iy)
-    rw = oracle.conv_backward_filter_at(x, g, ly.n, *iw)
-    err = max(float(np.max(np.abs(yh[tuple(iy)] - ry)) / np.max(np.abs(ry))),
-              float(np.max(np.abs(dwh[tuple(iw)] - rw)) / np.max(np.abs(rw))))
+    S = 24
+    iy = [rng.integers(0, s, S) for s in (ly.B, ly.K, ly.M, ly.M)]
+    ix = [rng.integers(0, s, S) for s in (ly.B, ly.C, ly.N, ly.N)]
+    iw = [rng.integers(0, s, S) for s in (ly.K, ly.C, ly.n, ly.n)]
+    yh, dxh, dwh = y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
+    errs = {}
+    for key, got, ref in (("y", yh[tuple(iy)], oracle.conv_forward_at(x, w, *iy)),
+                          ("dx", dxh[tuple(ix)], oracle.conv_backward_data_at(g, w, ly.N, *ix)),
+                          ("dw", dwh[tuple(iw)], oracle.conv_backward_filter_at(x, g, ly.n, *iw))):
+        scale = float(np.max(np.abs(ref)))
+        diff = float(np.max(np.abs(got - ref)))
+        errs[key] = diff / scale if scale > 0 else diff
+    err = max(errs.values())
 
     out = {
         "metric": "OaA conv fwd+bwd ms & direct-equiv TFLOP/s; % of HBM BW / MFMA peak",
@@ -547,6 +646,7 @@ def main():
         "graph_ms_per_step": ms_graph,
         "stages": per_stage,
         "sampled_rel_err": err,
+        "sampled_rel_err_by_output": errs,
     }
     if args.stages_out:
         with open(args.stages_out, "w") as f:
@@ -557,6 +657,9 @@ def main():
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
+    if not err <= PARITY_TOL:
+        print(f"[bench] sampled outputs differ from the oracle: {errs} > {PARITY_TOL}", file=sys.stderr, flush=True)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -14,10 +14,18 @@ def pytest_configure(config):
 
 
 def relerr(got, ref):
-    """max|got - ref| / max|ref|; if ref is all zeros, max|got - ref|."""
+    """max|got - ref| / max|ref| (complex moduli for complex input); if ref
+    is all zeros, max|got - ref|. Real and complex arguments may not be
+    mixed: a spectrum compared with a real array (or the other way round)
+    would hide the imaginary part."""
     import numpy as np
-    got = np.asarray(got, dtype=np.float64)
-    ref = np.asarray(ref, dtype=np.float64)
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    if np.iscomplexobj(got) != np.iscomplexobj(ref):
+        raise AssertionError(f"real/complex mismatch: {got.dtype} against {ref.dtype}")
+    dt = np.complex128 if np.iscomplexobj(ref) else np.float64
+    got = got.astype(dt)
+    ref = ref.astype(dt)
     if got.shape != ref.shape:
         raise AssertionError(f"shape {got.shape} != {ref.shape}")
     err = float(np.max(np.abs(got - ref))) if ref.size else 0.0

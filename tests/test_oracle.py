@@ -374,3 +374,21 @@ def test_oas_weight_gradient_with_conjugated_windows(shape):
     idx = (h + np.arange(n)) % L
     got = c[:, :, idx][:, :, :, idx]
     assert relerr(got, oracle.conv_backward_filter(x, g, n)) <= 1e-13
+
+
+def test_relerr_sees_imaginary_parts():
+    """The comparison used by every parity test: a conjugated or
+    sign-flipped spectrum must fail it, and a complex array may not be
+    compared with a real one."""
+    rng = np.random.default_rng(4)
+    z = rng.standard_normal((6, 5)) + 1j * rng.standard_normal((6, 5))
+    assert relerr(z, z) == 0.0
+    assert relerr(np.conj(z), z) > 0.1
+    assert relerr(z.real - 1j * z.imag, z) > 0.1
+    assert relerr(1j * z, z) > 0.1
+    assert relerr(z.astype(np.complex64), z) < 1e-6
+    assert relerr(np.array([1 + 1j, 2]), np.array([1 - 1j, 2])) == 1.0
+    with pytest.raises(AssertionError):
+        relerr(z.real, z)
+    with pytest.raises(AssertionError):
+        relerr(z, z.real)

@@ -3,7 +3,10 @@
 Bar: max|gpu - oracle| / max|oracle| <= 2e-5 per output tensor and pass, for
 float32 data. Whole arrays are compared wherever the oracle finishes in
 seconds; the full-size layers are compared on sampled outputs that the
-oracle evaluates one by one, in the same launch configuration bench.py times.
+oracle evaluates one by one, in the same launch configuration bench.py times:
+whole images (first and last), every image and channel block on sampled
+pixels, and the weight gradient whole for kernel-channel pairs spanning every
+output tile.
 """
 
 import numpy as np
@@ -264,25 +267,112 @@ def test_reduced_large_layers_whole(gpu_lib, name, batch, C, K, tiling):
     check_whole(x, w, g, tiling=tiling)
 
 
+def run_training_step(plan, x, w, g):
+    """The three passes as bench.py times them: backward_data reuses the
+    forward's kernel spectra, backward_filter the input and gradient spectra
+    of the two passes before it."""
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    y = plan.forward(xd, wd)
+    dx = plan.backward_data(gd, None)
+    dw = plan.backward_filter(None, None)
+    torch.cuda.synchronize()
+    return y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
+
+
+def _stratified(rng, B, nch, side, per=4, block=32):
+    """Index lists (b, ch, i, j): `per` random pixels for every image and
+    every block of `block` channels (the row tiles of the contractions span
+    whole 32-channel blocks, their column tiles whole images or parts of
+    one), plus the last pixel of the last channel of every image."""
+    cols = [[], [], [], []]
+    for b in range(B):
+        for c0 in range(0, nch, block):
+            c1 = min(c0 + block, nch)
+            cols[0] += [b] * per
+            cols[1] += list(rng.integers(c0, c1, per))
+            cols[2] += list(rng.integers(0, side, per))
+            cols[3] += list(rng.integers(0, side, per))
+        cols[0].append(b)
+        cols[1].append(nch - 1)
+        cols[2].append(side - 1)
+        cols[3].append(side - 1)
+    return [np.asarray(c) for c in cols]
+
+
+def _one_per_block(rng, nch, block=32):
+    """One random channel from every block of `block`, plus the first and
+    last channel."""
+    picks = {0, nch - 1}
+    for c0 in range(0, nch, block):
+        picks.add(int(rng.integers(c0, min(c0 + block, nch))))
+    return sorted(picks)
+
+
+_FULL_INPUTS = {}
+_FULL_REFS = {}
+
+
+def full_size_inputs(name):
+    """Seeded inputs of a named layer at full size (drawn once per session)."""
+    if name not in _FULL_INPUTS:
+        _FULL_INPUTS[name] = make_inputs(LAYERS[name], seed=0)
+    return _FULL_INPUTS[name]
+
+
+def full_size_refs(name):
+    """Oracle values for check_full_size, computed once per layer: the first
+    and last image whole, stratified pixels, and whole dw planes of kernel-
+    channel pairs spanning every 32 x 32 block."""
+    if name not in _FULL_REFS:
+        ly = LAYERS[name]
+        x, w, g = full_size_inputs(name)
+        B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
+        ends = sorted({0, B - 1})
+        rng = np.random.default_rng(1)
+        iy = _stratified(rng, B, K, M)
+        ix = _stratified(rng, B, C, N)
+        cs, ks = _one_per_block(rng, C), _one_per_block(rng, K)
+        _FULL_REFS[name] = dict(
+            ends=ends, y_ends=oracle.conv_forward(x[ends], w), dx_ends=oracle.conv_backward_data(g[ends], w, N),
+            iy=iy, y_at=oracle.conv_forward_at(x, w, *iy), ix=ix, dx_at=oracle.conv_backward_data_at(g, w, N, *ix),
+            cs=cs, ks=ks, dw_pairs=oracle.conv_backward_filter(x[:, cs], g[:, ks], n))
+    return _FULL_REFS[name]
+
+
+def check_full_size(name, y, dx, dw, label):
+    """Full-size outputs against the oracle:
+    * y and dx compared whole for the first and the last image (all output
+      and input channels);
+    * y and dx on four random pixels of every image and every block of 32
+      channels (every column and row tile of the forward and error-propagation
+      contractions);
+    * dw whole (all n^2 taps) for one input channel from every block of 32
+      and one kernel from every block of 32, all pairs of the two sets (every
+      output tile of the weight-gradient contraction)."""
+    r = full_size_refs(name)
+    n = LAYERS[name].n
+    e_whole = (relerr(y[r["ends"]], r["y_ends"]), relerr(dx[r["ends"]], r["dx_ends"]))
+    e_strat = (relerr(y[tuple(r["iy"])], r["y_at"]), relerr(dx[tuple(r["ix"])], r["dx_at"]))
+    e_dw = relerr(dw[np.ix_(r["ks"], r["cs"])], r["dw_pairs"])
+    print(f"{label}: whole images {r['ends']}: fwd {e_whole[0]:.2e} bwd_data {e_whole[1]:.2e}; "
+          f"{len(r['iy'][0])} y and {len(r['ix'][0])} dx pixels over every image and channel block: "
+          f"fwd {e_strat[0]:.2e} bwd_data {e_strat[1]:.2e}; dw {len(r['ks'])}x{len(r['cs'])} kernel-channel "
+          f"pairs x {n * n} taps: {e_dw:.2e}", flush=True)
+    assert max(e_whole + e_strat + (e_dw,)) <= TOL, (e_whole, e_strat, e_dw)
+    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dw).all()
+
+
 @pytest.mark.parametrize("tiling", ["paper", "auto"])
 @pytest.mark.parametrize("name", ["first224", "mid56", "large128"])
-def test_full_size_layers_sampled(gpu_lib, name, tiling):
+def test_full_size_layers(gpu_lib, name, tiling):
+    """Full size, in the launch configuration bench.py times (tiling "auto"
+    is its default)."""
     ly = LAYERS[name]
-    x, w, g = make_inputs(ly, seed=0)
-    _, y, dx, dw = run_layer(x, w, g, tiling=tiling)
-    rng = np.random.default_rng(1)
-    S = 48
-    B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
-    # include the corners (ragged last block row and column) among the samples
-    iy = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, K, M, M)]
-    ix = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, C, N, N)]
-    iw = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (K, C, n, n)]
-    e = (relerr(y[tuple(iy)], oracle.conv_forward_at(x, w, *iy)),
-         relerr(dx[tuple(ix)], oracle.conv_backward_data_at(g, w, N, *ix)),
-         relerr(dw[tuple(iw)], oracle.conv_backward_filter_at(x, g, n, *iw)))
-    print(f"{name} sampled rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e} bwd_filter {e[2]:.2e}", flush=True)
-    assert max(e) <= TOL, e
-    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dw).all()
+    x, w, g = full_size_inputs(name)
+    plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=DEV, tiling=tiling)
+    y, dx, dw = run_training_step(plan, x, w, g)
+    del plan
+    check_full_size(name, y, dx, dw, label=f"{name} {tiling} {y.shape}")
 
 
 def test_stage_spectra_match_oracle_steps(gpu_lib):
@@ -509,30 +599,14 @@ def test_overlap_save_reduced_large_layers_whole(gpu_lib, name, batch, C, K):
 
 
 @pytest.mark.parametrize("name", ["first224", "mid56", "large128"])
-def test_overlap_save_full_size_layers_sampled(gpu_lib, name):
-    """Full size, in the launch configuration bench.py --method oas times:
-    cached spectra reused (w, x, g NULL where the bench passes NULL)."""
+def test_overlap_save_full_size_layers(gpu_lib, name):
+    """Full size, in the launch configuration bench.py --method oas times."""
     ly = LAYERS[name]
-    x, w, g = make_inputs(ly, seed=0)
+    x, w, g = full_size_inputs(name)
     plan = binding.Plan(ly.B, ly.C, ly.K, ly.N, ly.n, device=DEV, tiling="auto", method=OAS)
-    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
-    y = plan.forward(xd, wd)
-    dx = plan.backward_data(gd, None)
-    dw = plan.backward_filter(None, None)
-    torch.cuda.synchronize()
-    y, dx, dw = y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
-    rng = np.random.default_rng(2)
-    S = 48
-    B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
-    iy = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, K, M, M)]
-    ix = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (B, C, N, N)]
-    iw = [np.r_[rng.integers(0, s, S), [0, s - 1]] for s in (K, C, n, n)]
-    e = (relerr(y[tuple(iy)], oracle.conv_forward_at(x, w, *iy)),
-         relerr(dx[tuple(ix)], oracle.conv_backward_data_at(g, w, N, *ix)),
-         relerr(dw[tuple(iw)], oracle.conv_backward_filter_at(x, g, n, *iw)))
-    print(f"{name} overlap-save sampled rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e} bwd_filter {e[2]:.2e}", flush=True)
-    assert max(e) <= TOL, e
-    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dw).all()
+    y, dx, dw = run_training_step(plan, x, w, g)
+    del plan
+    check_full_size(name, y, dx, dw, label=f"{name} overlap-save")
 
 
 def test_overlap_save_stage_spectra_match_oracle(gpu_lib):

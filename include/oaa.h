@@ -216,6 +216,27 @@ oaa_status_t oaa_conv_backward_data(oaa_plan_t plan, const float* g, const float
 oaa_status_t oaa_conv_backward_filter(oaa_plan_t plan, const float* x, const float* g, float* dw,
                                       void* hip_stream);
 
+/* Forward pass without device allocation, for callers that cannot allocate:
+ * code being captured into a HIP graph, tight serving loops, harnesses that
+ * forbid hipMalloc. Same result as oaa_conv_forward(plan, x, w, y, stream)
+ * (the same kernels), but the spectra live in a static scratch array inside
+ * the library (64 MiB on each device, held until the process ends) instead
+ * of the plan's bound workspace, so no workspace need be bound.
+ *   - plan: a plan whose oaa_plan_workspace_bytes() is at most 64 MiB, else
+ *     OAA_ERR_UNSUPPORTED before anything is enqueued.
+ *   - x, w, y: device pointers as for oaa_conv_forward, all non-NULL
+ *     (OAA_ERR_INVALID_ARG otherwise): no cached spectra are read, and none
+ *     are recorded for later NULL arguments (the plan's own cache and
+ *     workspace are left untouched).
+ *   - stream: a stream of the current device (NULL = its null stream).
+ * Makes no hipMalloc / hipFree call and allocates nothing; the first call on
+ * a device looks up that device's copy of the array. Per-stage timing is
+ * not recorded. Every call on one device shares that device's array, which
+ * keeps the last call's contents (nothing in it needs to start at zero):
+ * calls that overlap in time on one device, from any plan or stream, race. */
+oaa_status_t oaa_conv_forward_noalloc(oaa_plan_t plan, const float* x, const float* w, float* y,
+                                      void* hip_stream);
+
 /* Static text for a status code. */
 const char* oaa_status_string(oaa_status_t status);
 

@@ -46,6 +46,7 @@ SIGNATURES = {
     "oaa_conv_forward": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
     "oaa_conv_backward_data": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
     "oaa_conv_backward_filter": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
+    "oaa_conv_forward_noalloc": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
     "oaa_status_string": (ctypes.c_char_p, [_c_int]),
     "oaa_last_error_detail": (ctypes.c_char_p, []),
 }
@@ -159,6 +160,10 @@ def oaa_conv_backward_filter(plan, x, g, dw, stream):
     return _check(load().oaa_conv_backward_filter(plan, x, g, dw, stream))
 
 
+def oaa_conv_forward_noalloc(plan, x, w, y, stream):
+    return _check(load().oaa_conv_forward_noalloc(plan, x, w, y, stream))
+
+
 def oaa_status_string(status):
     return load().oaa_status_string(status).decode()
 
@@ -237,6 +242,15 @@ class Plan:
         y = self._empty((B, K, M, M)) if y is None else y
         oaa_conv_forward(self.handle, self._ptr(x, (B, C, N, N), "x"), self._ptr(w, (K, C, n, n), "w"),
                          self._ptr(y, (B, K, M, M), "y"), self._stream())
+        return y
+
+    def forward_noalloc(self, x, w, y):
+        """oaa_conv_forward_noalloc into the caller's y: the library's static
+        scratch instead of this plan's workspace, no allocation."""
+        g = self.geometry
+        B, C, K, N, n, M = g["B"], g["C"], g["K"], g["N"], g["n"], g["M"]
+        oaa_conv_forward_noalloc(self.handle, self._ptr(x, (B, C, N, N), "x"), self._ptr(w, (K, C, n, n), "w"),
+                                 self._ptr(y, (B, K, M, M), "y"), self._stream())
         return y
 
     def backward_data(self, gr, w, dx=None):

@@ -10,6 +10,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -105,7 +106,18 @@ oaa_status_t hip_status(hipError_t e, const char* what) {
   return fail(OAA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-float2* region(oaa_plan_t p, int r) { return reinterpret_cast<float2*>(p->ws + p->off[r]); }
+// What one pass runs against: the plan, the device memory its spectra live in
+// (the bound workspace, or the library's static scratch for the
+// allocation-free entry point), and the stream. `own` is true for the bound
+// workspace: only then are launches timed and cached spectra recorded.
+struct Ctx {
+  oaa_plan_t p;
+  char* ws;
+  hipStream_t s;
+  bool own;
+};
+
+float2* region(const Ctx& cx, int r) { return reinterpret_cast<float2*>(cx.ws + cx.p->off[r]); }
 
 hipError_t take_event(oaa_plan_t p, hipEvent_t* ev) {
   if (!p->event_pool.empty()) {
@@ -118,8 +130,10 @@ hipError_t take_event(oaa_plan_t p, hipEvent_t* ev) {
 
 // Run one launch; when timing is on, bracket it with events on stream s.
 template <class Fn>
-oaa_status_t timed(oaa_plan_t p, oaa_stage_t stage, hipStream_t s, const char* what, Fn&& launch) {
-  if (!p->timing) return hip_status(launch(), what);
+oaa_status_t timed(const Ctx& cx, oaa_stage_t stage, const char* what, Fn&& launch) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
+  if (!cx.own || !p->timing) return hip_status(launch(), what);
   hipEvent_t a = nullptr, b = nullptr;
   hipError_t e = take_event(p, &a);
   if (e == hipSuccess) e = take_event(p, &b);
@@ -140,10 +154,12 @@ oaa_status_t timed(oaa_plan_t p, oaa_stage_t stage, hipStream_t s, const char* w
   return OAA_OK;
 }
 
-oaa_status_t run_filter_fft(oaa_plan_t p, const float* w, hipStream_t s) {
+oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
   oaa::TileFwdParams t{};
   t.src = w;
-  t.dst = region(p, OAA_REGION_W_SPECTRUM);
+  t.dst = region(cx, OAA_REGION_W_SPECTRUM);
   t.n_img = p->K;   // w[k][c] plane; spectra [F][C][K]
   t.n_ch = p->C;
   t.H = p->n;
@@ -152,18 +168,20 @@ oaa_status_t run_filter_fft(oaa_plan_t p, const float* w, hipStream_t s) {
   t.R = p->n;
   t.T = 1;
   t.gather = 1;
-  oaa_status_t st = timed(p, OAA_STAGE_W_SPECTRUM, s, "kernel spectra",
+  oaa_status_t st = timed(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra",
                           [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
-  if (st == OAA_OK) p->w_valid = true;
+  if (st == OAA_OK && cx.own) p->w_valid = true;
   return st;
 }
 
-oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
+oaa_status_t run_input_fft(const Ctx& cx, const float* x) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // L x L windows of x starting every h = L - n + 1
     oaa::WindowParams t{};
     t.src = x;
-    t.dst = region(p, OAA_REGION_X_SPECTRUM);
+    t.dst = region(cx, OAA_REGION_X_SPECTRUM);
     t.n_img = p->B;
     t.n_ch = p->C;
     t.H = p->N;
@@ -171,9 +189,9 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
     t.S = p->L;
     t.off = 0;
     t.T = p->T;
-    oaa_status_t st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input window spectra",
+    oaa_status_t st = timed(cx, OAA_STAGE_X_SPECTRUM, "input window spectra",
                             [&] { return oaa::launch_window_rfft2(p->L, t, s); });
-    if (st == OAA_OK) p->x_valid = true;
+    if (st == OAA_OK && cx.own) p->x_valid = true;
     return st;
   }
   oaa_status_t st;
@@ -181,7 +199,7 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
     // b x b blocks as windows of side b at pitch b
     oaa::WindowParams t{};
     t.src = x;
-    t.dst = region(p, OAA_REGION_X_SPECTRUM);
+    t.dst = region(cx, OAA_REGION_X_SPECTRUM);
     t.n_img = p->B;
     t.n_ch = p->C;
     t.H = p->N;
@@ -189,12 +207,12 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
     t.S = p->b;
     t.off = 0;
     t.T = p->T;
-    st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
+    st = timed(cx, OAA_STAGE_X_SPECTRUM, "input block spectra",
                [&] { return oaa::launch_window_rfft2(p->L, t, s); });
   } else {
     oaa::TileFwdParams t{};
     t.src = x;
-    t.dst = region(p, OAA_REGION_X_SPECTRUM);
+    t.dst = region(cx, OAA_REGION_X_SPECTRUM);
     t.n_img = p->B;
     t.n_ch = p->C;
     t.H = p->N;
@@ -202,21 +220,23 @@ oaa_status_t run_input_fft(oaa_plan_t p, const float* x, hipStream_t s) {
     t.off = 0;
     t.R = p->b;
     t.T = p->T;
-    st = timed(p, OAA_STAGE_X_SPECTRUM, s, "input block spectra",
+    st = timed(cx, OAA_STAGE_X_SPECTRUM, "input block spectra",
                [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
   }
-  if (st == OAA_OK) p->x_valid = true;
+  if (st == OAA_OK && cx.own) p->x_valid = true;
   return st;
 }
 
-oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
+oaa_status_t run_grad_fft(const Ctx& cx, const float* g) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // h x h blocks of g, h = L - n + 1
     oaa_status_t st;
     if (blocks_as_windows(p)) {
       oaa::WindowParams t{};
       t.src = g;
-      t.dst = region(p, OAA_REGION_G_SPECTRUM);
+      t.dst = region(cx, OAA_REGION_G_SPECTRUM);
       t.n_img = p->B;
       t.n_ch = p->K;
       t.H = p->M;
@@ -224,12 +244,12 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
       t.S = p->b;
       t.off = 0;
       t.T = p->T;
-      st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient block spectra",
+      st = timed(cx, OAA_STAGE_G_SPECTRUM, "gradient block spectra",
                  [&] { return oaa::launch_window_rfft2(p->L, t, s); });
     } else {
       oaa::TileFwdParams t{};
       t.src = g;
-      t.dst = region(p, OAA_REGION_G_SPECTRUM);
+      t.dst = region(cx, OAA_REGION_G_SPECTRUM);
       t.n_img = p->B;
       t.n_ch = p->K;
       t.H = p->M;
@@ -237,17 +257,17 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
       t.off = 0;
       t.R = p->b;
       t.T = p->T;
-      st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient block spectra",
+      st = timed(cx, OAA_STAGE_G_SPECTRUM, "gradient block spectra",
                  [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
     }
-    if (st == OAA_OK) p->g_valid = true;
+    if (st == OAA_OK && cx.own) p->g_valid = true;
     return st;
   }
   // window (P,Q) of the zero-framed gradient: g[P*n + r - (n-1)][Q*n + s - (n-1)],
   // r, s < 2n
   oaa::WindowParams t{};
   t.src = g;
-  t.dst = region(p, OAA_REGION_G_SPECTRUM);
+  t.dst = region(cx, OAA_REGION_G_SPECTRUM);
   t.n_img = p->B;
   t.n_ch = p->K;
   t.H = p->M;
@@ -255,13 +275,15 @@ oaa_status_t run_grad_fft(oaa_plan_t p, const float* g, hipStream_t s) {
   t.S = 2 * p->b <= p->L ? 2 * p->b : p->L;  // window side, >= b + n - 1
   t.off = p->n - 1;
   t.T = p->T;
-  oaa_status_t st = timed(p, OAA_STAGE_G_SPECTRUM, s, "gradient window spectra",
+  oaa_status_t st = timed(cx, OAA_STAGE_G_SPECTRUM, "gradient window spectra",
                           [&] { return oaa::launch_window_rfft2(p->L, t, s); });
-  if (st == OAA_OK) p->g_valid = true;
+  if (st == OAA_OK && cx.own) p->g_valid = true;
   return st;
 }
 
-oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipStream_t s, const char* what) {
+oaa_status_t run_gemm(const Ctx& cx, oaa::GemmParams& g, oaa_stage_t stage, const char* what) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
   g.F = oaa::unique_bins(p->L);
   g.L = p->L;
   oaa_contraction_t c = p->contraction;
@@ -271,7 +293,7 @@ oaa_status_t run_gemm(oaa_plan_t p, oaa::GemmParams& g, oaa_stage_t stage, hipSt
                                    : OAA_CONTRACTION_VALU;
   if (c == OAA_CONTRACTION_NARROW && !oaa::narrow_supported(g))
     return fail(OAA_ERR_UNSUPPORTED, "%s: the streaming contraction needs C <= %d", what, oaa::kNarrowMaxC);
-  return timed(p, stage, s, what, [&] {
+  return timed(cx, stage, what, [&] {
     switch (c) {
       case OAA_CONTRACTION_MFMA: return oaa::launch_cgemm_mfma(g, s);
       case OAA_CONTRACTION_NARROW: return oaa::launch_cgemm_narrow(g, s);
@@ -337,6 +359,173 @@ int choose_oas_side(int C, int K, int N, int n) {
     }
   }
   return L;
+}
+
+// The passes, after validation, on the context's workspace and stream.
+oaa_status_t forward_pass(const Ctx& cx, const float* x, const float* w, float* y) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
+  oaa_status_t st;
+  if (w && (st = run_filter_fft(cx, w))) return st;
+  if ((st = run_input_fft(cx, x))) return st;
+  // Yhat[f] (K x BP) = What[f]^T (K x C) * Xhat[f] (C x BP)
+  const long BP = (long)p->B * p->P;
+  oaa::GemmParams g{};
+  g.A = region(cx, OAA_REGION_W_SPECTRUM);
+  g.B = region(cx, OAA_REGION_X_SPECTRUM);
+  g.C = region(cx, OAA_REGION_PRODUCT);
+  g.M = p->K; g.N = (int)BP; g.Kr = p->C;
+  g.lda = p->K; g.ldb = BP; g.ldc = BP;
+  g.a_fstride = (size_t)p->C * p->K;
+  g.b_fstride = (size_t)p->C * BP;
+  g.c_fstride = (size_t)p->K * BP;
+  g.nsplit = 1; g.kchunk = p->C; g.c_sstride = 0;
+  g.a_trans = true; g.a_conj = false; g.b_trans = false; g.b_conj = false;
+  if ((st = run_gemm(cx, g, OAA_STAGE_FWD_PRODUCT, "forward contraction"))) return st;
+  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
+    // rows and columns [n-1, L) of each window's inverse are its h x h outputs
+    oaa::CropParams c{};
+    c.src = region(cx, OAA_REGION_PRODUCT);
+    c.nsplit = 1; c.split_stride = 0;
+    c.dst = y;
+    c.n_img = p->B; c.n_ch = p->K;
+    c.H = p->M; c.n = p->b; c.T = p->T;
+    c.origin = p->n - 1;
+    return timed(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-save crop",
+                 [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+  }
+  oaa::FoldCropParams o{};
+  o.src = region(cx, OAA_REGION_PRODUCT);
+  o.dst = y;
+  o.n_img = p->B; o.n_ch = p->K;
+  o.M = p->M; o.n = p->b; o.off = p->n - 1; o.T = p->T;
+  o.To = p->T; o.shift = 0;
+  o.S = p->b + p->n - 1;
+  // the overlap-add in the frequency domain needs neighbours shifted by b not
+  // to wrap into the block (2b <= L); larger blocks add their neighbours in space
+  if (2 * p->b <= p->L)
+    return timed(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-add",
+                 [&] { return oaa::launch_irfft2_fold_crop(p->L, o, s); });
+  return timed(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-add",
+               [&] { return oaa::launch_irfft2_overlap_crop(p->L, o, s); });
+}
+
+
+oaa_status_t backward_data_pass(const Ctx& cx, const float* g, const float* w, float* dx) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
+  oaa_status_t st;
+  if (w && (st = run_filter_fft(cx, w))) return st;
+  if ((st = run_grad_fft(cx, g))) return st;
+  // dXhat[f] (C x BP) = conj(What[f]) (C x K) * Ghat[f] (K x BP)
+  const long BP = (long)p->B * p->P;
+  oaa::GemmParams gm{};
+  gm.A = region(cx, OAA_REGION_W_SPECTRUM);
+  gm.B = region(cx, OAA_REGION_G_SPECTRUM);
+  gm.C = region(cx, OAA_REGION_PRODUCT);
+  gm.M = p->C; gm.N = (int)BP; gm.Kr = p->K;
+  gm.lda = p->K; gm.ldb = BP; gm.ldc = BP;
+  gm.a_fstride = (size_t)p->C * p->K;
+  gm.b_fstride = (size_t)p->K * BP;
+  gm.c_fstride = (size_t)p->C * BP;
+  gm.nsplit = 1; gm.kchunk = p->K; gm.c_sstride = 0;
+  gm.a_trans = false; gm.a_conj = true; gm.b_trans = false; gm.b_conj = false;
+  if ((st = run_gemm(cx, gm, OAA_STAGE_BWD_DATA_PRODUCT, "backward-data contraction"))) return st;
+  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
+    // overlap-add of the gradient blocks' results into dx. The contraction
+    // used conj(W): each inverse is a circular correlation with support
+    // [-(n-1), h), i.e. the block's convolution with the flipped kernel
+    // circularly shifted up and left by n-1; the kernel shifts it back.
+    oaa::FoldCropParams o{};
+    o.src = region(cx, OAA_REGION_PRODUCT);
+    o.dst = dx;
+    o.n_img = p->B; o.n_ch = p->C;
+    o.M = p->N; o.n = p->b; o.off = 0; o.T = p->T;
+    o.To = (p->N + p->b - 1) / p->b;
+    o.shift = p->n - 1;
+    o.S = p->L;
+    return timed(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + overlap-add",
+                 [&] { return oaa::launch_irfft2_overlap_crop(p->L, o, s); });
+  }
+  oaa::CropParams c{};
+  c.src = region(cx, OAA_REGION_PRODUCT);
+  c.nsplit = 1; c.split_stride = 0;
+  c.dst = dx;
+  c.n_img = p->B; c.n_ch = p->C;
+  c.H = p->N; c.n = p->b; c.T = p->T;
+  c.origin = 0;
+  return timed(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + block crop",
+               [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+}
+
+
+oaa_status_t backward_filter_pass(const Ctx& cx, const float* x, const float* g, float* dw) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
+  oaa_status_t st;
+  if (x && (st = run_input_fft(cx, x))) return st;
+  if (g && (st = run_grad_fft(cx, g))) return st;
+  // dWhat^T[f] (C x K) = conj(Xhat[f]) (C x BP) * Ghat[f]^T (BP x K), split over BP
+  const long BP = (long)p->B * p->P;
+  oaa::GemmParams gm{};
+  gm.A = region(cx, OAA_REGION_X_SPECTRUM);
+  gm.B = region(cx, OAA_REGION_G_SPECTRUM);
+  gm.C = region(cx, OAA_REGION_PRODUCT);
+  gm.M = p->C; gm.N = p->K; gm.Kr = (int)BP;
+  gm.lda = BP; gm.ldb = BP; gm.ldc = p->K;
+  gm.a_fstride = (size_t)p->C * BP;
+  gm.b_fstride = (size_t)p->K * BP;
+  gm.c_fstride = (size_t)p->C * p->K;
+  gm.nsplit = p->split; gm.kchunk = p->kchunk;
+  gm.c_sstride = (size_t)p->F * p->C * p->K;
+  gm.a_trans = false; gm.a_conj = true; gm.b_trans = true; gm.b_conj = false;
+  if ((st = run_gemm(cx, gm, OAA_STAGE_BWD_FILTER_PRODUCT, "backward-filter contraction"))) return st;
+  oaa::CropParams c{};
+  c.src = region(cx, OAA_REGION_PRODUCT);
+  c.nsplit = p->split;
+  c.split_stride = (size_t)p->F * p->C * p->K;
+  c.dst = dw;
+  c.n_img = p->K; c.n_ch = p->C;   // spectra [F][C][K], output planes dw[k][c]
+  c.H = p->n; c.n = p->n; c.T = 1;
+  // overlap-save: the windows carry the conjugate, so dw[u][v] sits at rows
+  // and columns (h + u) mod L of the inverse
+  c.origin = p->method == OAA_METHOD_OVERLAP_SAVE ? p->b & (p->L - 1) : 0;
+  return timed(cx, OAA_STAGE_BWD_FILTER_INVERSE, "inverse transform of weight gradient",
+               [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+}
+
+
+// Static scratch of oaa_conv_forward_noalloc: spectra of layers whose
+// workspace fits, for callers that cannot allocate device memory. Every
+// device that runs the library holds its own copy until the process ends.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (with that device current). In host code the array's name
+// stands for a host-side symbol, not a device address: only this pointer may
+// be handed to kernels.
+oaa_status_t scratch_on_current_device(char** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(OAA_ERR_UNSUPPORTED, "device %d is beyond the %d devices the static scratch serves", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress of the static scratch");
+    if (!ptr || reinterpret_cast<uintptr_t>(ptr) % kAlign)
+      return fail(OAA_ERR_HIP, "static scratch address %p is not %zu-byte aligned", ptr, kAlign);
+    g_scratch_ptr[dev] = static_cast<char*>(ptr);
+  }
+  *out = g_scratch_ptr[dev];
+  return OAA_OK;
 }
 
 }  // namespace
@@ -564,101 +753,16 @@ oaa_status_t oaa_conv_forward(oaa_plan_t p, const float* x, const float* w, floa
   if (oaa_status_t st = check_plan(p, true)) return st;
   if (!x || !y) return fail(OAA_ERR_INVALID_ARG, "x and y must be non-NULL");
   if (!w && !p->w_valid) return fail(OAA_ERR_NO_CACHE, "w is NULL and no kernel spectra are cached");
-  hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  oaa_status_t st;
-  if (w && (st = run_filter_fft(p, w, s))) return st;
-  if ((st = run_input_fft(p, x, s))) return st;
-  // Yhat[f] (K x BP) = What[f]^T (K x C) * Xhat[f] (C x BP)
-  const long BP = (long)p->B * p->P;
-  oaa::GemmParams g{};
-  g.A = region(p, OAA_REGION_W_SPECTRUM);
-  g.B = region(p, OAA_REGION_X_SPECTRUM);
-  g.C = region(p, OAA_REGION_PRODUCT);
-  g.M = p->K; g.N = (int)BP; g.Kr = p->C;
-  g.lda = p->K; g.ldb = BP; g.ldc = BP;
-  g.a_fstride = (size_t)p->C * p->K;
-  g.b_fstride = (size_t)p->C * BP;
-  g.c_fstride = (size_t)p->K * BP;
-  g.nsplit = 1; g.kchunk = p->C; g.c_sstride = 0;
-  g.a_trans = true; g.a_conj = false; g.b_trans = false; g.b_conj = false;
-  if ((st = run_gemm(p, g, OAA_STAGE_FWD_PRODUCT, s, "forward contraction"))) return st;
-  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
-    // rows and columns [n-1, L) of each window's inverse are its h x h outputs
-    oaa::CropParams c{};
-    c.src = region(p, OAA_REGION_PRODUCT);
-    c.nsplit = 1; c.split_stride = 0;
-    c.dst = y;
-    c.n_img = p->B; c.n_ch = p->K;
-    c.H = p->M; c.n = p->b; c.T = p->T;
-    c.origin = p->n - 1;
-    return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-save crop",
-                 [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
-  }
-  oaa::FoldCropParams o{};
-  o.src = region(p, OAA_REGION_PRODUCT);
-  o.dst = y;
-  o.n_img = p->B; o.n_ch = p->K;
-  o.M = p->M; o.n = p->b; o.off = p->n - 1; o.T = p->T;
-  o.To = p->T; o.shift = 0;
-  o.S = p->b + p->n - 1;
-  // the overlap-add in the frequency domain needs neighbours shifted by b not
-  // to wrap into the block (2b <= L); larger blocks add their neighbours in space
-  if (2 * p->b <= p->L)
-    return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
-                 [&] { return oaa::launch_irfft2_fold_crop(p->L, o, s); });
-  return timed(p, OAA_STAGE_FWD_INVERSE, s, "inverse transform + overlap-add",
-               [&] { return oaa::launch_irfft2_overlap_crop(p->L, o, s); });
+  return forward_pass(Ctx{p, p->ws, static_cast<hipStream_t>(stream), true}, x, w, y);
 }
 
 oaa_status_t oaa_conv_backward_data(oaa_plan_t p, const float* g, const float* w, float* dx, void* stream) {
   if (oaa_status_t st = check_plan(p, true)) return st;
   if (!g || !dx) return fail(OAA_ERR_INVALID_ARG, "g and dx must be non-NULL");
   if (!w && !p->w_valid) return fail(OAA_ERR_NO_CACHE, "w is NULL and no kernel spectra are cached");
-  hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  oaa_status_t st;
-  if (w && (st = run_filter_fft(p, w, s))) return st;
-  if ((st = run_grad_fft(p, g, s))) return st;
-  // dXhat[f] (C x BP) = conj(What[f]) (C x K) * Ghat[f] (K x BP)
-  const long BP = (long)p->B * p->P;
-  oaa::GemmParams gm{};
-  gm.A = region(p, OAA_REGION_W_SPECTRUM);
-  gm.B = region(p, OAA_REGION_G_SPECTRUM);
-  gm.C = region(p, OAA_REGION_PRODUCT);
-  gm.M = p->C; gm.N = (int)BP; gm.Kr = p->K;
-  gm.lda = p->K; gm.ldb = BP; gm.ldc = BP;
-  gm.a_fstride = (size_t)p->C * p->K;
-  gm.b_fstride = (size_t)p->K * BP;
-  gm.c_fstride = (size_t)p->C * BP;
-  gm.nsplit = 1; gm.kchunk = p->K; gm.c_sstride = 0;
-  gm.a_trans = false; gm.a_conj = true; gm.b_trans = false; gm.b_conj = false;
-  if ((st = run_gemm(p, gm, OAA_STAGE_BWD_DATA_PRODUCT, s, "backward-data contraction"))) return st;
-  if (p->method == OAA_METHOD_OVERLAP_SAVE) {
-    // overlap-add of the gradient blocks' results into dx. The contraction
-    // used conj(W): each inverse is a circular correlation with support
-    // [-(n-1), h), i.e. the block's convolution with the flipped kernel
-    // circularly shifted up and left by n-1; the kernel shifts it back.
-    oaa::FoldCropParams o{};
-    o.src = region(p, OAA_REGION_PRODUCT);
-    o.dst = dx;
-    o.n_img = p->B; o.n_ch = p->C;
-    o.M = p->N; o.n = p->b; o.off = 0; o.T = p->T;
-    o.To = (p->N + p->b - 1) / p->b;
-    o.shift = p->n - 1;
-    o.S = p->L;
-    return timed(p, OAA_STAGE_BWD_DATA_INVERSE, s, "inverse transform + overlap-add",
-                 [&] { return oaa::launch_irfft2_overlap_crop(p->L, o, s); });
-  }
-  oaa::CropParams c{};
-  c.src = region(p, OAA_REGION_PRODUCT);
-  c.nsplit = 1; c.split_stride = 0;
-  c.dst = dx;
-  c.n_img = p->B; c.n_ch = p->C;
-  c.H = p->N; c.n = p->b; c.T = p->T;
-  c.origin = 0;
-  return timed(p, OAA_STAGE_BWD_DATA_INVERSE, s, "inverse transform + block crop",
-               [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+  return backward_data_pass(Ctx{p, p->ws, static_cast<hipStream_t>(stream), true}, g, w, dx);
 }
 
 oaa_status_t oaa_conv_backward_filter(oaa_plan_t p, const float* x, const float* g, float* dw, void* stream) {
@@ -666,38 +770,22 @@ oaa_status_t oaa_conv_backward_filter(oaa_plan_t p, const float* x, const float*
   if (!dw) return fail(OAA_ERR_INVALID_ARG, "dw must be non-NULL");
   if (!x && !p->x_valid) return fail(OAA_ERR_NO_CACHE, "x is NULL and no input block spectra are cached");
   if (!g && !p->g_valid) return fail(OAA_ERR_NO_CACHE, "g is NULL and no gradient window spectra are cached");
-  hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  oaa_status_t st;
-  if (x && (st = run_input_fft(p, x, s))) return st;
-  if (g && (st = run_grad_fft(p, g, s))) return st;
-  // dWhat^T[f] (C x K) = conj(Xhat[f]) (C x BP) * Ghat[f]^T (BP x K), split over BP
-  const long BP = (long)p->B * p->P;
-  oaa::GemmParams gm{};
-  gm.A = region(p, OAA_REGION_X_SPECTRUM);
-  gm.B = region(p, OAA_REGION_G_SPECTRUM);
-  gm.C = region(p, OAA_REGION_PRODUCT);
-  gm.M = p->C; gm.N = p->K; gm.Kr = (int)BP;
-  gm.lda = BP; gm.ldb = BP; gm.ldc = p->K;
-  gm.a_fstride = (size_t)p->C * BP;
-  gm.b_fstride = (size_t)p->K * BP;
-  gm.c_fstride = (size_t)p->C * p->K;
-  gm.nsplit = p->split; gm.kchunk = p->kchunk;
-  gm.c_sstride = (size_t)p->F * p->C * p->K;
-  gm.a_trans = false; gm.a_conj = true; gm.b_trans = true; gm.b_conj = false;
-  if ((st = run_gemm(p, gm, OAA_STAGE_BWD_FILTER_PRODUCT, s, "backward-filter contraction"))) return st;
-  oaa::CropParams c{};
-  c.src = region(p, OAA_REGION_PRODUCT);
-  c.nsplit = p->split;
-  c.split_stride = (size_t)p->F * p->C * p->K;
-  c.dst = dw;
-  c.n_img = p->K; c.n_ch = p->C;   // spectra [F][C][K], output planes dw[k][c]
-  c.H = p->n; c.n = p->n; c.T = 1;
-  // overlap-save: the windows carry the conjugate, so dw[u][v] sits at rows
-  // and columns (h + u) mod L of the inverse
-  c.origin = p->method == OAA_METHOD_OVERLAP_SAVE ? p->b & (p->L - 1) : 0;
-  return timed(p, OAA_STAGE_BWD_FILTER_INVERSE, s, "inverse transform of weight gradient",
-               [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
+  return backward_filter_pass(Ctx{p, p->ws, static_cast<hipStream_t>(stream), true}, x, g, dw);
+}
+
+oaa_status_t oaa_conv_forward_noalloc(oaa_plan_t p, const float* x, const float* w, float* y, void* stream) {
+  if (oaa_status_t st = check_plan(p, false)) return st;
+  if (!x || !w || !y) return fail(OAA_ERR_INVALID_ARG, "x, w and y must be non-NULL (no cached spectra are used)");
+  if (p->ws_bytes > kScratchBytes)
+    return fail(OAA_ERR_UNSUPPORTED,
+                "the layer needs %zu bytes of spectra, more than the %zu bytes of static scratch "
+                "(use oaa_conv_forward with a bound workspace)",
+                p->ws_bytes, kScratchBytes);
+  char* ws = nullptr;
+  if (oaa_status_t st = scratch_on_current_device(&ws)) return st;
+  (void)hipGetLastError();
+  return forward_pass(Ctx{p, ws, static_cast<hipStream_t>(stream), false}, x, w, y);
 }
 
 }  // extern "C"

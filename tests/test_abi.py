@@ -288,3 +288,24 @@ def test_small_division_by_reciprocal_is_exact():
         assert m < (1 << 32)
         assert np.array_equal((x * m) >> np.uint64(32), x // np.uint64(d)), d
     assert (0xFFFFFFFF // 1 + 1) & 0xFFFFFFFF == 0  # why d = 1 needs its own path
+
+
+def test_forward_noalloc_validation(lib):
+    """oaa_conv_forward_noalloc refuses NULL tensors and layers whose spectra
+    exceed its 64 MiB static scratch before touching any device."""
+    h = binding.oaa_plan_create(32, 96, 256, 128, 16)
+    try:
+        assert binding.oaa_plan_workspace_bytes(h) > 64 << 20
+        st = lib.oaa_conv_forward_noalloc(h, 256, 256, 256, None)
+        assert binding.STATUS[st] == "OAA_ERR_UNSUPPORTED"
+        assert "static scratch" in binding.oaa_last_error_detail()
+    finally:
+        binding.oaa_plan_destroy(h)
+    h = binding.oaa_plan_create(1, 3, 4, 32, 5)
+    try:
+        for args in ((None, 256, 256), (256, None, 256), (256, 256, None)):
+            st = lib.oaa_conv_forward_noalloc(h, *args, None)
+            assert binding.STATUS[st] == "OAA_ERR_INVALID_ARG"
+        assert binding.STATUS[lib.oaa_conv_forward_noalloc(None, 256, 256, 256, None)] == "OAA_ERR_INVALID_ARG"
+    finally:
+        binding.oaa_plan_destroy(h)

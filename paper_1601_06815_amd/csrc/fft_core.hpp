@@ -80,37 +80,59 @@ __host__ __device__ __forceinline__ void fft_dif(float (&re)[L], float (&im)[L])
 
 // Value of x in the other lane of the pair, via DPP quad permute [1,0,3,2].
 __device__ __forceinline__ float pair_swap(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, false));
+}
+
+// c ? a : b for register-array elements a and b of compile-time index. The
+// operands are made opaque first: otherwise the compiler may select the
+// index instead of the value and lower the access into a compare-and-select
+// over the whole array.
+__device__ __forceinline__ float pick(bool c, float a, float b) {
+  asm volatile("" : "+v"(a), "+v"(b));
+  return c ? a : b;
 }
 
 // Length-L transform; lane h holds elements h L/2 + i, i < L/2. The first
-// decimation-in-frequency stage pairs element i of lane 0 with element i of
-// lane 1; then each lane transforms its half alone. On return lane h holds
-// coefficient 2m + h at position bitrev(m, L/2). Both lanes of every pair
-// must execute this together.
+// decimation-in-frequency stage pairs element i of lane 0 (a) with element i
+// of lane 1 (b): lane 0 keeps a + b, lane 1 (a - b) w^i. Both lanes run the
+// same instructions: with the partner's value p, each forms p + sg * own
+// (sg = +1 on lane 0, -1 on lane 1) and multiplies by 1 + hf (w^i - 1)
+// (hf = 0 on lane 0, 1 on lane 1), so no lane branches or selects. Then each
+// lane transforms its half alone. On return lane h holds coefficient 2m + h
+// at position bitrev(m, L/2). Both lanes of every pair must execute this
+// together.
 template <int L, int SIGN>
 __device__ __forceinline__ void fft_dif_split(float (&re)[L / 2], float (&im)[L / 2], int h) {
+  const float sg = h ? -1.f : 1.f, hf = h ? 1.f : 0.f;
 #pragma unroll
   for (int i = 0; i < L / 2; ++i) {
     const float pr = pair_swap(re[i]), pi = pair_swap(im[i]);
-    if (h == 0) {
-      re[i] += pr;
-      im[i] += pi;
+    const float dr = __builtin_fmaf(sg, re[i], pr), di = __builtin_fmaf(sg, im[i], pi);
+    if (i == 0) {
+      re[i] = dr;
+      im[i] = di;
     } else {
-      // (a - b) * exp(SIGN 2 pi i i / L): a from lane 0, b from this lane
-      twiddle_mul<L, SIGN>(i, pr - re[i], pi - im[i], re[i], im[i]);
+      const float c = tw::kTable<L>.c[i], sn = SIGN > 0 ? tw::kTable<L>.s[i] : -tw::kTable<L>.s[i];
+      const float wr = __builtin_fmaf(hf, c - 1.f, 1.f), wi = hf * sn;
+      re[i] = __builtin_fmaf(dr, wr, -di * wi);
+      im[i] = __builtin_fmaf(dr, wi, di * wr);
     }
   }
   fft_dif<L / 2, SIGN, false>(re, im);
 }
 
 // Same when elements [L/2, L) are zero: both lanes hold elements [0, L/2)
-// on entry and no exchange is needed.
+// on entry and no exchange is needed (lane 1 multiplies by w^i).
 template <int L, int SIGN>
 __device__ __forceinline__ void fft_dif_split_zh(float (&re)[L / 2], float (&im)[L / 2], int h) {
-  if (h == 1) {
+  const float hf = h ? 1.f : 0.f;
 #pragma unroll
-    for (int i = 0; i < L / 2; ++i) twiddle_mul<L, SIGN>(i, re[i], im[i], re[i], im[i]);
+  for (int i = 1; i < L / 2; ++i) {
+    const float c = tw::kTable<L>.c[i], sn = SIGN > 0 ? tw::kTable<L>.s[i] : -tw::kTable<L>.s[i];
+    const float wr = __builtin_fmaf(hf, c - 1.f, 1.f), wi = hf * sn;
+    const float dr = re[i], di = im[i];
+    re[i] = __builtin_fmaf(dr, wr, -di * wi);
+    im[i] = __builtin_fmaf(dr, wi, di * wr);
   }
   fft_dif<L / 2, SIGN, false>(re, im);
 }
@@ -119,7 +141,7 @@ __device__ __forceinline__ void fft_dif_split_zh(float (&re)[L / 2], float (&im)
 // getB(v) return bin v in [0, L/2] of the two half spectra. On return lane h
 // holds L * row0[s] in zr and L * row1[s] in zi for s = 2m + h at position
 // bitrev(m, L/2). The imaginary parts of bins 0 and L/2 are ignored.
-template <int L, class FA, class FB>
+template <int L, int BATCH = 0, class FA, class FB>
 __device__ __forceinline__ void irfft_pair_split(FA getA, FB getB, float (&zr)[L / 2], float (&zi)[L / 2], int h) {
   constexpr int H = L / 2;
 #pragma unroll
@@ -131,9 +153,14 @@ __device__ __forceinline__ void irfft_pair_split(FA getA, FB getB, float (&zr)[L
       zr[0] = a.x;
       zi[0] = b.x;
     } else {
-      zr[i] = h ? a.x + b.y : a.x - b.y;
-      zi[i] = h ? b.x - a.y : a.y + b.x;
+      // lane 0: a.x - b.y, a.y + b.x; lane 1: a.x + b.y, b.x - a.y
+      const float sg = h ? 1.f : -1.f;
+      zr[i] = __builtin_fmaf(sg, b.y, a.x);
+      zi[i] = __builtin_fmaf(-sg, a.y, b.x);
     }
+    // (with BATCH, the reads are issued in groups of BATCH elements, which
+    // bounds the registers they hold)
+    if (BATCH && i % BATCH == BATCH - 1) asm volatile("" ::: "memory");
   }
   fft_dif_split<L, +1>(zr, zi, h);
 }

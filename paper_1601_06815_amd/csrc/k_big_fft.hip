@@ -1,0 +1,535 @@
+// Transforms of side L = 64 and 128 (arXiv:1601.06815, Section 2: block
+// division, zero padding, the per-block transforms and the overlap-add of the
+// block results; Section 3.3 for the transform sides of large kernels), as
+// used for large blocks (b up to L - n + 1) and large kernels.
+//
+// Each L-point transform is split over a pair of neighbouring lanes
+// (fft_dif_split): a lane holds L/2 complex values, about 64 registers at
+// L = 64. A workgroup keeps the intermediate of TQ tiles in LDS (17 KB per
+// tile at L = 64, so one workgroup of up to nine tiles per CU) and walks over
+// groups of TQ consecutive tiles of one channel:
+//  * forward: pass 1 transforms the column pairs (s, s + L/2) of every window
+//    along its rows, lanes over consecutive columns so that the loads of a
+//    row are coalesced, and keeps rows u <= L/2 of the two real columns'
+//    spectra (rows past L/2 are their conjugates); pass 2 transforms each of
+//    those rows along the columns and writes bins (u, v) and (L - u, v) of
+//    the half spectrum with lanes over the group's tiles, so that a store
+//    instruction writes runs of TQ consecutive tiles of a bin;
+//  * inverse: pass 1 inverts the columns v <= L/2 (loads in runs of TQ
+//    tiles), pass 2 inverts row pairs to real rows, pass 3 writes the kept
+//    part of each tile (crop) or the overlap-added plane.
+// Consecutive groups run on one XCD at about the same time, so the runs that
+// neighbouring groups write into a bin meet in that XCD's L2. The next
+// group's input is loaded into registers while the current group's second
+// pass runs.
+#include <algorithm>
+#include <type_traits>
+
+#include "fft_core.hpp"
+#include "oaa_internal.hpp"
+#include "tile_common.hpp"
+
+namespace oaa {
+
+namespace {
+
+using namespace tile;
+
+constexpr size_t kBigLds = 160 * 1024;  // LDS of one CU
+
+// Tiles per group at L = 64 (overridable at build time for tuning sweeps).
+#ifndef OAA_BIG_TQ
+#define OAA_BIG_TQ 8
+#endif
+
+template <int L>
+struct Big {
+  static constexpr int H2 = L / 2, V = L / 2 + 1;
+  // forward LDS row stride (complex): columns [0, L/2) then, one slot on,
+  // columns [L/2, L)
+  static constexpr int RS = L + 2;
+  // inverse LDS row stride (complex): L/2 slots, slot 0 holding the real
+  // columns 0 and L/2 as (re, im), plus one slot of padding
+  static constexpr int RI = H2 + 1;
+  static constexpr int TQ_MAX = L == 64 ? 9 : 2;  // tiles per group (LDS)
+};
+
+// threads of a workgroup (at most): eight waves, which leaves a lane 256
+// registers; L per tile, one task per thread with the register prefetch,
+// else threads loop over the tasks
+template <int L, bool PF>
+constexpr int big_threads() {
+  return L == 64 && !PF ? 576 : 512;
+}
+
+// LDS per tile (complex elements, odd)
+template <int L>
+__host__ __device__ inline int fwd_tile_stride() {
+  return odd_at_least(Big<L>::H2 * Big<L>::RS);
+}
+template <int L>
+__host__ __device__ inline int inv_tile_stride(int KR) {
+  return odd_at_least(KR * Big<L>::RI);
+}
+
+// first group of this workgroup; groups advance by gridDim.x (a multiple of
+// 8), and the workgroups of one XCD take consecutive groups
+__device__ __forceinline__ long first_group() {
+  const unsigned nwg = gridDim.x;
+  return long(blockIdx.x % 8) * (nwg / 8) + blockIdx.x / 8;
+}
+
+// ---------------------------------------------------------------------------
+// forward: windows of planes -> half spectra
+//
+// Pass 1: z = x[., j] + i x[., j + L/2] along the rows; the real columns'
+// spectra are C_j[u] = (Z[u] + conj Z[-u]) / 2, C_{j+L/2}[u] =
+// (Z[u] - conj Z[-u]) / (2i), Hermitian in u, so rows u <= L/2 suffice; rows
+// 0 and L/2 are real and share LDS row 0 as (re, im). Pass 2: rows u in
+// [1, L/2) along the columns give bins (u, v), v <= L/2, and (L - u, v) =
+// conj X[u][L - v], 0 < v < L/2 (the other bins of rows past L/2 are
+// conjugates that nothing reads); the packed row gives rows 0 and L/2 by the
+// same separation as pass 1.
+template <int L, bool O32, bool PF>
+__global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFwdParams p) {
+  constexpr int H2 = Big<L>::H2, V = Big<L>::V, RS = Big<L>::RS;
+  static_assert(L >= 64, "the pass-1 lanes of one tile must fill whole waves");
+  extern __shared__ float smem[];
+  float2* lds = reinterpret_cast<float2*>(smem);
+  const int TSZ = fwd_tile_stride<L>();
+  const int tid = threadIdx.x, h = tid & 1;
+  const int P = p.T * p.T, tpc = p.n_img * P;
+  const size_t fstride = size_t(p.n_ch) * tpc;
+  const long ngroups = long(p.n_ch) * p.ngrp;
+  const unsigned nwg = gridDim.x;
+  // pass 1: tile q1, columns j and j + L/2, rows [h L/2, h L/2 + L/2); a
+  // wave holds one tile (lane = h + 2 (j + (L/2) q1))
+  const int j = (tid >> 1) % H2, q1 = (tid >> 1) / H2;
+  // pass 2: tile q2 (fastest), LDS row u
+  const int q2 = (tid >> 1) % p.TQ, u = (tid >> 1) / p.TQ;
+  float zr[H2], zi[H2];
+
+  auto load = [&](long gg) {
+    const int ch = int(gg / p.ngrp), t0 = int(gg % p.ngrp) * p.TQ;
+    const int nq = min(p.TQ, tpc - t0);
+    if (q1 >= nq) return;
+    const int t = t0 + q1, img = t / P, pp = t - img * P;
+    const int pr = pp / p.T, qc = pp - pr * p.T;
+    const float* plane = p.src + (size_t(img) * p.n_ch + ch) * size_t(p.H) * size_t(p.H);
+    const __amdgpu_buffer_rsrc_t rs = buffer_resource(plane, unsigned(p.H) * unsigned(p.H) * 4u);
+    const int gr0 = pr * p.pitch - p.off + h * H2;
+    const int ca = qc * p.pitch - p.off + j, cb = ca + H2;
+    const bool oka = j < p.S && unsigned(ca) < unsigned(p.H);
+    const bool okb = j + H2 < p.S && unsigned(cb) < unsigned(p.H);
+    const int lim = p.S - h * H2;  // rows of this half inside the window
+#pragma unroll
+    for (int i = 0; i < H2; ++i) {
+      const int gr = gr0 + i;
+      const bool okr = i < lim && unsigned(gr) < unsigned(p.H);
+      zr[i] = buffer_load_f1(rs, okr && oka ? unsigned(gr * p.H + ca) * 4u : kOutOfRange);
+      zi[i] = buffer_load_f1(rs, okr && okb ? unsigned(gr * p.H + cb) * 4u : kOutOfRange);
+    }
+  };
+
+  long g = first_group();
+  if (PF && g < ngroups) load(g);
+  for (; g < ngroups; g += nwg) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
+    const int nq = min(p.TQ, tpc - t0);
+    if (!PF) load(g);
+    if (q1 < nq) {
+      fft_dif_split<L, -1>(zr, zi, h);  // lane h: Z[2m + h] at bitrev(m)
+      float2* bq = lds + q1 * TSZ;
+#pragma unroll
+      for (int m = 1; m < H2 / 2; ++m) {  // u = 2m + h in [2, L/2), with u = 1 below
+        const int uu = 2 * m + h;
+        const int ps = bitrev(m, H2);
+        const int p0 = bitrev(H2 - m, H2), p1 = bitrev(H2 - m - 1, H2);  // -uu for h = 0, 1
+        const float a = zr[ps], b = zi[ps];
+        const float c = pick(h, zr[p1], zr[p0]), d = pick(h, zi[p1], zi[p0]);
+        bq[uu * RS + j] = make_float2(0.5f * (a + c), 0.5f * (b - d));
+        bq[uu * RS + H2 + 1 + j] = make_float2(0.5f * (b + d), 0.5f * (c - a));
+      }
+      // m = 0: u = 0 (lane 0) and u = 1 (lane 1, partner L - 1 at m = L/2 - 1);
+      // lane 0 also holds u = L/2 at m = L/4
+      const float a0 = zr[0], b0 = zi[0];
+      if (h) {
+        const int pl = bitrev(H2 - 1, H2);
+        const float c = zr[pl], d = zi[pl];
+        bq[RS + j] = make_float2(0.5f * (a0 + c), 0.5f * (b0 - d));
+        bq[RS + H2 + 1 + j] = make_float2(0.5f * (b0 + d), 0.5f * (c - a0));
+      } else {
+        const int ph = bitrev(H2 / 2, H2);
+        bq[j] = make_float2(a0, zr[ph]);
+        bq[H2 + 1 + j] = make_float2(b0, zi[ph]);
+      }
+    }
+    __syncthreads();
+    if (PF && g + nwg < ngroups) load(g + nwg);  // in flight during pass 2
+    if (q2 < nq && u < H2) {
+      const float2* row = lds + q2 * TSZ + u * RS + h * (H2 + 1);
+      float re[H2], im[H2];
+#pragma unroll
+      for (int i = 0; i < H2; ++i) {
+        const float2 z = row[i];
+        re[i] = z.x;
+        im[i] = z.y;
+      }
+      fft_dif_split<L, -1>(re, im, h);  // lane h: Y[2m + h] at bitrev(m)
+      const size_t tb = size_t(ch) * tpc + t0 + q2;
+      // bins (r, v) for v = 2m + h: element (r V + h) fstride + tb + m (2 fstride)
+      auto put = [&](int r, int m, float2 val) {
+        if (O32) {
+          store_at(p.dst, unsigned(((size_t(r) * V + h) * fstride + tb) * 8u) + unsigned(m) * unsigned(2 * fstride * 8u),
+                   val);
+        } else {
+          p.dst[(size_t(r) * V + h) * fstride + tb + size_t(2 * m) * fstride] = val;
+        }
+      };
+      if (u > 0) {
+#pragma unroll
+        for (int m = 0; m <= H2 / 2; ++m) {
+          const int v = 2 * m + h, ps = bitrev(m, H2);
+          if (v <= H2) put(u, m, make_float2(re[ps], im[ps]));
+          if (v >= 1 && v < H2) {
+            const int q0i = bitrev((H2 - m) % H2, H2), q1i = bitrev(H2 - m - 1, H2);
+            const float xr = pick(h, re[q1i], re[q0i]), xi = pick(h, im[q1i], im[q0i]);
+            put(L - u, m, make_float2(xr, -xi));
+          }
+        }
+      } else {
+        // packed row: Y = X[0] + i X[L/2] (both Hermitian in v)
+#pragma unroll
+        for (int m = 0; m <= H2 / 2; ++m) {
+          const int v = 2 * m + h, ps = bitrev(m, H2);
+          if (v > H2) continue;
+          const int q0i = bitrev((H2 - m) % H2, H2), q1i = bitrev((H2 - m - 1 + H2) % H2, H2);
+          const float a = re[ps], b = im[ps];
+          const float c = pick(h, re[q1i], re[q0i]), d = pick(h, im[q1i], im[q0i]);
+          put(0, m, make_float2(0.5f * (a + c), 0.5f * (b - d)));
+          put(H2, m, make_float2(0.5f * (b + d), 0.5f * (c - a)));
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// inverse: half spectra -> kept part of every tile (crop), or the plane the
+// tiles overlap-add to
+//
+// Pass 1 inverts column w of every tile, w < L/2; column 0 carries the real
+// columns 0 and L/2 together as h0[u] + i h1[u] (rows past L/2 rebuilt as the
+// conjugates of rows L - u, which are not stored), so its inverse holds both
+// real columns. Row r of the inverse becomes kept row (r + rot) mod L. Pass 2
+// inverts pairs of kept rows to real rows, written over their own storage;
+// column s becomes kept column (s + rot) mod L.
+template <int L, bool O32, bool PF>
+__global__ void __launch_bounds__((big_threads<L, PF>())) big_irfft2_kernel(BigInvParams p) {
+  constexpr int H2 = Big<L>::H2, V = Big<L>::V, RI = Big<L>::RI;
+  extern __shared__ float smem[];
+  float2* lds = reinterpret_cast<float2*>(smem);
+  const float* ldf = smem;
+  const int KR = p.KR, rot = p.rot;
+  const int TSZ = inv_tile_stride<L>(KR);
+  const int tid = threadIdx.x, nthr = blockDim.x, h = tid & 1;
+  const int P = p.T * p.T, tpc = p.n_img * P;
+  const size_t fstride = size_t(p.n_ch) * tpc;
+  const long ngroups = long(p.n_ch) * p.ngrp;
+  const unsigned nwg = gridDim.x;
+  const int npair = (KR + 1) / 2;
+  const float scale = 1.0f / float(L * L);
+  // tasks of passes 1 and 2: h + 2 (q + TQ w), tile q fastest; w is the
+  // column (pass 1) or the row pair (pass 2). With the prefetch, each thread
+  // has one task per pass (the launcher gives L TQ threads).
+  float zr[H2], zi[H2];
+
+  // Column w of tile q, rows [h L/2, h L/2 + L/2), summed over the split
+  // partial spectra. Bins are read at a lane offset that steps by one row of
+  // bins per element; the offset is made opaque first, so that the addresses
+  // of all elements are not precomputed and kept across the group loop.
+  using off_t = typename std::conditional<O32, unsigned, size_t>::type;
+  auto at = [&](const float2* base, off_t e) { return O32 ? load_at(base, unsigned(e) * 8u) : base[e]; };
+  auto load = [&](int ch, int t0, int q, int w) {
+    const size_t tb = size_t(ch) * tpc + t0 + q;
+    const off_t row = off_t(size_t(V) * fstride);
+#pragma unroll
+    for (int i = 0; i < H2; ++i) {
+      zr[i] = 0.f;
+      zi[i] = 0.f;
+    }
+    for (int sp = 0; sp < p.nsplit; ++sp) {
+      const float2* base = p.src + size_t(sp) * p.split_stride;
+      if (w > 0) {
+        off_t e = off_t((size_t(h) * H2 * V + w) * fstride + tb);
+        if (O32) asm volatile("" : "+v"(e));
+#pragma unroll
+        for (int i = 0; i < H2; ++i) {
+          const float2 z = at(base, e);
+          e += row;
+          zr[i] += z.x;
+          zi[i] += z.y;
+        }
+      } else {
+        // columns 0 and L/2 together: rows u <= L/2 give b0 + i b1; rows
+        // u > L/2 (lane 1, i > 0) conj b0 + i conj b1 of row L - u. Lane 0
+        // walks rows 0, 1, ..., lane 1 rows L/2, L/2 - 1, ...
+        off_t e = off_t(size_t(h) * H2 * V * fstride + tb);
+        if (O32) asm volatile("" : "+v"(e));
+        const off_t half = off_t(size_t(H2) * fstride);
+#pragma unroll
+        for (int i = 0; i < H2; ++i) {
+          const float2 b0 = at(base, e), b1 = at(base, e + half);
+          if (h) e -= row; else e += row;
+          const bool mirror = h && i > 0;
+          zr[i] += mirror ? b0.x + b1.y : b0.x - b1.y;
+          zi[i] += mirror ? b1.x - b0.y : b0.y + b1.x;
+        }
+      }
+    }
+  };
+  // pass 1 of one task: column inverse; row r becomes kept row (r + rot) mod L
+  auto column = [&](int q, int w) {
+    fft_dif_split<L, +1>(zr, zi, h);  // lane h: row 2m + h at bitrev(m)
+    int qo = q * TSZ + w, ro = h + rot;  // opaque: see load
+    asm volatile("" : "+v"(qo), "+v"(ro));
+    float2* bq = lds + qo;
+#pragma unroll
+    for (int m = 0; m < H2; ++m) {
+      const int rr = (2 * m + ro) & (L - 1);
+      if (rr < KR) bq[rr * RI] = make_float2(zr[bitrev(m, H2)], zi[bitrev(m, H2)]);
+    }
+  };
+  // pass 2 of one task: kept rows 2w, 2w + 1 to real rows, written over their
+  // own storage; column s becomes kept column (s + rot) mod L
+  auto rows = [&](int q, int w) {
+    const int r0 = 2 * w;
+    const bool has1 = r0 + 1 < KR;
+    int zo = q * TSZ + r0 * RI, co = h + rot;
+    asm volatile("" : "+v"(zo), "+v"(co));
+    const float2* za = lds + zo;
+    const float2* zb = za + RI;
+    // bin v of a kept row: slot v, bins 0 and L/2 being the parts of slot 0
+    auto row_bin = [&](const float2* z, int v) {
+      const float2 s0 = z[v == H2 ? 0 : v];
+      return v == 0 ? make_float2(s0.x, 0.f) : (v == H2 ? make_float2(s0.y, 0.f) : s0);
+    };
+    float xr[H2], xi[H2];
+    irfft_pair_split<L, PF ? 0 : 8>([&](int v) { return row_bin(za, v); },
+                        [&](int v) { return has1 ? row_bin(zb, v) : make_float2(0.f, 0.f); }, xr, xi, h);
+    float* d0 = smem + 2 * zo;
+#pragma unroll
+    for (int m = 0; m < H2; ++m) {
+      const int cc = (2 * m + co) & (L - 1);
+      if (cc < KR) {
+        d0[cc] = xr[bitrev(m, H2)] * scale;
+        if (has1) d0[2 * RI + cc] = xi[bitrev(m, H2)] * scale;
+      }
+    }
+  };
+
+  const int tq0 = (tid >> 1) % p.TQ, tw0 = (tid >> 1) / p.TQ;  // this thread's first task
+  long g = first_group();
+  if (PF && g < ngroups) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
+    if (tq0 < min(p.TQ, tpc - t0) && tw0 < H2) load(ch, t0, tq0, tw0);
+  }
+  for (; g < ngroups; g += nwg) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
+    const int nq = min(p.TQ, tpc - t0);
+    if (PF) {
+      if (tq0 < nq && tw0 < H2) column(tq0, tw0);
+    } else {
+      for (int task = tid; task < L * p.TQ; task += nthr) {
+        const int q = (task >> 1) % p.TQ, w = (task >> 1) / p.TQ;
+        if (q >= nq) continue;
+        load(ch, t0, q, w);
+        column(q, w);
+      }
+    }
+    __syncthreads();
+    if (PF && g + nwg < ngroups) {  // in flight during passes 2 and 3
+      const long gn = g + nwg;
+      const int chn = int(gn / p.ngrp), t0n = int(gn % p.ngrp) * p.TQ;
+      if (tq0 < min(p.TQ, tpc - t0n) && tw0 < H2) load(chn, t0n, tq0, tw0);
+    }
+    for (int task = tid; task < 2 * npair * p.TQ; task += nthr) {
+      const int q = (task >> 1) % p.TQ, w = (task >> 1) / p.TQ;
+      if (q < nq) rows(q, w);
+    }
+    __syncthreads();
+    const int H = p.H;
+    const int wave = tid >> 6, lane = tid & 63, nwave = nthr >> 6;
+    if (!p.overlap) {
+      // kept KR x KR of every tile to its block: a wave per tile (decoded
+      // once, wave-uniform), lanes over the block in row order
+      const SmallDiv div_k(KR);
+      for (int qq = wave; qq < nq; qq += nwave) {
+        const int t = t0 + qq, img = t / P, pp = t - img * P;
+        const int pr = pp / p.T, qc = pp - pr * p.T;
+        const int nrow = min(KR, H - pr * p.pitch), ncol = min(KR, H - qc * p.pitch);
+        float* oblk = p.dst + ((size_t(img) * p.n_ch + ch) * H + pr * p.pitch) * H + qc * p.pitch;
+        const float* lt = ldf + 2 * qq * TSZ;
+        for (int e = lane; e < KR * nrow; e += 64) {
+          const int rr = div_k(e), cc = e - rr * KR;
+          if (cc < ncol) oblk[rr * H + cc] = lt[2 * rr * RI + cc];
+        }
+      }
+    } else {
+      // the group is one whole plane: output pixel (i, j) is framed pixel
+      // (i + off, j + off), the sum of at most two tiles per side, added in
+      // a fixed order. A wave per output row, lanes over the columns.
+      const int img = t0 / P, T = p.T, b = p.pitch;
+      float* out = p.dst + (size_t(img) * p.n_ch + ch) * H * H;
+      const SmallDiv div_b(b);
+      for (int i = wave; i < H; i += nwave) {
+        const int a = i + p.off, P1 = div_b(a), ra1 = a - P1 * b;
+        // tile rows covering framed row a: P1 (row ra1) and P1 - 1 (row ra1 + b)
+        const bool r1 = P1 < T, r0 = P1 >= 1 && P1 - 1 < T && ra1 + b < KR;
+        const float* l1 = ldf + 2 * (P1 * T * TSZ + ra1 * RI);
+        const float* l0 = ldf + 2 * ((P1 - 1) * T * TSZ + (ra1 + b) * RI);
+        float* orow = out + size_t(i) * H;
+        for (int jx = lane; jx < H; jx += 64) {
+          const int c = jx + p.off, Q1 = div_b(c), ca1 = c - Q1 * b;
+          const bool c1 = Q1 < T, c0 = Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR;
+          const int o1 = Q1 * TSZ * 2 + ca1, o0 = (Q1 - 1) * TSZ * 2 + ca1 + b;
+          float acc = 0.f;
+          if (r0 && c0) acc += l0[o0];
+          if (r0 && c1) acc += l0[o1];
+          if (r1 && c0) acc += l1[o0];
+          if (r1 && c1) acc += l1[o1];
+          orow[jx] = acc;
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+
+int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
+    cached[dev] = cus;
+  }
+  return cached[dev];
+}
+
+// Persistent grid: whole rounds over the 8 XCDs, as many workgroups as are
+// resident (LDS-bound), at most one per group.
+unsigned persistent_grid(long ngroups, size_t lds) {
+  const long per_cu = std::max<long>(1, long(kBigLds / std::max<size_t>(lds, 1)));
+  long nwg = std::min<long>(per_cu * cu_count(), (ngroups + 7) / 8 * 8);
+  nwg = std::max<long>(8, nwg / 8 * 8);
+  return unsigned(nwg);
+}
+
+// tiles per group: runs of eight (64-byte segments of a bin) at L = 64, or
+// whole planes where fewer fit; two at L = 128
+template <int L>
+int group_tiles(int P, long tpc) {
+  int tq = L == 64 ? OAA_BIG_TQ : 2;
+  if (P > 1 && P < tq) tq = P * (tq / P);
+  return int(std::max<long>(1, std::min<long>(tq, tpc)));
+}
+
+template <int L, bool PF>
+hipError_t launch_big_fwd_LP(const BigFwdParams& p, size_t lds, long ngroups, hipStream_t s) {
+  constexpr int V = Big<L>::V;
+  const bool o32 = size_t(L) * V * size_t(p.n_ch) * size_t(p.n_img) * p.T * p.T * 8 < (size_t(1) << 32);
+  auto kern = o32 ? big_rfft2_kernel<L, true, PF> : big_rfft2_kernel<L, false, PF>;
+  const hipError_t e = allow_lds(kern, kBigLds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds)), dim3(L * p.TQ), lds, s, p);
+  return hipGetLastError();
+}
+
+template <int L>
+hipError_t launch_big_fwd_L(BigFwdParams p, hipStream_t s) {
+  if (p.S < 1 || p.S > L || p.T < 1 || p.H < 1 || size_t(p.H) * p.H * 4 >= (size_t(1) << 31))
+    return hipErrorInvalidValue;
+  const int P = p.T * p.T;
+  const long tpc = long(p.n_img) * P;
+  if (tpc < 1 || tpc > 0x7fffffffL) return hipErrorInvalidValue;
+  p.TQ = group_tiles<L>(P, tpc);
+  p.ngrp = int((tpc + p.TQ - 1) / p.TQ);
+  const size_t lds = size_t(fwd_tile_stride<L>()) * p.TQ * 8;
+  // one task per thread (group_tiles keeps L TQ within a workgroup)
+  if (lds > kBigLds || L * p.TQ > big_threads<L, true>()) return hipErrorInvalidConfiguration;
+  const long ngroups = long(p.n_ch) * p.ngrp;
+  if constexpr (L == 64) return launch_big_fwd_LP<L, true>(p, lds, ngroups, s);
+  else return launch_big_fwd_LP<L, false>(p, lds, ngroups, s);
+}
+
+template <int L, bool PF>
+hipError_t launch_big_inv_LP(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
+  constexpr int V = Big<L>::V;
+  const bool o32 =
+      (size_t(L) * V * size_t(p.n_ch) * size_t(p.n_img) * p.T * p.T + size_t(p.nsplit - 1) * p.split_stride) * 8 <
+      (size_t(1) << 32);
+  auto kern = o32 ? big_irfft2_kernel<L, true, PF> : big_irfft2_kernel<L, false, PF>;
+  const hipError_t e = allow_lds(kern, kBigLds);
+  if (e != hipSuccess) return e;
+  const int nthr = std::min(L * p.TQ, big_threads<L, PF>());
+  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds)), dim3(nthr), lds, s, p);
+  return hipGetLastError();
+}
+
+template <int L>
+hipError_t launch_big_inv_L(BigInvParams p, hipStream_t s) {
+  if (p.KR < 1 || p.KR > L || p.rot < 0 || p.rot >= L || p.T < 1 || p.H < 1 || p.nsplit < 1 ||
+      p.H >= 65536 || size_t(p.H) * p.H >= (size_t(1) << 31))
+    return hipErrorInvalidValue;
+  const int P = p.T * p.T;
+  const long tpc = long(p.n_img) * P;
+  if (tpc < 1 || tpc > 0x7fffffffL) return hipErrorInvalidValue;
+  if (p.overlap) {
+    if (P > Big<L>::TQ_MAX || p.pitch < 1 || p.off < 0 || p.H + p.off >= 65536) return hipErrorInvalidValue;
+    p.TQ = P;  // one plane per group
+  } else {
+    if (p.pitch != p.KR) return hipErrorInvalidValue;
+    p.TQ = group_tiles<L>(P, tpc);
+    if (long(p.KR) * p.KR * p.TQ >= 65536) return hipErrorInvalidValue;
+  }
+  p.ngrp = int((tpc + p.TQ - 1) / p.TQ);
+  const size_t lds = size_t(inv_tile_stride<L>(p.KR)) * p.TQ * 8;
+  if (lds > kBigLds) return hipErrorInvalidConfiguration;
+  const long ngroups = long(p.n_ch) * p.ngrp;
+  // the register prefetch needs one task per thread
+  if constexpr (L == 64)
+    if (L * p.TQ <= big_threads<L, true>()) return launch_big_inv_LP<L, true>(p, lds, ngroups, s);
+  return launch_big_inv_LP<L, false>(p, lds, ngroups, s);
+}
+
+}  // namespace
+
+hipError_t launch_big_rfft2(int L, const BigFwdParams& p, hipStream_t s) {
+  switch (L) {
+    case 64: return launch_big_fwd_L<64>(p, s);
+    case 128: return launch_big_fwd_L<128>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_big_irfft2(int L, const BigInvParams& p, hipStream_t s) {
+  switch (L) {
+    case 64: return launch_big_inv_L<64>(p, s);
+    case 128: return launch_big_inv_L<128>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+bool big_overlap_supported(int L, int T) {
+  if (L == 64) return T * T <= Big<64>::TQ_MAX;
+  if (L == 128) return T * T <= Big<128>::TQ_MAX;
+  return false;
+}
+
+}  // namespace oaa

@@ -62,7 +62,7 @@ __device__ __forceinline__ void row_pair_split(const float* row_a, const float* 
     const int p0 = bitrev(m == 0 ? 0 : H - m, H);   // partner of v = 2m (lane 0)
     const int p1 = bitrev(H - 1 - (m < H / 2 ? m : 0), H);  // partner of v = 2m + 1 (lane 1)
     const float a = zr[ps], b = zi[ps];
-    const float c = h ? zr[p1] : zr[p0], d = h ? zi[p1] : zi[p0];
+    const float c = pick(h, zr[p1], zr[p0]), d = pick(h, zi[p1], zi[p0]);
     const int v = 2 * m + h;
     if (h == 0 || m < H / 2) {
       zt[v] = make_float2(0.5f * (a + c), 0.5f * (b - d));

@@ -112,6 +112,46 @@ struct GemmParams {
   bool a_trans, a_conj, b_trans, b_conj;
 };
 
+// Large transform sides (L = 64, 128), k_big_fft.hip. Tiles of one channel
+// are numbered t = img * T * T + P * T + Q; a workgroup transforms TQ
+// consecutive tiles of one channel at a time.
+//
+// Forward: tile t is the S x S window of plane (img, ch) of src whose
+// rows and columns start at P * pitch - off and Q * pitch - off (zero outside
+// the plane), zero-padded to L x L. Kernel spectra are the case T = 1,
+// pitch = S = H (tile t = kernel t).
+struct BigFwdParams {
+  const float* src;  // [n_img][n_ch][H][H]
+  float2* dst;       // [F][n_ch][n_img * T * T]
+  int n_img, n_ch;
+  int H, pitch, off, S, T;
+  int TQ, ngrp;      // tiles per group, groups per channel (launcher)
+};
+
+// Inverse: the (optionally split-summed) spectra of each tile -> L x L
+// inverse transform, row and column r of which become index (r + rot) mod L;
+// indices [0, KR) are kept.
+//  * crop (overlap = 0): kept element (a, c) of tile (img, P, Q) goes to
+//    dst[img][ch][P * pitch + a][Q * pitch + c] (inside the H x H plane);
+//  * overlap-add (overlap = 1): output pixel (i, j) of the H x H plane is the
+//    sum over tiles (P, Q) with 0 <= i + off - P pitch < KR (and likewise in
+//    j) of their kept element (i + off - P pitch, j + off - Q pitch); a group
+//    is a whole plane (TQ = T * T).
+struct BigInvParams {
+  const float2* src;  // [nsplit][F][n_ch][n_img * T * T]
+  int nsplit;
+  size_t split_stride;
+  float* dst;         // [n_img][n_ch][H][H]
+  int n_img, n_ch;
+  int H, pitch, off, T;
+  int KR, rot, overlap;
+  int TQ, ngrp;       // launcher
+};
+hipError_t launch_big_rfft2(int L, const BigFwdParams& p, hipStream_t s);
+hipError_t launch_big_irfft2(int L, const BigInvParams& p, hipStream_t s);
+// Whether launch_big_irfft2 takes an overlap-add of this many tiles per plane.
+bool big_overlap_supported(int L, int T);
+
 hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);
 hipError_t launch_window_rfft2(int L, const WindowParams& p, hipStream_t s);

@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
@@ -25,6 +26,12 @@
 // register-heavy variant).
 #ifndef OAA_BLOCKS_AS_WINDOWS
 #define OAA_BLOCKS_AS_WINDOWS 1
+#endif
+
+// Transform sides from which the tile-group kernels of k_big_fft.hip take
+// every transform (overridable at build time for comparisons).
+#ifndef OAA_BIG_MIN_L
+#define OAA_BIG_MIN_L 64
 #endif
 
 
@@ -154,9 +161,61 @@ oaa_status_t timed(const Ctx& cx, oaa_stage_t stage, const char* what, Fn&& laun
   return OAA_OK;
 }
 
+bool big_side(const oaa_plan_s* p) { return p->L >= OAA_BIG_MIN_L; }
+
+// Forward transform of S x S windows starting every `pitch` at -off in the
+// H x H planes of src (n_img x n_ch of them, T x T windows each) into `dst`.
+oaa_status_t big_forward(const Ctx& cx, oaa_stage_t stage, const char* what, const float* src, float2* dst,
+                         int n_img, int n_ch, int H, int pitch, int off, int S, int T) {
+  oaa::BigFwdParams b{};
+  b.src = src;
+  b.dst = dst;
+  b.n_img = n_img;
+  b.n_ch = n_ch;
+  b.H = H;
+  b.pitch = pitch;
+  b.off = off;
+  b.S = S;
+  b.T = T;
+  return timed(cx, stage, what, [&] { return oaa::launch_big_rfft2(cx.p->L, b, cx.s); });
+}
+
+// Inverse transform of the spectra at src (nsplit partial sums spaced
+// split_stride apart) of n_img x n_ch planes of T x T tiles; row and column r
+// of each inverse become index (r + rot) mod L, of which [0, KR) are kept and
+// either written to block (P, Q) at (P pitch, Q pitch) of the H x H output
+// planes (overlap false) or overlap-added there, pixel (i, j) being framed
+// pixel (i + off, j + off) (overlap true).
+oaa_status_t big_inverse(const Ctx& cx, oaa_stage_t stage, const char* what, const float2* src, int nsplit,
+                         size_t split_stride, float* dst, int n_img, int n_ch, int H, int pitch, int off, int T, int KR,
+                         int rot, bool overlap) {
+  oaa::BigInvParams b{};
+  b.src = src;
+  b.nsplit = nsplit;
+  b.split_stride = split_stride;
+  b.dst = dst;
+  b.n_img = n_img;
+  b.n_ch = n_ch;
+  b.H = H;
+  b.pitch = pitch;
+  b.off = off;
+  b.T = T;
+  b.KR = KR;
+  b.rot = rot;
+  b.overlap = overlap ? 1 : 0;
+  return timed(cx, stage, what, [&] { return oaa::launch_big_irfft2(cx.p->L, b, cx.s); });
+}
+
 oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
   oaa_plan_t p = cx.p;
   hipStream_t s = cx.s;
+  if (big_side(p)) {
+    // kernels as single-tile planes w[k][c]: spectra [F][C][K]
+    oaa_status_t st = big_forward(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", w, region(cx, OAA_REGION_W_SPECTRUM),
+                                  p->K, p->C, p->n, p->n, 0, p->n, 1);
+    if (st == OAA_OK && cx.own) p->w_valid = true;
+    return st;
+  }
   oaa::TileFwdParams t{};
   t.src = w;
   t.dst = region(cx, OAA_REGION_W_SPECTRUM);
@@ -177,6 +236,15 @@ oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
 oaa_status_t run_input_fft(const Ctx& cx, const float* x) {
   oaa_plan_t p = cx.p;
   hipStream_t s = cx.s;
+  if (big_side(p)) {
+    // overlap-save: L x L windows every h; overlap-add: b x b blocks
+    const bool oas = p->method == OAA_METHOD_OVERLAP_SAVE;
+    oaa_status_t st = big_forward(cx, OAA_STAGE_X_SPECTRUM, oas ? "input window spectra" : "input block spectra", x,
+                                  region(cx, OAA_REGION_X_SPECTRUM), p->B, p->C, p->N, p->b, 0, oas ? p->L : p->b,
+                                  p->T);
+    if (st == OAA_OK && cx.own) p->x_valid = true;
+    return st;
+  }
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // L x L windows of x starting every h = L - n + 1
     oaa::WindowParams t{};
@@ -230,6 +298,16 @@ oaa_status_t run_input_fft(const Ctx& cx, const float* x) {
 oaa_status_t run_grad_fft(const Ctx& cx, const float* g) {
   oaa_plan_t p = cx.p;
   hipStream_t s = cx.s;
+  if (big_side(p)) {
+    // overlap-save: h x h blocks of g; overlap-add: windows of side
+    // min(2b, L) of the gradient framed by n - 1 zeros, every b
+    const bool oas = p->method == OAA_METHOD_OVERLAP_SAVE;
+    oaa_status_t st = big_forward(cx, OAA_STAGE_G_SPECTRUM, oas ? "gradient block spectra" : "gradient window spectra",
+                                  g, region(cx, OAA_REGION_G_SPECTRUM), p->B, p->K, p->M, p->b,
+                                  oas ? 0 : p->n - 1, oas ? p->b : std::min(2 * p->b, p->L), p->T);
+    if (st == OAA_OK && cx.own) p->g_valid = true;
+    return st;
+  }
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // h x h blocks of g, h = L - n + 1
     oaa_status_t st;
@@ -307,11 +385,13 @@ oaa_status_t run_gemm(const Ctx& cx, oaa::GemmParams& g, oaa_stage_t stage, cons
 // [max(1, n-1), L-n+1]. Per tile: the contraction, 8 C K flops per computed
 // bin, and four transforms per channel pair (input, gradient window, two
 // inverses), about 2.5 L^2 log2(L^2) flops each on the vector units, weighted
-// 4x against the matrix cores, and a further 1.5x at L = 32 and 3x at L = 64
-// (register-resident transforms of those sides run at lower occupancy, as
-// measured); blocks over L/2 add half a transform (the forward inverse then
-// transforms the columns of the block row above too). Ties go to the smaller
-// L.
+// 4x against the matrix cores, and a further 1.5x at L = 32 and L = 64
+// (calibrated against the measured stage times of the large-kernel layer:
+// one lane per transform at L = 32, tile-group kernels at L = 64); blocks
+// over L/2 add half a transform (the forward inverse then transforms the
+// columns of the block row above too). This is a fixed calibration, not a
+// measured search. Ties go to the smaller L, and at one L to the larger
+// block (same tile count, fewer zeros).
 void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   (void)B;
   const int L0 = pow2_at_least(2 * n - 1);
@@ -321,10 +401,10 @@ void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
     int lg = 0;
     while ((1 << lg) < Lc) ++lg;
-    const double eff = Lc <= 16 ? 1.0 : (Lc == 32 ? 1.5 : 3.0);
+    const double eff = Lc <= 16 ? 1.0 : 1.5;
     const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg);
     const double con = 8.0 * C * K * oaa::unique_bins(Lc);
-    for (int bc = (n > 1 ? n - 1 : 1); bc + n - 1 <= Lc; ++bc) {
+    for (int bc = Lc - n + 1; bc >= (n > 1 ? n - 1 : 1); --bc) {
       const double T = double((N + bc - 1) / bc);
       const double f = 2 * bc <= Lc ? fft : fft * 1.125;
       const double cost = T * T * (con + f) * (Lc > L0 ? 1.1 : 1.0);
@@ -348,7 +428,7 @@ int choose_oas_side(int C, int K, int N, int n) {
   for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
     int lg = 0;
     while ((1 << lg) < Lc) ++lg;
-    const double eff = Lc <= 16 ? 1.0 : (Lc == 32 ? 1.5 : 3.0);
+    const double eff = Lc <= 16 ? 1.0 : 1.5;
     const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg) * 1.125;
     const double con = 8.0 * C * K * oaa::unique_bins(Lc);
     const double T = double((M + (Lc - n + 1) - 1) / (Lc - n + 1));
@@ -382,6 +462,13 @@ oaa_status_t forward_pass(const Ctx& cx, const float* x, const float* w, float* 
   g.nsplit = 1; g.kchunk = p->C; g.c_sstride = 0;
   g.a_trans = true; g.a_conj = false; g.b_trans = false; g.b_conj = false;
   if ((st = run_gemm(cx, g, OAA_STAGE_FWD_PRODUCT, "forward contraction"))) return st;
+  if (big_side(p) && p->method == OAA_METHOD_OVERLAP_SAVE)
+    return big_inverse(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-save crop",
+                       region(cx, OAA_REGION_PRODUCT), 1, 0, y, p->B, p->K, p->M, p->b, 0, p->T, p->b,
+                       (p->L - (p->n - 1)) & (p->L - 1), false);
+  if (big_side(p) && oaa::big_overlap_supported(p->L, p->T))
+    return big_inverse(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-add", region(cx, OAA_REGION_PRODUCT),
+                       1, 0, y, p->B, p->K, p->M, p->b, p->n - 1, p->T, p->b + p->n - 1, 0, true);
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // rows and columns [n-1, L) of each window's inverse are its h x h outputs
     oaa::CropParams c{};
@@ -431,6 +518,12 @@ oaa_status_t backward_data_pass(const Ctx& cx, const float* g, const float* w, f
   gm.nsplit = 1; gm.kchunk = p->K; gm.c_sstride = 0;
   gm.a_trans = false; gm.a_conj = true; gm.b_trans = false; gm.b_conj = false;
   if ((st = run_gemm(cx, gm, OAA_STAGE_BWD_DATA_PRODUCT, "backward-data contraction"))) return st;
+  if (big_side(p) && p->method != OAA_METHOD_OVERLAP_SAVE)
+    return big_inverse(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + block crop", region(cx, OAA_REGION_PRODUCT),
+                       1, 0, dx, p->B, p->C, p->N, p->b, 0, p->T, p->b, 0, false);
+  if (big_side(p) && oaa::big_overlap_supported(p->L, p->T))
+    return big_inverse(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + overlap-add",
+                       region(cx, OAA_REGION_PRODUCT), 1, 0, dx, p->B, p->C, p->N, p->b, 0, p->T, p->L, p->n - 1, true);
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
     // overlap-add of the gradient blocks' results into dx. The contraction
     // used conj(W): each inverse is a circular correlation with support
@@ -480,6 +573,13 @@ oaa_status_t backward_filter_pass(const Ctx& cx, const float* x, const float* g,
   gm.c_sstride = (size_t)p->F * p->C * p->K;
   gm.a_trans = false; gm.a_conj = true; gm.b_trans = true; gm.b_conj = false;
   if ((st = run_gemm(cx, gm, OAA_STAGE_BWD_FILTER_PRODUCT, "backward-filter contraction"))) return st;
+  // overlap-save: the windows carry the conjugate, so dw[u][v] sits at rows
+  // and columns (h + u) mod L of the inverse
+  const int origin = p->method == OAA_METHOD_OVERLAP_SAVE ? p->b & (p->L - 1) : 0;
+  if (big_side(p))
+    return big_inverse(cx, OAA_STAGE_BWD_FILTER_INVERSE, "inverse transform of weight gradient",
+                       region(cx, OAA_REGION_PRODUCT), p->split, (size_t)p->F * p->C * p->K, dw, p->K, p->C, p->n,
+                       p->n, 0, 1, p->n, (p->L - origin) & (p->L - 1), false);
   oaa::CropParams c{};
   c.src = region(cx, OAA_REGION_PRODUCT);
   c.nsplit = p->split;
@@ -487,9 +587,7 @@ oaa_status_t backward_filter_pass(const Ctx& cx, const float* x, const float* g,
   c.dst = dw;
   c.n_img = p->K; c.n_ch = p->C;   // spectra [F][C][K], output planes dw[k][c]
   c.H = p->n; c.n = p->n; c.T = 1;
-  // overlap-save: the windows carry the conjugate, so dw[u][v] sits at rows
-  // and columns (h + u) mod L of the inverse
-  c.origin = p->method == OAA_METHOD_OVERLAP_SAVE ? p->b & (p->L - 1) : 0;
+  c.origin = origin;
   return timed(cx, OAA_STAGE_BWD_FILTER_INVERSE, "inverse transform of weight gradient",
                [&] { return oaa::launch_irfft2_crop(p->L, c, s); });
 }

@@ -87,7 +87,7 @@ def test_geometry_of_named_layers(lib, name, expect):
         binding.oaa_plan_destroy(h)
 
 
-@pytest.mark.parametrize("name,L,b", [("tiny", 16, 11), ("mid56", 16, 14), ("first224", 16, 10), ("large128", 32, 16)])
+@pytest.mark.parametrize("name,L,b", [("tiny", 16, 12), ("mid56", 16, 14), ("first224", 16, 10), ("large128", 64, 49)])
 def test_library_tiling_choice(lib, name, L, b):
     """L = b = 0: fewer, larger blocks where that cuts the estimated work."""
     ly = LAYERS[name]

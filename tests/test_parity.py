@@ -147,6 +147,28 @@ def test_tiled_layers_all_passes(gpu_lib, shape):
     check_whole(x, w, g, tiling=(L, b))
 
 
+BIG64 = [  # (B, C, K, N, n, L, b, method): transform side 64 through the tile-group kernels
+    (2, 16, 24, 128, 16, 64, 49, "oaa"),   # the large-kernel layer's blocks of 49, reduced: T = 3
+    (1, 3, 5, 100, 16, 64, 40, "oaa"),     # T = 3, ragged last block row and column
+    (2, 2, 3, 70, 16, 64, 49, "oaa"),      # T = 2
+    (3, 2, 2, 45, 7, 64, 58, "oaa"),       # one block per plane (FFTconv-like)
+    (1, 4, 3, 150, 20, 64, 40, "oaa"),     # T = 4: forward overlap-add through the per-row kernels
+    (1, 2, 3, 200, 32, 64, 32, "oaa"),     # the paper's tiling at n = 32: T = 7, frequency-domain fold
+    (2, 3, 17, 60, 9, 64, 56, "oaa"),      # odd channel and kernel counts, partial groups
+    (2, 5, 6, 100, 20, 64, 0, "oas"),      # overlap-save: h = 45, T = 2
+    (1, 3, 4, 120, 10, 64, 0, "oas"),      # overlap-save: h = 55, T = 3
+]
+
+
+@pytest.mark.parametrize("shape", BIG64, ids=lambda s: "x".join(map(str, s)))
+def test_transform_side_64(gpu_lib, shape):
+    """Every pass at L = 64 against the oracle, compared whole."""
+    B, C, K, N, n, L, b, method = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=71 + sum(shape[:7]))
+    m = binding.METHOD_OVERLAP_SAVE if method == "oas" else binding.METHOD_OVERLAP_ADD
+    check_whole(x, w, g, tiling=(L, b), method=m)
+
+
 FOLD_RUNS = [  # (B, C, K, N, n, L): blocks of L/2, where the forward inverse takes several
     # whole block rows per workgroup (runs of consecutive tiles)
     (2, 3, 512, 64, 5, 32),    # T = 4: four block rows per workgroup

@@ -56,7 +56,7 @@ typedef struct oaa_plan_s* oaa_plan_t;
 typedef enum {
   OAA_OK = 0,
   OAA_ERR_INVALID_ARG = 1,   /* bad dimension, NULL pointer, unknown enum   */
-  OAA_ERR_UNSUPPORTED = 2,   /* valid but outside this library (n > 32)      */
+  OAA_ERR_UNSUPPORTED = 2,   /* valid but outside this library (n > 64)      */
   OAA_ERR_NO_WORKSPACE = 3,  /* no workspace bound, or the one bound is too small */
   OAA_ERR_NO_CACHE = 4,      /* a NULL input asks for a spectrum not yet computed */
   OAA_ERR_HIP = 5            /* the HIP runtime reported an error             */
@@ -140,8 +140,9 @@ typedef enum {
  * (Section 2: blocks of the kernel's size, b = n; transform side L the
  * smallest power of two >= 2n - 1, Sections 3.2-3.3). Host-only: makes no
  * HIP call and allocates no device memory. Requires B, C, K >= 1 and
- * 1 <= n <= N (else OAA_ERR_INVALID_ARG); n <= 32 and element counts within
- * 2^31 blocks per spectrum row (else OAA_ERR_UNSUPPORTED). On success *plan
+ * 1 <= n <= N (else OAA_ERR_INVALID_ARG); n <= 64 (transform sides up to
+ * 128) and element counts within 2^31 blocks per spectrum row (else
+ * OAA_ERR_UNSUPPORTED). On success *plan
  * is set; on failure *plan is set to NULL. */
 oaa_status_t oaa_plan_create(oaa_plan_t* plan, int B, int C, int K, int N, int n);
 
@@ -149,16 +150,17 @@ oaa_status_t oaa_plan_create(oaa_plan_t* plan, int B, int C, int K, int N, int n
  * then have support b + n - 1 and the result is the same convolution for any
  * b with max(1, n-1) <= b <= L - n + 1 (up to L/2 the forward overlap-add is
  * done on the spectra; above, after the inverse). L must be a power of two
- * in [2, 64] (else OAA_ERR_UNSUPPORTED); a b outside that range is
+ * in [2, 128] (else OAA_ERR_UNSUPPORTED); a b outside that range is
  * OAA_ERR_INVALID_ARG.
- * L = b = 0 lets the library choose: L in {L0, 2 L0} (L0 the paper's side)
+ * L = b = 0 lets the library choose: L in {L0, 2 L0} up to 64, or L0 = 128
+ * (L0 the paper's side)
  * and b by a work estimate of contraction and transforms. Larger blocks
  * mean fewer tiles: fewer spectra to transform, store and contract. */
 oaa_status_t oaa_plan_create_tiled(oaa_plan_t* plan, int B, int C, int K, int N, int n, int L, int b);
 
 /* Same, with a choice of method (oaa_method_t). For OAA_METHOD_OVERLAP_ADD
  * this is oaa_plan_create_tiled. For OAA_METHOD_OVERLAP_SAVE, L is a power of
- * two in [max(2, 2n-1 rounded up), 64], or 0 for the library's choice between
+ * two in [max(2, 2n-1 rounded up), 128], or 0 for the library's choice between
  * that side and twice it; b must be 0 or L - n + 1 (the hop). An unknown
  * method is OAA_ERR_INVALID_ARG. */
 oaa_status_t oaa_plan_create_method(oaa_plan_t* plan, int B, int C, int K, int N, int n, int L, int b,
@@ -171,7 +173,9 @@ oaa_status_t oaa_plan_destroy(oaa_plan_t plan);
 /* Copy the plan's derived sizes into *out. */
 oaa_status_t oaa_plan_geometry(oaa_plan_t plan, oaa_geometry_t* out);
 
-/* Device workspace the plan needs, in bytes (0 for a NULL plan). */
+/* Device workspace the plan needs, in bytes (0 for a NULL plan): the four
+ * regions below and, for L = 128 planes of several tiles per side, a scratch
+ * after them that holds the real tile results of the overlap-add. */
 size_t oaa_plan_workspace_bytes(oaa_plan_t plan);
 
 /* Byte offset and size of one workspace region (layouts above). */

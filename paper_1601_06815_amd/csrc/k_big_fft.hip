@@ -361,7 +361,19 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_irfft2_kernel(BigI
     __syncthreads();
     const int H = p.H;
     const int wave = tid >> 6, lane = tid & 63, nwave = nthr >> 6;
-    if (!p.overlap) {
+    if (p.overlap == 2) {
+      // kept KR x KR of every tile to the scratch, tile after tile
+      float* ob = p.tiles + (size_t(ch) * tpc + t0) * KR * KR;
+      const SmallDiv div_k(KR);
+      for (int qq = wave; qq < nq; qq += nwave) {
+        const float* lt = ldf + 2 * qq * TSZ;
+        float* ot = ob + size_t(qq) * KR * KR;
+        for (int e = lane; e < KR * KR; e += 64) {
+          const int rr = div_k(e), cc = e - rr * KR;
+          ot[e] = lt[2 * rr * RI + cc];
+        }
+      }
+    } else if (!p.overlap) {
       // kept KR x KR of every tile to its block: a wave per tile (decoded
       // once, wave-uniform), lanes over the block in row order
       const SmallDiv div_k(KR);
@@ -404,6 +416,40 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_irfft2_kernel(BigI
       }
     }
     __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// overlap-add of tiles kept in the scratch (planes of more tiles than a
+// workgroup holds): output pixel (i, j) of plane (img, ch) is the sum, in a
+// fixed order, of the kept elements of the at most two tiles per side whose
+// kept range covers framed pixel (i + off, j + off). A workgroup per (plane,
+// run of rows), lanes over the columns.
+__global__ void __launch_bounds__(256) overlap_gather_kernel(BigInvParams p, int rows_per_wg, int nrg) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned wg = xcd_local_order(blockIdx.x, gridDim.x);
+  const int rg = int(wg % unsigned(nrg));
+  const unsigned plane = wg / unsigned(nrg);
+  const int img = int(plane / unsigned(p.n_ch)), ch = int(plane % unsigned(p.n_ch));
+  const int H = p.H, T = p.T, b = p.pitch, KR = p.KR, P = T * T;
+  const size_t tile_elems = size_t(KR) * KR;
+  const float* tb = p.tiles + (size_t(ch) * p.n_img * P + size_t(img) * P) * tile_elems;
+  float* out = p.dst + size_t(plane) * H * H;
+  const SmallDiv div_b(b);
+  const int i0 = rg * rows_per_wg, i1 = min(H, i0 + rows_per_wg);
+  for (int i = i0 + wave; i < i1; i += 4) {
+    const int a = i + p.off, P1 = div_b(a), ra1 = a - P1 * b;
+    const bool r1 = P1 < T, r0 = P1 >= 1 && P1 - 1 < T && ra1 + b < KR;
+    for (int jx = lane; jx < H; jx += 64) {
+      const int c = jx + p.off, Q1 = div_b(c), ca1 = c - Q1 * b;
+      const bool c1 = Q1 < T, c0 = Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR;
+      float acc = 0.f;
+      if (r0 && c0) acc += tb[size_t((P1 - 1) * T + Q1 - 1) * tile_elems + (ra1 + b) * KR + ca1 + b];
+      if (r0 && c1) acc += tb[size_t((P1 - 1) * T + Q1) * tile_elems + (ra1 + b) * KR + ca1];
+      if (r1 && c0) acc += tb[size_t(P1 * T + Q1 - 1) * tile_elems + ra1 * KR + ca1 + b];
+      if (r1 && c1) acc += tb[size_t(P1 * T + Q1) * tile_elems + ra1 * KR + ca1];
+      out[size_t(i) * H + jx] = acc;
+    }
   }
 }
 
@@ -490,9 +536,18 @@ hipError_t launch_big_inv_L(BigInvParams p, hipStream_t s) {
   const int P = p.T * p.T;
   const long tpc = long(p.n_img) * P;
   if (tpc < 1 || tpc > 0x7fffffffL) return hipErrorInvalidValue;
+  bool two_step = false;
   if (p.overlap) {
-    if (P > Big<L>::TQ_MAX || p.pitch < 1 || p.off < 0 || p.H + p.off >= 65536) return hipErrorInvalidValue;
-    p.TQ = P;  // one plane per group
+    if (p.pitch < 1 || p.off < 0 || p.H + p.off >= 65536) return hipErrorInvalidValue;
+    if (P <= Big<L>::TQ_MAX) {
+      p.TQ = P;  // one plane per group
+    } else {
+      // keep every tile's KR x KR in the scratch, then add in a second kernel
+      if (!p.tiles || long(p.KR) * p.KR >= 65536) return hipErrorInvalidValue;
+      two_step = true;
+      p.overlap = 2;
+      p.TQ = group_tiles<L>(P, tpc);
+    }
   } else {
     if (p.pitch != p.KR) return hipErrorInvalidValue;
     p.TQ = group_tiles<L>(P, tpc);
@@ -503,9 +558,22 @@ hipError_t launch_big_inv_L(BigInvParams p, hipStream_t s) {
   if (lds > kBigLds) return hipErrorInvalidConfiguration;
   const long ngroups = long(p.n_ch) * p.ngrp;
   // the register prefetch needs one task per thread
-  if constexpr (L == 64)
-    if (L * p.TQ <= big_threads<L, true>()) return launch_big_inv_LP<L, true>(p, lds, ngroups, s);
-  return launch_big_inv_LP<L, false>(p, lds, ngroups, s);
+  hipError_t e = hipSuccess;
+  if constexpr (L == 64) {
+    if (L * p.TQ <= big_threads<L, true>())
+      e = launch_big_inv_LP<L, true>(p, lds, ngroups, s);
+    else
+      e = launch_big_inv_LP<L, false>(p, lds, ngroups, s);
+  } else {
+    e = launch_big_inv_LP<L, false>(p, lds, ngroups, s);
+  }
+  if (e != hipSuccess || !two_step) return e;
+  // second step: about 8 rows per workgroup
+  const int rows = 8, nrg = (p.H + rows - 1) / rows;
+  const long nwg = long(p.n_img) * p.n_ch * nrg;
+  if (nwg > 0x7fffffffL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(overlap_gather_kernel, dim3(unsigned(nwg)), dim3(256), 0, s, p, rows, nrg);
+  return hipGetLastError();
 }
 
 }  // namespace

@@ -135,13 +135,17 @@ struct BigFwdParams {
 //    dst[img][ch][P * pitch + a][Q * pitch + c] (inside the H x H plane);
 //  * overlap-add (overlap = 1): output pixel (i, j) of the H x H plane is the
 //    sum over tiles (P, Q) with 0 <= i + off - P pitch < KR (and likewise in
-//    j) of their kept element (i + off - P pitch, j + off - Q pitch); a group
-//    is a whole plane (TQ = T * T).
+//    j) of their kept element (i + off - P pitch, j + off - Q pitch). Where a
+//    plane's tiles fit one workgroup (big_overlap_supported) a group is a
+//    whole plane; otherwise the kept KR x KR of every tile goes to `tiles`
+//    ([n_ch][n_img T T][KR][KR] floats, overlap_tile_bytes) and a second
+//    kernel adds them.
 struct BigInvParams {
   const float2* src;  // [nsplit][F][n_ch][n_img * T * T]
   int nsplit;
   size_t split_stride;
   float* dst;         // [n_img][n_ch][H][H]
+  float* tiles;       // overlap-add scratch for planes of many tiles (or NULL)
   int n_img, n_ch;
   int H, pitch, off, T;
   int KR, rot, overlap;
@@ -149,8 +153,13 @@ struct BigInvParams {
 };
 hipError_t launch_big_rfft2(int L, const BigFwdParams& p, hipStream_t s);
 hipError_t launch_big_irfft2(int L, const BigInvParams& p, hipStream_t s);
-// Whether launch_big_irfft2 takes an overlap-add of this many tiles per plane.
+// Whether launch_big_irfft2 overlap-adds planes of T x T tiles in one
+// workgroup (else it needs the `tiles` scratch).
 bool big_overlap_supported(int L, int T);
+// Bytes of that scratch for n_planes planes of T x T tiles keeping KR x KR.
+inline size_t overlap_tile_bytes(long n_planes, int T, int KR) {
+  return size_t(n_planes) * T * T * KR * KR * 4;
+}
 
 hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);

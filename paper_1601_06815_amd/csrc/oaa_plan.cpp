@@ -54,6 +54,8 @@ struct oaa_plan_s {
   int split, kchunk;
   size_t off[4];
   size_t size[4];
+  size_t tiles_off;  // overlap-add scratch after the regions (0 bytes if unused)
+  size_t tiles_size;
   size_t ws_bytes;
   char* ws;
   size_t ws_bound;
@@ -91,6 +93,8 @@ oaa_status_t fail(oaa_status_t st, const char* fmt, ...) {
 
 constexpr size_t kAlign = 256;
 constexpr unsigned long long kMaxElems = 1ull << 60;
+constexpr int kMaxSide = 128;   // largest transform side
+constexpr int kMaxKernel = 64;  // largest kernel side (2n - 1 <= kMaxSide)
 constexpr long long kMaxInt = 0x7fffffffll;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -194,6 +198,7 @@ oaa_status_t big_inverse(const Ctx& cx, oaa_stage_t stage, const char* what, con
   b.nsplit = nsplit;
   b.split_stride = split_stride;
   b.dst = dst;
+  b.tiles = cx.p->tiles_size ? reinterpret_cast<float*>(cx.ws + cx.p->tiles_off) : nullptr;
   b.n_img = n_img;
   b.n_ch = n_ch;
   b.H = H;
@@ -398,10 +403,10 @@ void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   double best = 0;
   L = L0;
   b = n;
-  for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
+  for (int Lc = L0; Lc <= (L0 > 64 ? L0 : 64) && Lc <= 2 * L0; Lc *= 2) {
     int lg = 0;
     while ((1 << lg) < Lc) ++lg;
-    const double eff = Lc <= 16 ? 1.0 : 1.5;
+    const double eff = Lc <= 16 ? 1.0 : (Lc <= 64 ? 1.5 : 3.0);
     const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg);
     const double con = 8.0 * C * K * oaa::unique_bins(Lc);
     for (int bc = Lc - n + 1; bc >= (n > 1 ? n - 1 : 1); --bc) {
@@ -425,10 +430,10 @@ int choose_oas_side(int C, int K, int N, int n) {
   const int M = N - n + 1;
   double best = 0;
   int L = L0;
-  for (int Lc = L0; Lc <= 64 && Lc <= 2 * L0; Lc *= 2) {
+  for (int Lc = L0; Lc <= (L0 > 64 ? L0 : 64) && Lc <= 2 * L0; Lc *= 2) {
     int lg = 0;
     while ((1 << lg) < Lc) ++lg;
-    const double eff = Lc <= 16 ? 1.0 : 1.5;
+    const double eff = Lc <= 16 ? 1.0 : (Lc <= 64 ? 1.5 : 3.0);
     const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg) * 1.125;
     const double con = 8.0 * C * K * oaa::unique_bins(Lc);
     const double T = double((M + (Lc - n + 1) - 1) / (Lc - n + 1));
@@ -466,7 +471,7 @@ oaa_status_t forward_pass(const Ctx& cx, const float* x, const float* w, float* 
     return big_inverse(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-save crop",
                        region(cx, OAA_REGION_PRODUCT), 1, 0, y, p->B, p->K, p->M, p->b, 0, p->T, p->b,
                        (p->L - (p->n - 1)) & (p->L - 1), false);
-  if (big_side(p) && oaa::big_overlap_supported(p->L, p->T))
+  if (big_side(p) && (oaa::big_overlap_supported(p->L, p->T) || p->L > 64))
     return big_inverse(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-add", region(cx, OAA_REGION_PRODUCT),
                        1, 0, y, p->B, p->K, p->M, p->b, p->n - 1, p->T, p->b + p->n - 1, 0, true);
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
@@ -521,7 +526,7 @@ oaa_status_t backward_data_pass(const Ctx& cx, const float* g, const float* w, f
   if (big_side(p) && p->method != OAA_METHOD_OVERLAP_SAVE)
     return big_inverse(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + block crop", region(cx, OAA_REGION_PRODUCT),
                        1, 0, dx, p->B, p->C, p->N, p->b, 0, p->T, p->b, 0, false);
-  if (big_side(p) && oaa::big_overlap_supported(p->L, p->T))
+  if (big_side(p) && (oaa::big_overlap_supported(p->L, p->T) || p->L > 64))
     return big_inverse(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + overlap-add",
                        region(cx, OAA_REGION_PRODUCT), 1, 0, dx, p->B, p->C, p->N, p->b, 0, p->T, p->L, p->n - 1, true);
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
@@ -645,7 +650,7 @@ const char* oaa_status_string(oaa_status_t status) {
 const char* oaa_last_error_detail(void) { return g_detail.c_str(); }
 
 oaa_status_t oaa_plan_create(oaa_plan_t* out, int B, int C, int K, int N, int n) {
-  if (n >= 1 && n <= 32) return oaa_plan_create_tiled(out, B, C, K, N, n, pow2_at_least(2 * n - 1), n);
+  if (n >= 1 && n <= kMaxKernel) return oaa_plan_create_tiled(out, B, C, K, N, n, pow2_at_least(2 * n - 1), n);
   return oaa_plan_create_tiled(out, B, C, K, N, n, 0, 0);
 }
 
@@ -662,14 +667,15 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   if (B < 1 || C < 1 || K < 1 || N < 1 || n < 1)
     return fail(OAA_ERR_INVALID_ARG, "dimensions must be positive (B=%d C=%d K=%d N=%d n=%d)", B, C, K, N, n);
   if (n > N) return fail(OAA_ERR_INVALID_ARG, "kernel side n=%d exceeds input side N=%d", n, N);
-  if (n > 32) return fail(OAA_ERR_UNSUPPORTED, "kernel side n=%d > 32 (transform side would exceed 64)", n);
+  if (n > kMaxKernel)
+    return fail(OAA_ERR_UNSUPPORTED, "kernel side n=%d > %d (transform side would exceed %d)", n, kMaxKernel, kMaxSide);
   if (L < 0 || b < 0) return fail(OAA_ERR_INVALID_ARG, "negative tiling (L=%d b=%d)", L, b);
   const int M = N - n + 1;
   int T = 0;
   if (method == OAA_METHOD_OVERLAP_SAVE) {
     if (L == 0) L = choose_oas_side(C, K, N, n);
-    if (L < 2 || L > 64 || (L & (L - 1)))
-      return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
+    if (L < 2 || L > kMaxSide || (L & (L - 1)))
+      return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, %d]", L, kMaxSide);
     if (L < 2 * n - 1)
       return fail(OAA_ERR_INVALID_ARG, "overlap-save needs L >= 2n-1 (n=%d, L=%d)", n, L);
     if (b != 0 && b != L - n + 1)
@@ -682,8 +688,8 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
     } else if (L == 0 || b == 0) {
       return fail(OAA_ERR_INVALID_ARG, "give both L and b, or neither (L=%d b=%d)", L, b);
     }
-    if (L < 2 || L > 64 || (L & (L - 1)))
-      return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, 64]", L);
+    if (L < 2 || L > kMaxSide || (L & (L - 1)))
+      return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, %d]", L, kMaxSide);
     // block results (support b + n - 1) must fit the transform and may only
     // reach the next block
     if (b < (n > 1 ? n - 1 : 1) || b + n - 1 > L)
@@ -746,6 +752,16 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   for (int r = 0; r < 4; ++r) {
     p->off[r] = off;
     off = align_up(off + p->size[r]);
+  }
+  // scratch of the overlap-add passes (the forward pass with overlap-add,
+  // error propagation with overlap-save) whose planes hold more tiles than
+  // one workgroup keeps, where no other kernel exists (L > 64)
+  p->tiles_off = off;
+  p->tiles_size = 0;
+  if (L > 64 && !oaa::big_overlap_supported(L, T)) {
+    p->tiles_size = method == OAA_METHOD_OVERLAP_ADD ? oaa::overlap_tile_bytes((long)B * K, T, b + n - 1)
+                                                     : oaa::overlap_tile_bytes((long)B * C, T, L);
+    off = align_up(off + p->tiles_size);
   }
   p->ws_bytes = off;
   p->ws = nullptr;

@@ -103,7 +103,8 @@ def test_library_tiling_choice(lib, name, L, b):
 @pytest.mark.parametrize("dims,status", [
     ((1, 1, 1, 20, 5, 16, 8), 0), ((1, 1, 1, 20, 5, 16, 4), 0), ((1, 1, 1, 20, 5, 16, 3), 1),   # b < n-1
     ((1, 1, 1, 20, 5, 16, 12), 0), ((1, 1, 1, 20, 5, 16, 13), 1),                                # b > L-n+1
-    ((1, 1, 1, 20, 5, 12, 6), 2), ((1, 1, 1, 20, 5, 128, 8), 2), ((1, 1, 1, 20, 1, 4, 4), 0),
+    ((1, 1, 1, 20, 5, 12, 6), 2), ((1, 1, 1, 20, 5, 256, 8), 2), ((1, 1, 1, 20, 5, 128, 8), 0),
+    ((1, 1, 1, 20, 1, 4, 4), 0),
     ((1, 1, 1, 20, 5, 16, 0), 1), ((1, 1, 1, 20, 5, 0, 8), 1), ((1, 1, 1, 20, 1, 2, 1), 0),
     ((1, 1, 1, 20, 5, 0, 0), 0), ((1, 1, 1, 20, 5, -2, 4), 1),
 ])
@@ -122,7 +123,8 @@ def test_tiled_plan_validation(lib, dims, status):
 
 @pytest.mark.parametrize("dims,status", [
     ((0, 1, 1, 8, 3), 1), ((1, 0, 1, 8, 3), 1), ((1, 1, 0, 8, 3), 1), ((1, 1, 1, 0, 1), 1),
-    ((1, 1, 1, 8, 0), 1), ((1, 1, 1, 4, 5), 1), ((1, 1, 1, 64, 33), 2), ((1, 1, 1, 64, 32), 0),
+    ((1, 1, 1, 8, 0), 1), ((1, 1, 1, 4, 5), 1), ((1, 1, 1, 64, 33), 0), ((1, 1, 1, 64, 64), 0),
+    ((1, 1, 1, 80, 65), 2), ((1, 1, 1, 64, 32), 0),
     ((1, 1, 1, 1, 1), 0), ((1 << 20, 1, 1, 4096, 2), 2),
 ])
 def test_plan_create_validation(lib, dims, status):

@@ -169,6 +169,28 @@ def test_transform_side_64(gpu_lib, shape):
     check_whole(x, w, g, tiling=(L, b), method=m)
 
 
+BIG128 = [  # (B, C, K, N, n, L, b, method): transform side 128 (kernel sides up to 64)
+    (1, 2, 3, 64, 33, 128, 33, "oaa"),     # the paper's tiling at n = 33: T = 2, overlap-add in two steps
+    (1, 2, 2, 64, 48, 128, 48, "oaa"),     # T = 2
+    (2, 1, 2, 64, 64, 128, 64, "oaa"),     # n = N = 64: one output pixel, one block
+    (1, 3, 4, 100, 40, 128, 89, "oaa"),    # b = L - n + 1, T = 2, ragged
+    (2, 2, 3, 60, 33, 128, 60, "oaa"),     # one block per plane (FFTconv-like)
+    (1, 5, 6, 90, 20, 128, 60, "oaa"),     # a kernel that would also fit L = 64
+    (8, 40, 36, 64, 33, 128, 33, "oaa"),   # matrix-core contractions (C, K, B P >= 32)
+    (1, 2, 3, 70, 40, 128, 0, "oas"),      # overlap-save, h = 89: one window per plane
+    (1, 2, 2, 150, 33, 128, 0, "oas"),     # overlap-save, h = 96, T = 2: error propagation in two steps
+]
+
+
+@pytest.mark.parametrize("shape", BIG128, ids=lambda s: "x".join(map(str, s)))
+def test_transform_side_128(gpu_lib, shape):
+    """Every pass at L = 128 against the oracle, compared whole."""
+    B, C, K, N, n, L, b, method = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=73 + sum(shape[:7]))
+    m = binding.METHOD_OVERLAP_SAVE if method == "oas" else binding.METHOD_OVERLAP_ADD
+    check_whole(x, w, g, tiling=(L, b), method=m)
+
+
 FOLD_RUNS = [  # (B, C, K, N, n, L): blocks of L/2, where the forward inverse takes several
     # whole block rows per workgroup (runs of consecutive tiles)
     (2, 3, 512, 64, 5, 32),    # T = 4: four block rows per workgroup
@@ -596,8 +618,8 @@ def test_overlap_save_small_layers(gpu_lib, shape, double):
         L *= 2
     if double:
         L *= 2
-    if L > 64:
-        pytest.skip("transform side above 64")
+    if L > 128:
+        pytest.skip("transform side above 128")
     x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=53 + sum(shape))
     check_whole(x, w, g, tiling=(L, 0), method=OAS)
 

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <cstdarg>
+#include <cmath>
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
@@ -29,9 +30,14 @@
 #endif
 
 // Transform sides from which the tile-group kernels of k_big_fft.hip take
-// every transform (overridable at build time for comparisons).
+// every transform, and from which their two-step overlap-add (tile results
+// through a scratch) serves planes of more tiles than a workgroup holds
+// (overridable at build time for comparisons).
 #ifndef OAA_BIG_MIN_L
 #define OAA_BIG_MIN_L 64
+#endif
+#ifndef OAA_TWO_STEP_MIN_L
+#define OAA_TWO_STEP_MIN_L 128
 #endif
 
 
@@ -385,34 +391,42 @@ oaa_status_t run_gemm(const Ctx& cx, oaa::GemmParams& g, oaa_stage_t stage, cons
   });
 }
 
-// Tiling with the least estimated work: candidate transform sides L0 (the
-// smallest power of two >= 2n-1) and 2 L0, block pitches b in
-// [max(1, n-1), L-n+1]. Per tile: the contraction, 8 C K flops per computed
-// bin, and four transforms per channel pair (input, gradient window, two
-// inverses), about 2.5 L^2 log2(L^2) flops each on the vector units, weighted
-// 4x against the matrix cores, and a further 1.5x at L = 32 and L = 64
-// (calibrated against the measured stage times of the large-kernel layer:
-// one lane per transform at L = 32, tile-group kernels at L = 64); blocks
-// over L/2 add half a transform (the forward inverse then transforms the
-// columns of the block row above too). This is a fixed calibration, not a
-// measured search. Ties go to the smaller L, and at one L to the larger
-// block (same tile count, fewer zeros).
+// Estimated time (s) of a training step with T x T tiles of side L per
+// plane: the transform stages move every spectrum twice (written by one
+// kernel, read by the next) and the planes once each way, at a rate per
+// transform side that runs of few tiles per plane lower; the contractions
+// run on the matrix cores (C, K >= 32; three products, six flops per complex
+// multiply-add) or stream their spectra (few channels). The rates are a fixed
+// calibration against the measured training steps of the large layers
+// (transform stages at 3.5, 2.5, 2.1 and 1.05 TB/s for L <= 16, 32, 64 and
+// 128; 110 TFLOP/s executed on the matrix cores; 4 TB/s streaming), not a
+// measured search.
+double step_time_estimate(int B, int C, int K, int N, int n, int L, int T) {
+  const double M = N - n + 1, BP = double(B) * T * T, Fu = oaa::unique_bins(L);
+  const double spec = Fu * BP * 8;  // one spectrum channel, bytes
+  const double bytes = 2 * spec * (C + K) + 8.0 * B * (double(C) * N * N + double(K) * M * M);
+  const double rate = (L <= 16 ? 3.5 : L == 32 ? 2.5 : L == 64 ? 2.1 : 1.05) * 1e12;
+  const double runs = std::pow(std::min(1.0, double(T) * T / 16.0), 0.2);
+  double t = bytes / (rate * runs);
+  if (std::min(C, K) >= 32)
+    t += 18.0 * BP * C * K * Fu / 110e12;
+  else
+    t += 5.0 * spec * (C + K) / 4e12;  // X and G spectra read and written by the three products
+  return t;
+}
+
+// Tiling with the least estimated time: transform sides from L0 (the
+// smallest power of two >= 2n-1) up to 64 (or L0 itself when it is 128),
+// block pitches b in [max(1, n-1), L-n+1]. Ties go to the smaller L, and at
+// one L to the larger block (same tile count, fewer zeros).
 void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
-  (void)B;
   const int L0 = pow2_at_least(2 * n - 1);
   double best = 0;
   L = L0;
   b = n;
-  for (int Lc = L0; Lc <= (L0 > 64 ? L0 : 64) && Lc <= 2 * L0; Lc *= 2) {
-    int lg = 0;
-    while ((1 << lg) < Lc) ++lg;
-    const double eff = Lc <= 16 ? 1.0 : (Lc <= 64 ? 1.5 : 3.0);
-    const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg);
-    const double con = 8.0 * C * K * oaa::unique_bins(Lc);
+  for (int Lc = L0; Lc <= std::max(64, L0); Lc *= 2) {
     for (int bc = Lc - n + 1; bc >= (n > 1 ? n - 1 : 1); --bc) {
-      const double T = double((N + bc - 1) / bc);
-      const double f = 2 * bc <= Lc ? fft : fft * 1.125;
-      const double cost = T * T * (con + f) * (Lc > L0 ? 1.1 : 1.0);
+      const double cost = step_time_estimate(B, C, K, N, n, Lc, (N + bc - 1) / bc);
       if (best == 0 || cost < best) {
         best = cost;
         L = Lc;
@@ -422,22 +436,17 @@ void choose_tiling(int B, int C, int K, int N, int n, int& L, int& b) {
   }
 }
 
-// Transform side for the output-tiled method: L0 (the smallest power of two
-// >= 2n-1) or 2 L0, with the work estimate of choose_tiling at the hop
-// L - n + 1 over the output side M.
-int choose_oas_side(int C, int K, int N, int n) {
+// Transform side for the output-tiled method: the side from L0 up to 64 (or
+// L0 = 128) with the least estimated time at the hop L - n + 1 over the
+// output side M.
+int choose_oas_side(int B, int C, int K, int N, int n) {
   const int L0 = pow2_at_least(2 * n - 1);
   const int M = N - n + 1;
   double best = 0;
   int L = L0;
-  for (int Lc = L0; Lc <= (L0 > 64 ? L0 : 64) && Lc <= 2 * L0; Lc *= 2) {
-    int lg = 0;
-    while ((1 << lg) < Lc) ++lg;
-    const double eff = Lc <= 16 ? 1.0 : (Lc <= 64 ? 1.5 : 3.0);
-    const double fft = eff * 4.0 * 2.0 * (C + K) * 2.5 * double(Lc) * Lc * (2 * lg) * 1.125;
-    const double con = 8.0 * C * K * oaa::unique_bins(Lc);
-    const double T = double((M + (Lc - n + 1) - 1) / (Lc - n + 1));
-    const double cost = T * T * (con + fft) * (Lc > L0 ? 1.1 : 1.0);
+  for (int Lc = L0; Lc <= std::max(64, L0); Lc *= 2) {
+    const int h = Lc - n + 1;
+    const double cost = step_time_estimate(B, C, K, N, n, Lc, (M + h - 1) / h);
     if (best == 0 || cost < best) {
       best = cost;
       L = Lc;
@@ -471,7 +480,7 @@ oaa_status_t forward_pass(const Ctx& cx, const float* x, const float* w, float* 
     return big_inverse(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-save crop",
                        region(cx, OAA_REGION_PRODUCT), 1, 0, y, p->B, p->K, p->M, p->b, 0, p->T, p->b,
                        (p->L - (p->n - 1)) & (p->L - 1), false);
-  if (big_side(p) && (oaa::big_overlap_supported(p->L, p->T) || p->L > 64))
+  if (big_side(p) && (oaa::big_overlap_supported(p->L, p->T) || p->L >= OAA_TWO_STEP_MIN_L))
     return big_inverse(cx, OAA_STAGE_FWD_INVERSE, "inverse transform + overlap-add", region(cx, OAA_REGION_PRODUCT),
                        1, 0, y, p->B, p->K, p->M, p->b, p->n - 1, p->T, p->b + p->n - 1, 0, true);
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
@@ -526,7 +535,7 @@ oaa_status_t backward_data_pass(const Ctx& cx, const float* g, const float* w, f
   if (big_side(p) && p->method != OAA_METHOD_OVERLAP_SAVE)
     return big_inverse(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + block crop", region(cx, OAA_REGION_PRODUCT),
                        1, 0, dx, p->B, p->C, p->N, p->b, 0, p->T, p->b, 0, false);
-  if (big_side(p) && (oaa::big_overlap_supported(p->L, p->T) || p->L > 64))
+  if (big_side(p) && (oaa::big_overlap_supported(p->L, p->T) || p->L >= OAA_TWO_STEP_MIN_L))
     return big_inverse(cx, OAA_STAGE_BWD_DATA_INVERSE, "inverse transform + overlap-add",
                        region(cx, OAA_REGION_PRODUCT), 1, 0, dx, p->B, p->C, p->N, p->b, 0, p->T, p->L, p->n - 1, true);
   if (p->method == OAA_METHOD_OVERLAP_SAVE) {
@@ -673,7 +682,7 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   const int M = N - n + 1;
   int T = 0;
   if (method == OAA_METHOD_OVERLAP_SAVE) {
-    if (L == 0) L = choose_oas_side(C, K, N, n);
+    if (L == 0) L = choose_oas_side(B, C, K, N, n);
     if (L < 2 || L > kMaxSide || (L & (L - 1)))
       return fail(OAA_ERR_UNSUPPORTED, "transform side L=%d must be a power of two in [2, %d]", L, kMaxSide);
     if (L < 2 * n - 1)
@@ -755,10 +764,10 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   }
   // scratch of the overlap-add passes (the forward pass with overlap-add,
   // error propagation with overlap-save) whose planes hold more tiles than
-  // one workgroup keeps, where no other kernel exists (L > 64)
+  // one workgroup keeps (from OAA_TWO_STEP_MIN_L; L = 128 has no other kernel)
   p->tiles_off = off;
   p->tiles_size = 0;
-  if (L > 64 && !oaa::big_overlap_supported(L, T)) {
+  if (L >= OAA_TWO_STEP_MIN_L && L >= OAA_BIG_MIN_L && !oaa::big_overlap_supported(L, T)) {
     p->tiles_size = method == OAA_METHOD_OVERLAP_ADD ? oaa::overlap_tile_bytes((long)B * K, T, b + n - 1)
                                                      : oaa::overlap_tile_bytes((long)B * C, T, L);
     off = align_up(off + p->tiles_size);

@@ -8,17 +8,19 @@ Section 3.2 varies the number of kernels for a 32 x 32 one-channel input and
 which is not part of this library; this module reports the time of each pass
 and the direct-convolution-equivalent rate, the shape of those curves.
 
-Kernel sides above 32 need transforms longer than 64 and are skipped; the
-number of kernels of the input-size sweep is not stated and is taken as 100.
+Kernel sides 33 to 64 run at transform side 128. The number of kernels of
+the input-size sweep is not stated and is taken as 100.
 
 --tiling fftconv runs the paper's FFTconv baseline (Section 2): the whole
 plane as a single block, zero-padded to L >= N + n - 1, which the library
 expresses as the tiling (L, L - n + 1) with one block per plane. Planes that
-would need L > 64 are skipped.
+would need L > 128 are skipped.
 
     python -m paper_1601_06815_amd.sweeps [--sweep kernels|ksize|input|all] [--tiling paper|auto|fftconv]
+                                          [--out FILE]
 
-prints one JSON line per configuration.
+prints one JSON line per configuration (and with --out also writes them to
+FILE, after a line giving the command).
 """
 
 import argparse
@@ -35,7 +37,7 @@ def sweep_configs(which):
     if which in ("kernels", "all"):     # Section 3.2: 32 x 32 input, 5 x 5 kernels
         out += [("kernels", 1, 1, K, 32, 5) for K in (25, 50, 100, 200, 300, 400, 500, 600, 750)]
     if which in ("ksize", "all"):       # Section 3.3: 64 x 64 input, 100 kernels
-        out += [("ksize", 1, 1, 100, 64, n) for n in range(1, 33)]
+        out += [("ksize", 1, 1, 100, 64, n) for n in range(1, 65)]
     if which in ("input", "all"):       # Section 3.4: 5 x 5 kernels, sides 4 .. 256
         out += [("input", 1, 1, 100, N, 5) for N in range(8, 257, 8)]
     return out
@@ -43,11 +45,11 @@ def sweep_configs(which):
 
 def fftconv_tiling(N, n):
     """(L, b) of a single block covering the N x N plane, or None if the
-    linear convolution needs a transform longer than 64."""
+    linear convolution needs a transform longer than 128."""
     L = 2
     while L < N + n - 1:
         L *= 2
-    return (L, L - n + 1) if L <= 64 else None
+    return (L, L - n + 1) if L <= 128 else None
 
 
 def time_layer(torch, B, C, K, N, n, tiling, reps):
@@ -88,8 +90,14 @@ def main(argv=None):
     ap.add_argument("--sweep", default="all", choices=["kernels", "ksize", "input", "all"])
     ap.add_argument("--tiling", default="paper", choices=["paper", "auto", "fftconv"])
     ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--out", default=None, help="also write the lines here")
     args = ap.parse_args(argv)
     import torch
+    out = None
+    if args.out:
+        out = open(args.out, "w")
+        out.write("command: python -m paper_1601_06815_amd.sweeps " + " ".join(sys.argv[1:] if argv is None else argv)
+                  + "\n")
     for name, B, C, K, N, n in sweep_configs(args.sweep):
         tiling = args.tiling
         if tiling == "fftconv":
@@ -98,10 +106,16 @@ def main(argv=None):
                 continue
         t, geo, ly = time_layer(torch, B, C, K, N, n, tiling, args.reps)
         direct = ly.direct_flops()
-        print(json.dumps({"sweep": name, "B": B, "C": C, "K": K, "N": N, "n": n, "L": geo["L"], "b": geo["b"],
-                          "fwd_ms": round(t["fwd"], 4), "bwd_ms": round(t["bwd"], 4),
-                          "fwd_direct_tflops": round(direct / t["fwd"] * 1e-9, 4),
-                          "bwd_direct_tflops": round(2 * direct / t["bwd"] * 1e-9, 4)}), flush=True)
+        line = json.dumps({"sweep": name, "B": B, "C": C, "K": K, "N": N, "n": n, "L": geo["L"], "b": geo["b"],
+                           "fwd_ms": round(t["fwd"], 4), "bwd_ms": round(t["bwd"], 4),
+                           "fwd_direct_tflops": round(direct / t["fwd"] * 1e-9, 4),
+                           "bwd_direct_tflops": round(2 * direct / t["bwd"] * 1e-9, 4)})
+        print(line, flush=True)
+        if out:
+            out.write(line + "\n")
+            out.flush()
+    if out:
+        out.close()
     return 0
 
 

@@ -87,7 +87,7 @@ def test_geometry_of_named_layers(lib, name, expect):
         binding.oaa_plan_destroy(h)
 
 
-@pytest.mark.parametrize("name,L,b", [("tiny", 16, 12), ("mid56", 16, 14), ("first224", 16, 10), ("large128", 64, 49)])
+@pytest.mark.parametrize("name,L,b", [("tiny", 16, 12), ("mid56", 16, 14), ("first224", 64, 58), ("large128", 64, 49)])
 def test_library_tiling_choice(lib, name, L, b):
     """L = b = 0: fewer, larger blocks where that cuts the estimated work."""
     ly = LAYERS[name]
@@ -239,7 +239,7 @@ def test_paper_sweep_configurations():
     k = sweep_configs("kernels")
     assert all(c[1:] == (1, 1, c[3], 32, 5) for c in k) and [c[3] for c in k][0] == 25 and k[-1][3] == 750
     s = sweep_configs("ksize")
-    assert [c[5] for c in s] == list(range(1, 33)) and all(c[3:5] == (100, 64) for c in s)
+    assert [c[5] for c in s] == list(range(1, 65)) and all(c[3:5] == (100, 64) for c in s)
     i = sweep_configs("input")
     assert [c[4] for c in i] == list(range(8, 257, 8)) and all(c[5] == 5 for c in i)
     assert len(sweep_configs("all")) == len(k) + len(s) + len(i)

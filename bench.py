@@ -40,7 +40,14 @@ def stage_work(ly, geo):
     8 B P C K F per launch; "flops_exec" is what the matrix-core engine
     executes, 6 real flops per complex multiply-add (Gauss's three real
     products) over the unique_bins(L) bins that are not conjugates of
-    others."""
+    others.
+
+    "bound": the roofline a stage is measured against: the matrix cores for
+    the tiled contractions of many channels (min(C, K) >= 32), HBM for the
+    transforms, the streaming contraction of few channels and the fused
+    few-channel kernels (whose algorithmic bytes are their inputs and
+    outputs: the input or gradient planes, the spectra they read, the
+    planes or partial sums they write)."""
     B, C, K, N, n, M = ly.B, ly.C, ly.K, ly.N, ly.n, ly.M
     F, P, S, L = geo["F"], geo["P"], geo["split"], geo["L"]
     BP = B * P
@@ -50,7 +57,17 @@ def stage_work(ly, geo):
     exec_flops = 6.0 * BP * C * K * Fu
     # the transforms' outputs count the same unique bins (the others are
     # conjugates that no later stage reads)
-    prod = dict(flops=alg_flops, flops_exec=exec_flops)
+    prod = dict(flops=alg_flops, flops_exec=exec_flops, bound="mfma" if min(C, K) >= 32 else "hbm")
+    if geo.get("fused"):
+        fused = dict(flops=alg_flops, flops_exec=exec_flops, bound="hbm")
+        return {
+            "w_spectrum": dict(bytes=K * C * n * n * 4 + Fu * C * K * cplx),
+            "x_spectrum": dict(bytes=B * C * N * N * 4 + Fu * C * BP * cplx),
+            "fwd_inverse": dict(fused, bytes=(Fu * C * BP + Fu * C * K) * cplx + B * K * M * M * 4),
+            "bwd_data_product": dict(fused, bytes=B * K * M * M * 4 + Fu * C * K * cplx + B * C * N * N * 4),
+            "bwd_filter_product": dict(fused, bytes=B * K * M * M * 4 + Fu * C * BP * cplx + S * Fu * C * K * cplx),
+            "bwd_filter_inverse": dict(bytes=S * Fu * C * K * cplx + K * C * n * n * 4),
+        }
     return {
         "w_spectrum": dict(bytes=K * C * n * n * 4 + Fu * C * K * cplx),
         "x_spectrum": dict(bytes=B * C * N * N * 4 + Fu * C * BP * cplx),
@@ -64,6 +81,13 @@ def stage_work(ly, geo):
     }
 
 
+# fused few-channel passes (L = 64): the spectra of w and x by the tile-group
+# transforms, then one fused kernel per pass (and the tile-group inverse of
+# the weight gradient)
+KERNEL_SOURCE_FUSED = {
+    "w_spectrum": "k_big_fft.hip", "x_spectrum": "k_big_fft.hip", "fwd_inverse": "k_fused.hip",
+    "bwd_data_product": "k_fused.hip", "bwd_filter_product": "k_fused.hip", "bwd_filter_inverse": "k_big_fft.hip",
+}
 KERNEL_SOURCE = {
     "w_spectrum": "k_tile_fft.hip", "x_spectrum": "k_tile_fft.hip", "g_spectrum": "k_tile_fft.hip",
     "fwd_inverse": "k_fold_fft.hip", "bwd_data_inverse": "k_tile_fft.hip", "bwd_filter_inverse": "k_tile_fft.hip",
@@ -74,6 +98,10 @@ KERNEL_SOURCE_OAS = dict(KERNEL_SOURCE, fwd_inverse="k_tile_fft.hip", bwd_data_i
 
 
 def kernel_source(geo, stage):
+    if geo.get("fused"):
+        return KERNEL_SOURCE_FUSED[stage]
+    if geo["L"] >= 64 and stage not in ("fwd_product", "bwd_data_product", "bwd_filter_product"):
+        return "k_big_fft.hip"
     return (KERNEL_SOURCE_OAS if geo.get("method") else KERNEL_SOURCE)[stage]
 
 
@@ -360,7 +388,7 @@ def config_report(args):
         # gradient spectra of the two before it
         calls = {"fwd": lambda: plan.forward(xd, wd, y),
                  "bwd_data": lambda: plan.backward_data(gd, None, dx),
-                 "bwd_filter": lambda: plan.backward_filter(None, None, dw)}
+                 "bwd_filter": lambda: plan.backward_filter(None, None if plan.caches_grad_spectra else gd, dw)}
         for pas in ly.passes:
             call = calls[pas]
             for _ in range(3):
@@ -454,7 +482,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--layer", default="large128")
-    ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma", "narrow"])
+    ap.add_argument("--contraction", default="auto", choices=["auto", "valu", "mfma", "narrow", "fused"])
     ap.add_argument("--tiling", default="auto",
                     help="auto: the library's block size (fewer, larger blocks where that cuts work); "
                          "paper: blocks of the kernel's size n; L:b an explicit transform side and block")
@@ -517,7 +545,8 @@ def main():
     x, w, g = make_inputs(ly, seed=0)
     print(f"[bench] inputs for {ly.name} drawn in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
     which = {"auto": binding.CONTRACTION_AUTO, "valu": binding.CONTRACTION_VALU,
-             "mfma": binding.CONTRACTION_MFMA, "narrow": binding.CONTRACTION_NARROW}[args.contraction]
+             "mfma": binding.CONTRACTION_MFMA, "narrow": binding.CONTRACTION_NARROW,
+             "fused": binding.CONTRACTION_FUSED}[args.contraction]
     tiling = args.tiling if args.tiling in ("auto", "paper") else tuple(int(v) for v in args.tiling.split(":"))
     method = binding.METHOD_OVERLAP_SAVE if args.method == "oas" else binding.METHOD_OVERLAP_ADD
     if method == binding.METHOD_OVERLAP_SAVE and isinstance(tiling, tuple):
@@ -532,7 +561,7 @@ def main():
     def step():
         plan.forward(xd, wd, y)
         plan.backward_data(gd, None, dx)
-        plan.backward_filter(None, None, dw)
+        plan.backward_filter(None, None if plan.caches_grad_spectra else gd, dw)
 
     for _ in range(args.warmup):
         step()
@@ -580,7 +609,7 @@ def main():
     dom = max(per_stage, key=lambda k: per_stage[k]["ms_per_launch"] * per_stage[k]["launches"])
     avg_s = per_stage[dom]["ms_per_launch"] * 1e-3
     wk = work[dom]
-    if "flops" in wk:
+    if wk.get("bound") == "mfma":
         achieved = wk["flops"] / avg_s / 1e12
         executed = wk["flops_exec"] / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",

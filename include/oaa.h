@@ -74,6 +74,7 @@ typedef struct {
   int split;  /* partial sums of the weight-gradient contraction             */
   int b;      /* block pitch: blocks are b x b (oaa_plan_create: b = n)      */
   int method; /* oaa_method_t of the plan                                    */
+  int fused;  /* 1 if the passes run fused (OAA_CONTRACTION_FUSED), else 0   */
 } oaa_geometry_t;
 
 /* How the passes are tiled (oaa_plan_create_method).
@@ -111,7 +112,14 @@ typedef enum {
                                 the conjugates of bins (L-u, v), the spectra
                                 being Hermitian there. Nothing reads them: they
                                 are never written here, and the X and G
-                                regions may omit them too. */
+                                regions may omit them too.
+                              With the fused passes (OAA_CONTRACTION_FUSED) the layouts
+                              differ: W holds runs of four kernels, bin-minor
+                              ([ceil(K/4)][C][F][4]); X runs of a block row
+                              ([B*T][C][F][T], block (P, Q) of image b in run b*T + P at
+                              position Q); G and the forward product are never stored;
+                              PRODUCT holds only the weight-gradient partial sums,
+                              [split][F][C][K]. */
 } oaa_region_t;
 
 /* Contraction implementation (the per-bin complex matrix product). */
@@ -119,7 +127,12 @@ typedef enum {
   OAA_CONTRACTION_AUTO = 0,  /* library's choice by shape                        */
   OAA_CONTRACTION_VALU = 1,  /* LDS-tiled FMA on the vector ALUs                 */
   OAA_CONTRACTION_MFMA = 2,  /* fp32 matrix cores                                */
-  OAA_CONTRACTION_NARROW = 3 /* streaming, for C <= 4 input channels only       */
+  OAA_CONTRACTION_NARROW = 3, /* streaming, for C <= 4 input channels only      */
+  OAA_CONTRACTION_FUSED = 4   /* the contraction inside the transform kernels, so
+                                 that the product spectra (forward) and the
+                                 gradient window spectra (both backward passes)
+                                 are never stored: overlap-add plans with L = 64,
+                                 C <= 4 and T <= 8 (the library's choice there) */
 } oaa_contraction_t;
 
 /* Stages of the three passes, for per-stage timing. */
@@ -186,7 +199,10 @@ oaa_status_t oaa_plan_region(oaa_plan_t plan, oaa_region_t region, size_t* offse
  * The memory must stay allocated while calls that use it are in flight. */
 oaa_status_t oaa_plan_bind_workspace(oaa_plan_t plan, void* dev_ptr, size_t bytes);
 
-/* Choose the contraction implementation for later calls. */
+/* Choose the contraction implementation for later calls. OAA_CONTRACTION_FUSED
+ * on a plan that cannot take it is OAA_ERR_UNSUPPORTED. Switching between the
+ * fused and the unfused passes discards the cached spectra (their layouts
+ * differ). */
 oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which);
 
 /* Per-stage timing (the stage breakdown of Section 3.2's overhead
@@ -216,7 +232,8 @@ oaa_status_t oaa_conv_backward_data(oaa_plan_t plan, const float* g, const float
 /* Weight gradient (Section 3.2): dw[K,C,n,n] from x[B,C,N,N] and
  * g[B,K,M,M]. x == NULL reuses the block spectra of the last forward (or
  * backward_filter) call; g == NULL reuses the window spectra of the last
- * backward_data (or backward_filter) call. */
+ * backward_data (or backward_filter) call. The fused passes keep no gradient
+ * spectra: with them g == NULL is OAA_ERR_NO_CACHE. */
 oaa_status_t oaa_conv_backward_filter(oaa_plan_t plan, const float* x, const float* g, float* dw,
                                       void* hip_stream);
 

@@ -11,7 +11,9 @@ stride 1: y = OaAConv2d(x) equals torch's cross-correlation
 
 Spectra cached by a plan belong to the last pass it ran. The backward pass
 reuses the kernel and input spectra of its own forward pass when the plan has
-run nothing since, and recomputes them from the saved tensors otherwise.
+run nothing since (its ``generation`` counter, which every pass of the plan
+advances, is unchanged), and recomputes them from the saved tensors
+otherwise.
 """
 
 import math
@@ -28,7 +30,6 @@ class OaAConv2dFunction(torch.autograd.Function):
     def forward(ctx, x, w, plan):
         x, w = x.contiguous(), w.contiguous()
         y = plan.forward(x, w)
-        plan.generation = getattr(plan, "generation", 0) + 1
         ctx.generation = plan.generation
         ctx.plan = plan
         ctx.save_for_backward(x, w)
@@ -42,11 +43,12 @@ class OaAConv2dFunction(torch.autograd.Function):
         need_x, need_w = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
         if not (need_x or need_w):
             return None, None, None
-        fresh = getattr(plan, "generation", 0) == ctx.generation
+        fresh = plan.generation == ctx.generation
         # both gradients start from the gradient windows transformed here
+        # (which the fused passes do not keep: they transform them again)
         dx = plan.backward_data(gy, None if fresh else w)
-        dw = plan.backward_filter(None if fresh else x, None) if need_w else None
-        plan.generation = getattr(plan, "generation", 0) + 1
+        dw = (plan.backward_filter(None if fresh else x, None if plan.caches_grad_spectra else gy)
+              if need_w else None)
         return (dx if need_x else None), dw, None
 
 

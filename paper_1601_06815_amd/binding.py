@@ -16,7 +16,7 @@ OAA_OK = 0
 STATUS = {0: "OAA_OK", 1: "OAA_ERR_INVALID_ARG", 2: "OAA_ERR_UNSUPPORTED",
           3: "OAA_ERR_NO_WORKSPACE", 4: "OAA_ERR_NO_CACHE", 5: "OAA_ERR_HIP"}
 REGION_W_SPECTRUM, REGION_X_SPECTRUM, REGION_G_SPECTRUM, REGION_PRODUCT = 0, 1, 2, 3
-CONTRACTION_AUTO, CONTRACTION_VALU, CONTRACTION_MFMA, CONTRACTION_NARROW = 0, 1, 2, 3
+CONTRACTION_AUTO, CONTRACTION_VALU, CONTRACTION_MFMA, CONTRACTION_NARROW, CONTRACTION_FUSED = 0, 1, 2, 3, 4
 METHOD_OVERLAP_ADD, METHOD_OVERLAP_SAVE = 0, 1
 STAGES = ["w_spectrum", "x_spectrum", "g_spectrum", "fwd_product", "fwd_inverse",
           "bwd_data_product", "bwd_data_inverse", "bwd_filter_product", "bwd_filter_inverse"]
@@ -27,7 +27,7 @@ _c_int, _c_size, _vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
 
 class Geometry(ctypes.Structure):
     _fields_ = [(k, ctypes.c_int) for k in ("B", "C", "K", "N", "n", "M", "T", "P", "L", "F", "split", "b",
-                                            "method")]
+                                            "method", "fused")]
 
 
 SIGNATURES = {
@@ -177,7 +177,11 @@ def oaa_last_error_detail():
 class Plan:
     """One layer x[B,C,N,N] (*) w[K,C,n,n]; owns a plan handle and a device
     workspace tensor. Calls enqueue on torch's current stream of the tensors'
-    device and return without synchronising."""
+    device and return without synchronising. The workspace is marked as used
+    by every stream a call runs on, so that torch does not hand its memory
+    out again before that work is done once the plan is released.
+    ``generation`` counts the passes that replaced cached spectra (forward,
+    backward_data, backward_filter)."""
 
     def __init__(self, B, C, K, N, n, device="cuda", contraction=CONTRACTION_AUTO, tiling="paper",
                  method=METHOD_OVERLAP_ADD):
@@ -199,11 +203,14 @@ class Plan:
             self.handle = oaa_plan_create_tiled(B, C, K, N, n, L, b)
         self.geometry = oaa_plan_geometry(self.handle)
         self.device = torch.device(device)
+        self.generation = 0
         nbytes = oaa_plan_workspace_bytes(self.handle)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        self._streams = {torch.cuda.current_stream(self.device).cuda_stream}
         oaa_plan_bind_workspace(self.handle, self.workspace.data_ptr(), self.workspace.numel())
         if contraction != CONTRACTION_AUTO:
             oaa_plan_set_contraction(self.handle, contraction)
+            self.geometry = oaa_plan_geometry(self.handle)
 
     def __del__(self):
         h = getattr(self, "handle", None)
@@ -218,6 +225,12 @@ class Plan:
     def output_side(self):
         return self.geometry["M"]
 
+    @property
+    def caches_grad_spectra(self):
+        """Whether backward_filter may take gr=None after backward_data (the
+        fused few-channel passes keep no gradient spectra)."""
+        return not self.geometry["fused"]
+
     def _ptr(self, t, shape, name):
         import torch
         if t is None:
@@ -230,7 +243,11 @@ class Plan:
 
     def _stream(self):
         import torch
-        return torch.cuda.current_stream(self.device).cuda_stream
+        s = torch.cuda.current_stream(self.device)
+        if s.cuda_stream not in self._streams:
+            self.workspace.record_stream(s)
+            self._streams.add(s.cuda_stream)
+        return s.cuda_stream
 
     def _empty(self, shape):
         import torch
@@ -242,6 +259,7 @@ class Plan:
         y = self._empty((B, K, M, M)) if y is None else y
         oaa_conv_forward(self.handle, self._ptr(x, (B, C, N, N), "x"), self._ptr(w, (K, C, n, n), "w"),
                          self._ptr(y, (B, K, M, M), "y"), self._stream())
+        self.generation += 1
         return y
 
     def forward_noalloc(self, x, w, y):
@@ -259,6 +277,7 @@ class Plan:
         dx = self._empty((B, C, N, N)) if dx is None else dx
         oaa_conv_backward_data(self.handle, self._ptr(gr, (B, K, M, M), "g"), self._ptr(w, (K, C, n, n), "w"),
                                self._ptr(dx, (B, C, N, N), "dx"), self._stream())
+        self.generation += 1
         return dx
 
     def backward_filter(self, x, gr, dw=None):
@@ -267,6 +286,7 @@ class Plan:
         dw = self._empty((K, C, n, n)) if dw is None else dw
         oaa_conv_backward_filter(self.handle, self._ptr(x, (B, C, N, N), "x"), self._ptr(gr, (B, K, M, M), "g"),
                                  self._ptr(dw, (K, C, n, n), "dw"), self._stream())
+        self.generation += 1
         return dw
 
     def set_timing(self, enable):

@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "liboaa.so")
-SOURCES = ["oaa_plan.cpp", "k_tile_fft.hip", "k_fold_fft.hip", "k_big_fft.hip", "k_cgemm.hip", "k_narrow.hip"]
+SOURCES = ["oaa_plan.cpp", "k_tile_fft.hip", "k_fold_fft.hip", "k_big_fft.hip", "k_fused.hip", "k_cgemm.hip", "k_narrow.hip"]
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 FLAGS = [

@@ -61,6 +61,18 @@ template <int L, bool PF>
 constexpr int big_threads() {
   return L == 64 && !PF ? 576 : 512;
 }
+#ifndef OAA_BIG_INV_PF_BATCH
+#define OAA_BIG_INV_PF_BATCH 0
+#endif
+#ifndef OAA_BIG_INV_PF_THREADS
+#define OAA_BIG_INV_PF_THREADS 512
+#endif
+// the inverse: with the prefetch, nine tiles (a plane of 3 x 3 blocks) at
+// L = 64 take 576 threads
+template <int L, bool PF>
+constexpr int big_inv_threads() {
+  return L == 64 ? (PF ? OAA_BIG_INV_PF_THREADS : 576) : 512;
+}
 
 // LDS per tile (complex elements, odd)
 template <int L>
@@ -99,7 +111,7 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
   const int TSZ = fwd_tile_stride<L>();
   const int tid = threadIdx.x, h = tid & 1;
   const int P = p.T * p.T, tpc = p.n_img * P;
-  const size_t fstride = size_t(p.n_ch) * tpc;
+  const size_t bs = p.bs;
   const long ngroups = long(p.n_ch) * p.ngrp;
   const unsigned nwg = gridDim.x;
   // pass 1: tile q1, columns j and j + L/2, rows [h L/2, h L/2 + L/2); a
@@ -176,14 +188,14 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
         im[i] = z.y;
       }
       fft_dif_split<L, -1>(re, im, h);  // lane h: Y[2m + h] at bitrev(m)
-      const size_t tb = size_t(ch) * tpc + t0 + q2;
-      // bins (r, v) for v = 2m + h: element (r V + h) fstride + tb + m (2 fstride)
+      const int t = t0 + q2;
+      const size_t tb = size_t(ch) * p.cs + size_t(t / p.run) * p.rs + size_t(t % p.run);
+      // bins (r, v) for v = 2m + h: element (r V + h) bs + tb + m (2 bs)
       auto put = [&](int r, int m, float2 val) {
         if (O32) {
-          store_at(p.dst, unsigned(((size_t(r) * V + h) * fstride + tb) * 8u) + unsigned(m) * unsigned(2 * fstride * 8u),
-                   val);
+          store_at(p.dst, unsigned(((size_t(r) * V + h) * bs + tb) * 8u) + unsigned(m) * unsigned(2 * bs * 8u), val);
         } else {
-          p.dst[(size_t(r) * V + h) * fstride + tb + size_t(2 * m) * fstride] = val;
+          p.dst[(size_t(r) * V + h) * bs + tb + size_t(2 * m) * bs] = val;
         }
       };
       if (u > 0) {
@@ -226,7 +238,7 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
 // inverts pairs of kept rows to real rows, written over their own storage;
 // column s becomes kept column (s + rot) mod L.
 template <int L, bool O32, bool PF>
-__global__ void __launch_bounds__((big_threads<L, PF>())) big_irfft2_kernel(BigInvParams p) {
+__global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(BigInvParams p) {
   constexpr int H2 = Big<L>::H2, V = Big<L>::V, RI = Big<L>::RI;
   extern __shared__ float smem[];
   float2* lds = reinterpret_cast<float2*>(smem);
@@ -316,7 +328,7 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_irfft2_kernel(BigI
       return v == 0 ? make_float2(s0.x, 0.f) : (v == H2 ? make_float2(s0.y, 0.f) : s0);
     };
     float xr[H2], xi[H2];
-    irfft_pair_split<L, PF ? 0 : 8>([&](int v) { return row_bin(za, v); },
+    irfft_pair_split<L, PF ? OAA_BIG_INV_PF_BATCH : 8>([&](int v) { return row_bin(za, v); },
                         [&](int v) { return has1 ? row_bin(zb, v) : make_float2(0.f, 0.f); }, xr, xi, h);
     float* d0 = smem + 2 * zo;
 #pragma unroll
@@ -489,7 +501,11 @@ int group_tiles(int P, long tpc) {
 template <int L, bool PF>
 hipError_t launch_big_fwd_LP(const BigFwdParams& p, size_t lds, long ngroups, hipStream_t s) {
   constexpr int V = Big<L>::V;
-  const bool o32 = size_t(L) * V * size_t(p.n_ch) * size_t(p.n_img) * p.T * p.T * 8 < (size_t(1) << 32);
+  // one past the largest element the layout addresses
+  const long tpc = long(p.n_img) * p.T * p.T;
+  const size_t end = size_t(L * V - 1) * p.bs + size_t(p.n_ch - 1) * p.cs + size_t((tpc - 1) / p.run) * p.rs +
+                     size_t(std::min<long>(p.run, tpc));
+  const bool o32 = end * 8 < (size_t(1) << 32);
   auto kern = o32 ? big_rfft2_kernel<L, true, PF> : big_rfft2_kernel<L, false, PF>;
   const hipError_t e = allow_lds(kern, kBigLds);
   if (e != hipSuccess) return e;
@@ -504,6 +520,13 @@ hipError_t launch_big_fwd_L(BigFwdParams p, hipStream_t s) {
   const int P = p.T * p.T;
   const long tpc = long(p.n_img) * P;
   if (tpc < 1 || tpc > 0x7fffffffL) return hipErrorInvalidValue;
+  if (p.run == 0) {
+    p.run = int(tpc);
+    p.rs = 0;
+    p.bs = size_t(p.n_ch) * size_t(tpc);
+    p.cs = size_t(tpc);
+  }
+  if (p.run < 1) return hipErrorInvalidValue;
   p.TQ = group_tiles<L>(P, tpc);
   p.ngrp = int((tpc + p.TQ - 1) / p.TQ);
   const size_t lds = size_t(fwd_tile_stride<L>()) * p.TQ * 8;
@@ -523,7 +546,7 @@ hipError_t launch_big_inv_LP(const BigInvParams& p, size_t lds, long ngroups, hi
   auto kern = o32 ? big_irfft2_kernel<L, true, PF> : big_irfft2_kernel<L, false, PF>;
   const hipError_t e = allow_lds(kern, kBigLds);
   if (e != hipSuccess) return e;
-  const int nthr = std::min(L * p.TQ, big_threads<L, PF>());
+  const int nthr = std::min(L * p.TQ, big_inv_threads<L, PF>());
   hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds)), dim3(nthr), lds, s, p);
   return hipGetLastError();
 }
@@ -560,7 +583,7 @@ hipError_t launch_big_inv_L(BigInvParams p, hipStream_t s) {
   // the register prefetch needs one task per thread
   hipError_t e = hipSuccess;
   if constexpr (L == 64) {
-    if (L * p.TQ <= big_threads<L, true>())
+    if (L * p.TQ <= big_inv_threads<L, true>())
       e = launch_big_inv_LP<L, true>(p, lds, ngroups, s);
     else
       e = launch_big_inv_LP<L, false>(p, lds, ngroups, s);

@@ -120,11 +120,18 @@ struct GemmParams {
 // rows and columns start at P * pitch - off and Q * pitch - off (zero outside
 // the plane), zero-padded to L x L. Kernel spectra are the case T = 1,
 // pitch = S = H (tile t = kernel t).
+//
+// dst layout: element (bin f, ch, tile t) at f bs + ch cs + (t / run) rs +
+// t % run. run = 0 (the launcher's default) is [F][n_ch][n_img T T]; the
+// fused few-channel passes use runs of the T blocks of a block row
+// (run = T, rs = n_ch F T, bs = T, cs = F T) and of four kernels.
 struct BigFwdParams {
   const float* src;  // [n_img][n_ch][H][H]
-  float2* dst;       // [F][n_ch][n_img * T * T]
+  float2* dst;
   int n_img, n_ch;
   int H, pitch, off, S, T;
+  int run;
+  size_t bs, cs, rs;
   int TQ, ngrp;      // tiles per group, groups per channel (launcher)
 };
 
@@ -160,6 +167,49 @@ bool big_overlap_supported(int L, int T);
 inline size_t overlap_tile_bytes(long n_planes, int T, int KR) {
   return size_t(n_planes) * T * T * KR * KR * 4;
 }
+
+// Fused few-channel passes at L = 64 (k_fused.hip): the contraction over
+// C <= kFusedMaxC channels (forward, weight gradient) or over the kernels
+// (error propagation) inside the transform kernels, so that neither the
+// forward product spectra nor the gradient window spectra are stored. Input
+// block spectra come in runs of a block row: element (bin f, channel c, block
+// (P, Q) of image img) at ((img T + P) C + c) F T + f T + Q; kernel spectra
+// in runs of four kernels: (f, c, k) at ((k / 4) C + c) F 4 + f 4 + k % 4
+// (F = 64 * 33 bin positions f = u * 33 + v).
+constexpr int kFusedMaxC = 4;
+struct FusedFwdParams {
+  const float2* xs;  // input block spectra, runs of a block row
+  const float2* ws;  // kernel spectra, runs of four kernels
+  float* y;          // [B][K][M][M]
+  int B, K, M, T, b, KR, off;  // blocks b x b at pitch b, results KR = b + n - 1, off = n - 1
+  int Kg, ngrp;      // output planes per workgroup item, items per image (launcher)
+};
+struct FusedBwdDataParams {
+  const float* g;    // [B][K][M][M]
+  const float2* ws;  // kernel spectra, runs of four kernels
+  float* dx;         // [B][C][N][N]
+  int B, K, N, M, T, b, off, S;  // gradient windows: S x S at (P b - off, Q b - off)
+};
+struct FusedBwdFilterParams {
+  const float* g;     // [B][K][M][M]
+  const float2* xs;   // input block spectra, runs of a block row
+  float2* part;       // [nsplit][F][C][K] partial sums of the weight-gradient spectra
+  int B, K, M, T, b, off, S;
+  int nsplit;         // ranges of block rows
+  int Kf, nkg, rows_per_split;  // launcher
+};
+// Output planes (forward) or kernels (weight gradient) a workgroup item
+// takes for T blocks per side: T x group tiles fit the workgroup's LDS slots
+// (four, or eight for T > 4); 0 if T > 8.
+int fused_group(int T);
+// Ranges of block rows of the fused weight gradient for about `items`
+// workgroup items (kernel groups x ranges); 0 if the layer is not fused.
+int fused_filter_split(int B, int K, int T, int items);
+// Whether the fused passes take an overlap-add layer of this tiling.
+bool fused_supported(int L, int C, int N, int n, int b, int T);
+hipError_t launch_fused_forward(FusedFwdParams p, int C, hipStream_t s);
+hipError_t launch_fused_bwd_data(const FusedBwdDataParams& p, int C, hipStream_t s);
+hipError_t launch_fused_bwd_filter(FusedBwdFilterParams p, int C, hipStream_t s);
 
 hipError_t launch_tile_rfft2(int L, const TileFwdParams& p, hipStream_t s);
 hipError_t launch_irfft2_crop(int L, const CropParams& p, hipStream_t s);

@@ -51,6 +51,15 @@
 #define OAA_SPLIT_TILES 1152
 #endif
 
+// Workgroup items the fused weight gradient aims for (one per CU of a
+// 256-CU device): the kernel groups times the ranges of block rows. Each
+// range is one more partial sum for the inverse to read and add (measured at
+// the 224 x 224 RGB layer: 16 ranges cost its inverse 0.19 ms, 8 ranges
+// 0.09 ms, for the same contraction time).
+#ifndef OAA_FUSED_ITEMS
+#define OAA_FUSED_ITEMS 256
+#endif
+
 struct oaa_plan_s {
   int B, C, K, N, n;
   int method;  // oaa_method_t
@@ -67,6 +76,10 @@ struct oaa_plan_s {
   size_t ws_bound;
   bool w_valid, x_valid, g_valid;
   oaa_contraction_t contraction;
+  // fused few-channel passes: possible for this tiling, in use, and the
+  // ranges of block rows of their weight gradient
+  bool fused_ok, fused;
+  int fsplit;
   // per-stage timing: event pairs recorded around launches
   bool timing;
   std::vector<hipEvent_t> event_pool;
@@ -176,8 +189,13 @@ bool big_side(const oaa_plan_s* p) { return p->L >= OAA_BIG_MIN_L; }
 // Forward transform of S x S windows starting every `pitch` at -off in the
 // H x H planes of src (n_img x n_ch of them, T x T windows each) into `dst`.
 oaa_status_t big_forward(const Ctx& cx, oaa_stage_t stage, const char* what, const float* src, float2* dst,
-                         int n_img, int n_ch, int H, int pitch, int off, int S, int T) {
+                         int n_img, int n_ch, int H, int pitch, int off, int S, int T, int run = 0, size_t bs = 0,
+                         size_t cs = 0, size_t rs = 0) {
   oaa::BigFwdParams b{};
+  b.run = run;
+  b.bs = bs;
+  b.cs = cs;
+  b.rs = rs;
   b.src = src;
   b.dst = dst;
   b.n_img = n_img;
@@ -220,6 +238,14 @@ oaa_status_t big_inverse(const Ctx& cx, oaa_stage_t stage, const char* what, con
 oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
   oaa_plan_t p = cx.p;
   hipStream_t s = cx.s;
+  if (p->fused) {
+    // runs of four kernels: (f, c, k) at ((k / 4) C + c) F 4 + f 4 + k % 4
+    const size_t F = p->F, C = p->C;
+    oaa_status_t st = big_forward(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", w, region(cx, OAA_REGION_W_SPECTRUM),
+                                  p->K, p->C, p->n, p->n, 0, p->n, 1, 4, 4, F * 4, C * F * 4);
+    if (st == OAA_OK && cx.own) p->w_valid = true;
+    return st;
+  }
   if (big_side(p)) {
     // kernels as single-tile planes w[k][c]: spectra [F][C][K]
     oaa_status_t st = big_forward(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", w, region(cx, OAA_REGION_W_SPECTRUM),
@@ -247,6 +273,15 @@ oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
 oaa_status_t run_input_fft(const Ctx& cx, const float* x) {
   oaa_plan_t p = cx.p;
   hipStream_t s = cx.s;
+  if (p->fused) {
+    // runs of a block row: (f, c, block (P, Q) of img) at ((img T + P) C + c) F T + f T + Q
+    const size_t F = p->F, C = p->C, T = p->T;
+    oaa_status_t st = big_forward(cx, OAA_STAGE_X_SPECTRUM, "input block spectra", x,
+                                  region(cx, OAA_REGION_X_SPECTRUM), p->B, p->C, p->N, p->b, 0, p->b, p->T, p->T, T,
+                                  F * T, C * F * T);
+    if (st == OAA_OK && cx.own) p->x_valid = true;
+    return st;
+  }
   if (big_side(p)) {
     // overlap-save: L x L windows every h; overlap-add: b x b blocks
     const bool oas = p->method == OAA_METHOD_OVERLAP_SAVE;
@@ -462,6 +497,16 @@ oaa_status_t forward_pass(const Ctx& cx, const float* x, const float* w, float* 
   oaa_status_t st;
   if (w && (st = run_filter_fft(cx, w))) return st;
   if ((st = run_input_fft(cx, x))) return st;
+  if (p->fused) {
+    oaa::FusedFwdParams f{};
+    f.xs = region(cx, OAA_REGION_X_SPECTRUM);
+    f.ws = region(cx, OAA_REGION_W_SPECTRUM);
+    f.y = y;
+    f.B = p->B; f.K = p->K; f.M = p->M; f.T = p->T; f.b = p->b;
+    f.KR = p->b + p->n - 1; f.off = p->n - 1;
+    return timed(cx, OAA_STAGE_FWD_INVERSE, "fused contraction + inverse transform + overlap-add",
+                 [&] { return oaa::launch_fused_forward(f, p->C, s); });
+  }
   // Yhat[f] (K x BP) = What[f]^T (K x C) * Xhat[f] (C x BP)
   const long BP = (long)p->B * p->P;
   oaa::GemmParams g{};
@@ -517,6 +562,16 @@ oaa_status_t backward_data_pass(const Ctx& cx, const float* g, const float* w, f
   hipStream_t s = cx.s;
   oaa_status_t st;
   if (w && (st = run_filter_fft(cx, w))) return st;
+  if (p->fused) {
+    oaa::FusedBwdDataParams f{};
+    f.g = g;
+    f.ws = region(cx, OAA_REGION_W_SPECTRUM);
+    f.dx = dx;
+    f.B = p->B; f.K = p->K; f.N = p->N; f.M = p->M; f.T = p->T; f.b = p->b;
+    f.off = p->n - 1; f.S = std::min(2 * p->b, p->L);
+    return timed(cx, OAA_STAGE_BWD_DATA_PRODUCT, "fused gradient windows + contraction + inverse transform",
+                 [&] { return oaa::launch_fused_bwd_data(f, p->C, s); });
+  }
   if ((st = run_grad_fft(cx, g))) return st;
   // dXhat[f] (C x BP) = conj(What[f]) (C x K) * Ghat[f] (K x BP)
   const long BP = (long)p->B * p->P;
@@ -571,6 +626,21 @@ oaa_status_t backward_filter_pass(const Ctx& cx, const float* x, const float* g,
   hipStream_t s = cx.s;
   oaa_status_t st;
   if (x && (st = run_input_fft(cx, x))) return st;
+  if (p->fused) {
+    oaa::FusedBwdFilterParams f{};
+    f.g = g;
+    f.xs = region(cx, OAA_REGION_X_SPECTRUM);
+    f.part = region(cx, OAA_REGION_PRODUCT);
+    f.B = p->B; f.K = p->K; f.M = p->M; f.T = p->T; f.b = p->b;
+    f.off = p->n - 1; f.S = std::min(2 * p->b, p->L);
+    f.nsplit = p->fsplit;
+    if ((st = timed(cx, OAA_STAGE_BWD_FILTER_PRODUCT, "fused gradient windows + weight-gradient contraction",
+                    [&] { return oaa::launch_fused_bwd_filter(f, p->C, s); })))
+      return st;
+    return big_inverse(cx, OAA_STAGE_BWD_FILTER_INVERSE, "inverse transform of weight gradient",
+                       region(cx, OAA_REGION_PRODUCT), p->fsplit, (size_t)p->F * p->C * p->K, dw, p->K, p->C, p->n,
+                       p->n, 0, 1, p->n, 0, false);
+  }
   if (g && (st = run_grad_fft(cx, g))) return st;
   // dWhat^T[f] (C x K) = conj(Xhat[f]) (C x BP) * Ghat[f]^T (BP x K), split over BP
   const long BP = (long)p->B * p->P;
@@ -712,7 +782,11 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   if (BP > kMaxInt || (long long)N * N > kMaxInt || (long long)B * C > kMaxInt || (long long)B * K > kMaxInt ||
       (long long)K * C > kMaxInt)
     return fail(OAA_ERR_UNSUPPORTED, "layer too large for 32-bit tile and plane indices");
-  const unsigned long long eW = (unsigned long long)F * C * K;
+  const bool fused_ok = method == OAA_METHOD_OVERLAP_ADD && oaa::fused_supported(L, C, N, n, b, T);
+  int fsplit = 1;
+  if (fused_ok) fsplit = oaa::fused_filter_split(B, K, T, OAA_FUSED_ITEMS);
+  // (the fused layout of the kernel spectra rounds K up to whole runs of four)
+  const unsigned long long eW = (unsigned long long)F * C * (fused_ok ? (K + 3) / 4 * 4 : K);
   const unsigned long long eX = (unsigned long long)F * C * BP;
   const unsigned long long eG = (unsigned long long)F * K * BP;
   if (eX > kMaxElems || eG > kMaxElems || eW > kMaxElems)
@@ -753,6 +827,7 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   p->kchunk = (int)kchunk;
   unsigned long long eProd = eG > eX ? eG : eX;
   if ((unsigned long long)split * eW > eProd) eProd = (unsigned long long)split * eW;
+  if ((unsigned long long)fsplit * F * C * K > eProd) eProd = (unsigned long long)fsplit * F * C * K;
   p->size[OAA_REGION_W_SPECTRUM] = size_t(eW) * 8;
   p->size[OAA_REGION_X_SPECTRUM] = size_t(eX) * 8;
   p->size[OAA_REGION_G_SPECTRUM] = size_t(eG) * 8;
@@ -777,6 +852,8 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   p->ws_bound = 0;
   p->w_valid = p->x_valid = p->g_valid = false;
   p->contraction = OAA_CONTRACTION_AUTO;
+  p->fused_ok = p->fused = fused_ok;
+  p->fsplit = fsplit;
   p->timing = false;
   *out = p;
   return OAA_OK;
@@ -830,8 +907,9 @@ oaa_status_t oaa_plan_geometry(oaa_plan_t plan, oaa_geometry_t* out) {
   out->B = plan->B; out->C = plan->C; out->K = plan->K; out->N = plan->N; out->n = plan->n;
   out->M = plan->M; out->T = plan->T; out->P = plan->P; out->L = plan->L; out->F = plan->F;
   out->b = plan->b;
-  out->split = plan->split;
+  out->split = plan->fused ? plan->fsplit : plan->split;
   out->method = plan->method;
+  out->fused = plan->fused ? 1 : 0;
   return OAA_OK;
 }
 
@@ -863,11 +941,20 @@ oaa_status_t oaa_plan_bind_workspace(oaa_plan_t plan, void* dev_ptr, size_t byte
 oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which) {
   if (oaa_status_t st = check_plan(plan, false)) return st;
   if (which != OAA_CONTRACTION_AUTO && which != OAA_CONTRACTION_VALU && which != OAA_CONTRACTION_MFMA &&
-      which != OAA_CONTRACTION_NARROW)
+      which != OAA_CONTRACTION_NARROW && which != OAA_CONTRACTION_FUSED)
     return fail(OAA_ERR_INVALID_ARG, "unknown contraction %d", (int)which);
   if (which == OAA_CONTRACTION_NARROW && plan->C > oaa::kNarrowMaxC)
     return fail(OAA_ERR_UNSUPPORTED, "the streaming contraction needs C <= %d (plan has C=%d)", oaa::kNarrowMaxC,
                 plan->C);
+  if (which == OAA_CONTRACTION_FUSED && !plan->fused_ok)
+    return fail(OAA_ERR_UNSUPPORTED,
+                "the fused passes need the overlap-add method, L = 64, C <= %d and at most 8 blocks per side "
+                "(plan: method %d, L=%d, C=%d, T=%d)",
+                oaa::kFusedMaxC, plan->method, plan->L, plan->C, plan->T);
+  const bool fused = which == OAA_CONTRACTION_FUSED || (which == OAA_CONTRACTION_AUTO && plan->fused_ok);
+  // the two paths keep their spectra in different layouts
+  if (fused != plan->fused) plan->w_valid = plan->x_valid = plan->g_valid = false;
+  plan->fused = fused;
   plan->contraction = which;
   return OAA_OK;
 }
@@ -892,6 +979,8 @@ oaa_status_t oaa_conv_backward_filter(oaa_plan_t p, const float* x, const float*
   if (oaa_status_t st = check_plan(p, true)) return st;
   if (!dw) return fail(OAA_ERR_INVALID_ARG, "dw must be non-NULL");
   if (!x && !p->x_valid) return fail(OAA_ERR_NO_CACHE, "x is NULL and no input block spectra are cached");
+  if (!g && p->fused)
+    return fail(OAA_ERR_NO_CACHE, "g is NULL: the fused few-channel passes keep no gradient window spectra");
   if (!g && !p->g_valid) return fail(OAA_ERR_NO_CACHE, "g is NULL and no gradient window spectra are cached");
   (void)hipGetLastError();
   return backward_filter_pass(Ctx{p, p->ws, static_cast<hipStream_t>(stream), true}, x, g, dw);

@@ -3,6 +3,10 @@
 
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <set>
+#include <utility>
+
 #include "buffer_io.hpp"
 #include "fft_core.hpp"
 
@@ -85,19 +89,21 @@ constexpr size_t kLdsBudget = 60 * 1024;
 // two workgroups per CU)
 constexpr size_t kLdsRowsBudget = 80 * 1024;
 // Lets a kernel take up to `bytes` of dynamic LDS (beyond 64 KB) on the
-// current device; set once per device.
+// current device; set once per kernel and device (kernels of one signature
+// share the function type, so the record is kept per kernel address).
 template <class Kern>
 hipError_t allow_lds(Kern kern, size_t bytes) {
-  static int done[64] = {0};
+  static std::mutex mu;
+  static std::set<std::pair<const void*, int>> done;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  if (!done[dev]) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            int(bytes));
+  const void* fn = reinterpret_cast<const void*>(kern);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!done.count({fn, dev})) {
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
     if (e != hipSuccess) return e;
-    done[dev] = 1;
+    done.insert({fn, dev});
   }
   return hipSuccess;
 }

@@ -164,7 +164,7 @@ def test_null_and_workspace_validation(lib):
         assert lib.oaa_conv_backward_filter(h, fake, None, fake, None) == 4   # no cached window spectra
         assert lib.oaa_conv_backward_filter(h, fake, fake, None, None) == 1
         assert lib.oaa_plan_set_contraction(h, 7) == 1
-        assert lib.oaa_plan_set_contraction(h, 4) == 1
+        assert lib.oaa_plan_set_contraction(h, 4) == 2                    # fused: needs L = 64
         assert lib.oaa_plan_set_contraction(h, 3) == 0                    # streaming: C = 3 <= 4
         assert lib.oaa_plan_set_contraction(h, 1) == 0
         assert lib.oaa_plan_region(h, 4, None, None) == 1
@@ -173,6 +173,48 @@ def test_null_and_workspace_validation(lib):
         assert lib.oaa_plan_geometry(h, ctypes.byref(g)) == 0 and g.L == 16 and g.T == 4
     finally:
         binding.oaa_plan_destroy(h)
+
+
+def test_fused_passes_selection_and_caches(lib):
+    """Overlap-add plans at L = 64 with C <= 4 and at most 8 blocks per side
+    take the fused passes by default: kernel spectra in runs of four kernels,
+    one weight-gradient partial sum per range of block rows, and no gradient
+    spectra to reuse. Switching the contraction discards cached spectra."""
+    h = binding.oaa_plan_create_tiled(64, 3, 64, 224, 7, 64, 58)   # the first layer's tiling: T = 4
+    try:
+        g = binding.oaa_plan_geometry(h)
+        assert g["fused"] == 1 and g["T"] == 4 and g["split"] == 8   # 32 kernel pairs x 8 ranges of rows
+        _, wbytes = binding.oaa_plan_region(h, binding.REGION_W_SPECTRUM)
+        assert wbytes == 8 * g["F"] * 3 * 64
+        fake = 1 << 40   # never dereferenced: the calls below fail validation first
+        assert lib.oaa_plan_bind_workspace(h, fake, binding.oaa_plan_workspace_bytes(h)) == 0
+        assert lib.oaa_conv_backward_filter(h, fake, None, fake, None) == 4
+        assert "fused" in binding.oaa_last_error_detail()
+        assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_NARROW) == 0
+        g = binding.oaa_plan_geometry(h)
+        assert g["fused"] == 0 and g["split"] != 8
+        assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_FUSED) == 0
+        assert binding.oaa_plan_geometry(h)["fused"] == 1
+        assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_AUTO) == 0
+        assert binding.oaa_plan_geometry(h)["fused"] == 1
+    finally:
+        binding.oaa_plan_destroy(h)
+    h = binding.oaa_plan_create_tiled(1, 3, 5, 50, 7, 64, 58)          # K = 5: runs padded to 8
+    try:
+        _, wbytes = binding.oaa_plan_region(h, binding.REGION_W_SPECTRUM)
+        assert wbytes == 8 * 64 * 33 * 3 * 8
+    finally:
+        binding.oaa_plan_destroy(h)
+    for dims, tiling, method in [((1, 5, 4, 100, 7), (64, 58), 0),    # C = 5
+                                 ((1, 3, 4, 100, 7), (32, 26), 0),    # L = 32
+                                 ((1, 3, 4, 600, 7), (64, 58), 0),    # T = 11
+                                 ((1, 3, 4, 100, 7), (64, 0), 1)]:    # overlap-save
+        h = binding.oaa_plan_create_method(*dims, *tiling, method)
+        try:
+            assert binding.oaa_plan_geometry(h)["fused"] == 0
+            assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_FUSED) == 2
+        finally:
+            binding.oaa_plan_destroy(h)
 
 
 def test_streaming_contraction_needs_few_channels(lib):

@@ -169,6 +169,83 @@ def test_transform_side_64(gpu_lib, shape):
     check_whole(x, w, g, tiling=(L, b), method=m)
 
 
+@pytest.mark.parametrize("shape", [sh for sh in BIG64 if sh[7] == "oaa" and sh[1] <= 4],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_transform_side_64_unfused(gpu_lib, shape):
+    """The few-channel L = 64 layers above (which take the fused passes by
+    default) through the unfused passes: tile-group transforms and the
+    streaming contraction."""
+    B, C, K, N, n, L, b, method = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=71 + sum(shape[:7]))
+    check_whole(x, w, g, contraction=binding.CONTRACTION_NARROW, tiling=(L, b))
+
+
+FUSED = [  # (B, C, K, N, n, L, b): the fused few-channel passes (L = 64, C <= 4, T <= 8)
+    (2, 3, 5, 100, 7, 64, 58),     # the first layer's tiling, reduced: T = 2 (4 planes per item)
+    (1, 3, 9, 224, 7, 64, 58),     # the first layer's planes: T = 4, K off a multiple of four
+    (2, 1, 3, 60, 5, 64, 60),      # one block per plane, K < 4
+    (1, 2, 6, 120, 16, 64, 49),    # T = 3, kernels of 16 (15 carried rows)
+    (1, 4, 4, 150, 20, 64, 40),    # C = 4, T = 4, ragged last block
+    (1, 2, 3, 200, 32, 64, 32),    # T = 7: one plane per item
+    (3, 1, 2, 9, 1, 64, 8),        # n = 1: no overlap, nothing carried
+    (1, 3, 4, 80, 33, 64, 32),     # n = 33, b = n - 1: 32 carried rows, KR = 64
+    (5, 2, 7, 37, 4, 64, 20),      # odd block count per split, B T not a multiple of the splits
+]
+
+
+@pytest.mark.parametrize("shape", FUSED, ids=lambda s: "x".join(map(str, s)))
+def test_fused_few_channel_passes(gpu_lib, shape):
+    """The fused passes (the library's choice for these layers) against the
+    oracle, compared whole, in the training-step order (cached kernel and
+    input spectra, g given again to the weight gradient) and with explicit
+    inputs; then forced through OAA_CONTRACTION_FUSED."""
+    B, C, K, N, n, L, b = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=97 + sum(shape))
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    assert plan.geometry["fused"] == 1 and not plan.caches_grad_spectra
+    y, dx, dw = run_training_step(plan, x, w, g)
+    refs = (oracle.conv_forward(x, w), oracle.conv_backward_data(g, w, N), oracle.conv_backward_filter(x, g, n))
+    e = tuple(relerr(a, r) for a, r in zip((y, dx, dw), refs))
+    print(f"fused {shape}: rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e} bwd_filter {e[2]:.2e}", flush=True)
+    assert max(e) <= TOL, e
+    e2 = check_whole(x, w, g, contraction=binding.CONTRACTION_FUSED, tiling=(L, b))
+    assert max(e2) <= TOL
+
+
+def test_fused_spectra_layouts(gpu_lib):
+    """The W and X regions of a fused plan against the oracle's kernel and
+    block spectra, in the run layouts oaa.h documents, and the weight-gradient
+    partial sums in PRODUCT against the oracle's contraction."""
+    B, C, K, N, n, L, b = 2, 3, 6, 100, 7, 64, 58
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=13)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    geo = plan.geometry
+    T, F, S = geo["T"], geo["F"], geo["split"]
+    V = L // 2 + 1
+    assert geo["fused"] == 1
+    xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
+    plan.forward(xd, wd)
+    torch.cuda.synchronize()
+    K4 = (K + 3) // 4
+    Wh = plan.region(binding.REGION_W_SPECTRUM).cpu().numpy()[:K4 * C * F * 4].reshape(K4, C, L, V, 4)
+    Wh = Wh.transpose(0, 4, 1, 2, 3).reshape(K4 * 4, C, L, V)[:K]          # [K,C,L,V]
+    Xh = plan.region(binding.REGION_X_SPECTRUM).cpu().numpy()[:B * T * C * F * T].reshape(B, T, C, L, V, T)
+    Xh = Xh.transpose(0, 2, 1, 5, 3, 4)                                     # [B,C,T,T,L,V]
+    Wo = oaa_oracle.filter_spectra(w, L)
+    Xo = oaa_oracle.block_spectra(x, n, L, b)
+    keep = np.ones((L, V), bool)
+    keep[L // 2 + 1:, 0] = keep[L // 2 + 1:, V - 1] = False
+    assert relerr(Wh[..., keep], Wo[..., keep]) < TOL
+    assert relerr(Xh[..., keep], Xo[..., keep]) < TOL
+    plan.backward_data(gd, None)
+    plan.backward_filter(None, gd)
+    torch.cuda.synchronize()
+    part = plan.region(binding.REGION_PRODUCT).cpu().numpy()[:S * F * C * K].reshape(S, L, V, C, K)
+    dWh = part.astype(np.complex128).sum(0)
+    Go = oaa_oracle.window_spectra(g, n, N, L, side=min(2 * b, L), b=b)
+    assert relerr(dWh.transpose(3, 2, 0, 1)[..., keep], oaa_oracle.backward_filter_product(Go, Xo)[..., keep]) < TOL
+
+
 BIG128 = [  # (B, C, K, N, n, L, b, method): transform side 128 (kernel sides up to 64)
     (1, 2, 3, 64, 33, 128, 33, "oaa"),     # the paper's tiling at n = 33: T = 2, overlap-add in two steps
     (1, 2, 2, 64, 48, 128, 48, "oaa"),     # T = 2
@@ -314,11 +391,12 @@ def test_reduced_large_layers_whole(gpu_lib, name, batch, C, K, tiling):
 def run_training_step(plan, x, w, g):
     """The three passes as bench.py times them: backward_data reuses the
     forward's kernel spectra, backward_filter the input and gradient spectra
-    of the two passes before it."""
+    of the two passes before it (the fused passes keep no gradient spectra
+    and take g again)."""
     xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
     y = plan.forward(xd, wd)
     dx = plan.backward_data(gd, None)
-    dw = plan.backward_filter(None, None)
+    dw = plan.backward_filter(None, None if plan.caches_grad_spectra else gd)
     torch.cuda.synchronize()
     return y.cpu().numpy(), dx.cpu().numpy(), dw.cpu().numpy()
 

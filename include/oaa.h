@@ -114,8 +114,8 @@ typedef enum {
                                 are never written here, and the X and G
                                 regions may omit them too.
                               With the fused passes (OAA_CONTRACTION_FUSED) the layouts
-                              differ: W holds runs of four kernels, bin-minor
-                              ([ceil(K/4)][C][F][4]); X runs of a block row
+                              differ: W holds the kernels' bins contiguous
+                              ([K][C][F]); X runs of a block row
                               ([B*T][C][F][T], block (P, Q) of image b in run b*T + P at
                               position Q); G and the forward product are never stored;
                               PRODUCT holds only the weight-gradient partial sums,

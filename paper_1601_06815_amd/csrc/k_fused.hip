@@ -26,8 +26,9 @@
 // Spectra are held per tile as 64 x 33 bins (f = u * 33 + v) in LDS slots of
 // 2113 complex elements, eight slots per workgroup (one workgroup per CU).
 // The input block spectra come in runs of a block row (the T blocks of each
-// bin and channel together) and the kernel spectra in runs of four kernels,
-// so that a lane reads its bin's operands with a few vector loads.
+// bin and channel together) and the kernel spectra kernel by kernel, bins
+// contiguous, so that the lanes of a wave, one bin each, read their operands
+// from a few whole cache lines.
 #include <algorithm>
 
 #include "fft_core.hpp"
@@ -335,22 +336,20 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_fwd_kernel(FusedFwdPara
       asm volatile("" : "+v"(ft));
 #pragma unroll
       for (int i5 = 0; i5 < PI; ++i5) {
-        // two bins' operands in flight at a time (registers)
+        // two bins' operands in flight at a time (registers). The loads are
+        // unconditional (indices clamped into the operands), so that they
+        // issue together rather than one per branch
         if (i5 % 2 == 0) asm volatile("" ::: "memory");
-        const int f = ft + i5 * NT;
-        if (f >= kPos || !bin_used(f)) continue;
+        const int f = ft + i5 * NT, fl = min(f, kPos - 1);
         float2 xv[C][TMAX], wv[C][KG];
 #pragma unroll
         for (int c = 0; c < C; ++c) {
 #pragma unroll
-          for (int q = 0; q < TMAX; ++q)
-            if (q < T) xv[c][q] = xrow[(size_t(c) * kPos + f) * T + q];
+          for (int q = 0; q < TMAX; ++q) xv[c][q] = xrow[(size_t(c) * kPos + fl) * T + min(q, T - 1)];
 #pragma unroll
-          for (int ks = 0; ks < KG; ++ks) {
-            const int k = k0 + ks;
-            if (ks < nk) wv[c][ks] = p.ws[(size_t(k >> 2) * C + c) * kPos * 4 + size_t(f) * 4 + (k & 3)];
-          }
+          for (int ks = 0; ks < KG; ++ks) wv[c][ks] = p.ws[(size_t(k0 + min(ks, nk - 1)) * C + c) * kPos + fl];
         }
+        if (f >= kPos || !bin_used(f)) continue;
 #pragma unroll
         for (int ks = 0; ks < KG; ++ks) {
           if (ks >= nk) continue;
@@ -374,30 +373,42 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_fwd_kernel(FusedFwdPara
       // (or written, after the last one).
       // per lane, for each chunk of 64 output columns: the float offsets of
       // its column in the (at most two) blocks that cover it, -1 if none
+      // (offsets 0 and weight 0 where no block covers it, so that the reads
+      // need no branch)
       int o0[MCH], o1[MCH];
+      float m0[MCH], m1[MCH];
 #pragma unroll
       for (int ch = 0; ch < MCH; ++ch) {
         const int j = lane + 64 * ch, cf = j + off, Q1 = div_b(cf), ca1 = cf - Q1 * b;
         const bool in = j < M;
-        o0[ch] = in && Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR ? 2 * (Q1 - 1) * kSlot + ca1 + b : -1;
-        o1[ch] = in && Q1 < T ? 2 * Q1 * kSlot + ca1 : -1;
+        const bool v0 = in && Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR, v1 = in && Q1 < T;
+        o0[ch] = v0 ? 2 * (Q1 - 1) * kSlot + ca1 + b : 0;
+        o1[ch] = v1 ? 2 * Q1 * kSlot + ca1 : 0;
+        m0[ch] = v0 ? 1.f : 0.f;
+        m1[ch] = v1 ? 1.f : 0.f;
       }
+      const int nch = (M + 63) / 64;
       for (int task = wave; task < nk * b; task += nwave) {
         const int ks = task / b, ra = task - ks * b;
         const int i = r * b + ra - off;
         if (i < 0 || i >= M) continue;
         const bool add_carry = r > 0 && ra < nov;
-        const float* crow = carry + (ks * nov + ra) * M;
         const float* lrow = smem + 2 * (ks * T * kSlot + ra * kV);
+        const float* crow = add_carry ? carry + (ks * nov + ra) * M : lrow;  // (weight 0 then)
         float* orow = p.y + ((size_t(img) * p.K + k0 + ks) * M + i) * size_t(M);
+        const float cw = add_carry ? 1.f : 0.f;
+        float acc[MCH];
 #pragma unroll
         for (int ch = 0; ch < MCH; ++ch) {
+          if (ch >= nch) break;
+          const int j = min(lane + 64 * ch, M - 1);
+          acc[ch] = __builtin_fmaf(cw, crow[j], __builtin_fmaf(m0[ch], lrow[o0[ch]], m1[ch] * lrow[o1[ch]]));
+        }
+#pragma unroll
+        for (int ch = 0; ch < MCH; ++ch) {
+          if (ch >= nch) break;
           const int j = lane + 64 * ch;
-          if (j >= M) break;
-          float acc = add_carry ? crow[j] : 0.f;
-          if (o0[ch] >= 0) acc += lrow[o0[ch]];
-          if (o1[ch] >= 0) acc += lrow[o1[ch]];
-          orow[j] = acc;
+          if (j < M) orow[j] = acc[ch];
         }
       }
       lds_barrier();  // the carry has been read
@@ -409,17 +420,22 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_fwd_kernel(FusedFwdPara
         const float* lrow = smem + 2 * (ks * T * kSlot + ra * kV);
         float* crow = carry + (ks * nov + rb) * M;
         float* orow = p.y + ((size_t(img) * p.K + k0 + ks) * M + (last ? i : 0)) * size_t(M);
+        float acc[MCH];
 #pragma unroll
         for (int ch = 0; ch < MCH; ++ch) {
+          if (ch >= nch) break;
+          acc[ch] = __builtin_fmaf(m0[ch], lrow[o0[ch]], m1[ch] * lrow[o1[ch]]);
+        }
+#pragma unroll
+        for (int ch = 0; ch < MCH; ++ch) {
+          if (ch >= nch) break;
           const int j = lane + 64 * ch;
-          if (j >= M) break;
-          float acc = 0.f;
-          if (o0[ch] >= 0) acc += lrow[o0[ch]];
-          if (o1[ch] >= 0) acc += lrow[o1[ch]];
-          if (last)
-            orow[j] = acc;
-          else
-            crow[j] = acc;
+          if (j < M) {
+            if (last)
+              orow[j] = acc[ch];
+            else
+              crow[j] = acc[ch];
+          }
         }
       }
       lds_barrier();
@@ -476,15 +492,13 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_bwd_data_kernel(FusedBw
 #pragma unroll
       for (int i5 = 0; i5 < PI; ++i5) {
         if (i5 % 2 == 0) asm volatile("" ::: "memory");
-        const int f = ft + i5 * NT;
-        if (f >= kPos || !bin_used(f)) continue;
+        const int f = ft + i5 * NT, fl = min(f, kPos - 1);
         float2 wv[C][4];
 #pragma unroll
-        for (int c = 0; c < C; ++c) {
-          const float2* wr = p.ws + (size_t(kc) * C + c) * kPos * 4 + size_t(f) * 4;
+        for (int c = 0; c < C; ++c)
 #pragma unroll
-          for (int ks = 0; ks < 4; ++ks) wv[c][ks] = wr[ks];
-        }
+          for (int ks = 0; ks < 4; ++ks) wv[c][ks] = p.ws[(size_t(k0 + min(ks, nk - 1)) * C + c) * kPos + fl];
+        if (f >= kPos || !bin_used(f)) continue;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
           if (ks >= nk) continue;
@@ -575,14 +589,13 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_bwd_filter_kernel(Fused
 #pragma unroll
       for (int i5 = 0; i5 < PI; ++i5) {
         if (i5 % 2 == 0) asm volatile("" ::: "memory");
-        const int f = ft + i5 * NT;
-        if (f >= kPos || !bin_used(f)) continue;
+        const int f = ft + i5 * NT, fl = min(f, kPos - 1);
         float2 xv[C][TMAX];
 #pragma unroll
         for (int c = 0; c < C; ++c)
 #pragma unroll
-          for (int q = 0; q < TMAX; ++q)
-            if (q < T) xv[c][q] = xrow[(size_t(c) * kPos + f) * T + q];
+          for (int q = 0; q < TMAX; ++q) xv[c][q] = xrow[(size_t(c) * kPos + fl) * T + min(q, T - 1)];
+        if (f >= kPos || !bin_used(f)) continue;
 #pragma unroll
         for (int ks = 0; ks < KF; ++ks) {
           if (ks >= nk) continue;

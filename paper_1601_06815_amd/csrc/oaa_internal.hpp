@@ -174,19 +174,19 @@ inline size_t overlap_tile_bytes(long n_planes, int T, int KR) {
 // forward product spectra nor the gradient window spectra are stored. Input
 // block spectra come in runs of a block row: element (bin f, channel c, block
 // (P, Q) of image img) at ((img T + P) C + c) F T + f T + Q; kernel spectra
-// in runs of four kernels: (f, c, k) at ((k / 4) C + c) F 4 + f 4 + k % 4
+// kernel by kernel, bins contiguous: (f, c, k) at (k C + c) F + f
 // (F = 64 * 33 bin positions f = u * 33 + v).
 constexpr int kFusedMaxC = 4;
 struct FusedFwdParams {
   const float2* xs;  // input block spectra, runs of a block row
-  const float2* ws;  // kernel spectra, runs of four kernels
+  const float2* ws;  // kernel spectra [K][C][F]
   float* y;          // [B][K][M][M]
   int B, K, M, T, b, KR, off;  // blocks b x b at pitch b, results KR = b + n - 1, off = n - 1
   int Kg, ngrp;      // output planes per workgroup item, items per image (launcher)
 };
 struct FusedBwdDataParams {
   const float* g;    // [B][K][M][M]
-  const float2* ws;  // kernel spectra, runs of four kernels
+  const float2* ws;  // kernel spectra [K][C][F]
   float* dx;         // [B][C][N][N]
   int B, K, N, M, T, b, off, S;  // gradient windows: S x S at (P b - off, Q b - off)
 };

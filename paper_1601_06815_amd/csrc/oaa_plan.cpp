@@ -239,10 +239,10 @@ oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
   oaa_plan_t p = cx.p;
   hipStream_t s = cx.s;
   if (p->fused) {
-    // runs of four kernels: (f, c, k) at ((k / 4) C + c) F 4 + f 4 + k % 4
+    // kernel by kernel, bins contiguous: (f, c, k) at (k C + c) F + f
     const size_t F = p->F, C = p->C;
     oaa_status_t st = big_forward(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", w, region(cx, OAA_REGION_W_SPECTRUM),
-                                  p->K, p->C, p->n, p->n, 0, p->n, 1, 4, 4, F * 4, C * F * 4);
+                                  p->K, p->C, p->n, p->n, 0, p->n, 1, 1, 1, F, C * F);
     if (st == OAA_OK && cx.own) p->w_valid = true;
     return st;
   }
@@ -785,8 +785,7 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   const bool fused_ok = method == OAA_METHOD_OVERLAP_ADD && oaa::fused_supported(L, C, N, n, b, T);
   int fsplit = 1;
   if (fused_ok) fsplit = oaa::fused_filter_split(B, K, T, OAA_FUSED_ITEMS);
-  // (the fused layout of the kernel spectra rounds K up to whole runs of four)
-  const unsigned long long eW = (unsigned long long)F * C * (fused_ok ? (K + 3) / 4 * 4 : K);
+  const unsigned long long eW = (unsigned long long)F * C * K;
   const unsigned long long eX = (unsigned long long)F * C * BP;
   const unsigned long long eG = (unsigned long long)F * K * BP;
   if (eX > kMaxElems || eG > kMaxElems || eW > kMaxElems)

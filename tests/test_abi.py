@@ -177,7 +177,7 @@ def test_null_and_workspace_validation(lib):
 
 def test_fused_passes_selection_and_caches(lib):
     """Overlap-add plans at L = 64 with C <= 4 and at most 8 blocks per side
-    take the fused passes by default: kernel spectra in runs of four kernels,
+    take the fused passes by default: kernel spectra bin-contiguous per kernel,
     one weight-gradient partial sum per range of block rows, and no gradient
     spectra to reuse. Switching the contraction discards cached spectra."""
     h = binding.oaa_plan_create_tiled(64, 3, 64, 224, 7, 64, 58)   # the first layer's tiling: T = 4
@@ -197,12 +197,6 @@ def test_fused_passes_selection_and_caches(lib):
         assert binding.oaa_plan_geometry(h)["fused"] == 1
         assert lib.oaa_plan_set_contraction(h, binding.CONTRACTION_AUTO) == 0
         assert binding.oaa_plan_geometry(h)["fused"] == 1
-    finally:
-        binding.oaa_plan_destroy(h)
-    h = binding.oaa_plan_create_tiled(1, 3, 5, 50, 7, 64, 58)          # K = 5: runs padded to 8
-    try:
-        _, wbytes = binding.oaa_plan_region(h, binding.REGION_W_SPECTRUM)
-        assert wbytes == 8 * 64 * 33 * 3 * 8
     finally:
         binding.oaa_plan_destroy(h)
     for dims, tiling, method in [((1, 5, 4, 100, 7), (64, 58), 0),    # C = 5

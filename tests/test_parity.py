@@ -226,9 +226,7 @@ def test_fused_spectra_layouts(gpu_lib):
     xd, wd, gd = to_dev(x), to_dev(w), to_dev(g)
     plan.forward(xd, wd)
     torch.cuda.synchronize()
-    K4 = (K + 3) // 4
-    Wh = plan.region(binding.REGION_W_SPECTRUM).cpu().numpy()[:K4 * C * F * 4].reshape(K4, C, L, V, 4)
-    Wh = Wh.transpose(0, 4, 1, 2, 3).reshape(K4 * 4, C, L, V)[:K]          # [K,C,L,V]
+    Wh = plan.region(binding.REGION_W_SPECTRUM).cpu().numpy()[:K * C * F].reshape(K, C, L, V)
     Xh = plan.region(binding.REGION_X_SPECTRUM).cpu().numpy()[:B * T * C * F * T].reshape(B, T, C, L, V, T)
     Xh = Xh.transpose(0, 2, 1, 5, 3, 4)                                     # [B,C,T,T,L,V]
     Wo = oaa_oracle.filter_spectra(w, L)

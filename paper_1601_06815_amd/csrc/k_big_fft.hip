@@ -52,6 +52,7 @@ struct Big {
   // columns 0 and L/2 as (re, im), plus one slot of padding
   static constexpr int RI = H2 + 1;
   static constexpr int TQ_MAX = L == 64 ? 9 : 2;  // tiles per group (LDS)
+  static constexpr int SIDE_MAX = L == 64 ? 3 : 1;  // blocks per side of a one-group plane
 };
 
 // threads of a workgroup (at most): eight waves, which leaves a lane 256
@@ -61,6 +62,11 @@ template <int L, bool PF>
 constexpr int big_threads() {
   return L == 64 && !PF ? 576 : 512;
 }
+// The inverse without the prefetch (planes of nine tiles, overlap-added in
+// one workgroup) also takes eight waves: with nine, a lane's registers are
+// capped at 168 and the passes spill (measured at the large-kernel layer:
+// 0.99 ms with 512 threads, some looping over a second task, against 1.40 ms
+// with 576).
 #ifndef OAA_BIG_INV_PF_BATCH
 #define OAA_BIG_INV_PF_BATCH 0
 #endif
@@ -69,9 +75,12 @@ constexpr int big_threads() {
 #endif
 // the inverse: with the prefetch, nine tiles (a plane of 3 x 3 blocks) at
 // L = 64 take 576 threads
+#ifndef OAA_BIG_INV_THREADS
+#define OAA_BIG_INV_THREADS 512
+#endif
 template <int L, bool PF>
 constexpr int big_inv_threads() {
-  return L == 64 ? (PF ? OAA_BIG_INV_PF_THREADS : 576) : 512;
+  return L == 64 ? (PF ? OAA_BIG_INV_PF_THREADS : OAA_BIG_INV_THREADS) : 512;
 }
 
 // LDS per tile (complex elements, odd)
@@ -237,7 +246,10 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
 // real columns. Row r of the inverse becomes kept row (r + rot) mod L. Pass 2
 // inverts pairs of kept rows to real rows, written over their own storage;
 // column s becomes kept column (s + rot) mod L.
-template <int L, bool O32, bool PF>
+// MODE: the kernel's pass 3 (0 crop, 1 overlap-add of one-group planes, 2
+// tiles to the scratch), fixed per instance so that each carries only the
+// registers of its own output code.
+template <int L, bool O32, bool PF, int MODE>
 __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(BigInvParams p) {
   constexpr int H2 = Big<L>::H2, V = Big<L>::V, RI = Big<L>::RI;
   extern __shared__ float smem[];
@@ -314,22 +326,36 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
     }
   };
   // pass 2 of one task: kept rows 2w, 2w + 1 to real rows, written over their
-  // own storage; column s becomes kept column (s + rot) mod L
+  // own storage; column s becomes kept column (s + rot) mod L. Lane 0 takes
+  // bins 0, 1, ..., L/2 - 1 of both rows, lane 1 bins L/2, L/2 - 1, ..., 1
+  // (bins 0 and L/2 being the parts of slot 0); the addresses step by one
+  // slot per element from opaque starting values, and a missing second row
+  // reads the first again and is zeroed, so that neither the compiler's
+  // precomputed addresses nor a branch per element hold registers.
   auto rows = [&](int q, int w) {
     const int r0 = 2 * w;
     const bool has1 = r0 + 1 < KR;
-    int zo = q * TSZ + r0 * RI, co = h + rot;
-    asm volatile("" : "+v"(zo), "+v"(co));
+    int zo = q * TSZ + r0 * RI, co = h + rot, st = h ? -1 : 1, db = has1 ? RI : 0;
+    asm volatile("" : "+v"(zo), "+v"(co), "+v"(st), "+v"(db));
     const float2* za = lds + zo;
-    const float2* zb = za + RI;
-    // bin v of a kept row: slot v, bins 0 and L/2 being the parts of slot 0
-    auto row_bin = [&](const float2* z, int v) {
-      const float2 s0 = z[v == H2 ? 0 : v];
-      return v == 0 ? make_float2(s0.x, 0.f) : (v == H2 ? make_float2(s0.y, 0.f) : s0);
-    };
+    const float keep1 = has1 ? 1.f : 0.f, sg = h ? 1.f : -1.f;
     float xr[H2], xi[H2];
-    irfft_pair_split<L, PF ? OAA_BIG_INV_PF_BATCH : 8>([&](int v) { return row_bin(za, v); },
-                        [&](int v) { return has1 ? row_bin(zb, v) : make_float2(0.f, 0.f); }, xr, xi, h);
+    {
+      const float2 a0 = za[0], b0 = za[db];
+      xr[0] = h ? a0.y : a0.x;
+      xi[0] = keep1 * (h ? b0.y : b0.x);
+    }
+    int o = h ? H2 - 1 : 1;
+#pragma unroll
+    for (int i = 1; i < H2; ++i) {
+      const float2 a = za[o], bb = za[o + db];
+      o += st;
+      // lane 0: a.x - b.y, a.y + b.x; lane 1: a.x + b.y, b.x - a.y
+      xr[i] = __builtin_fmaf(sg * keep1, bb.y, a.x);
+      xi[i] = __builtin_fmaf(-sg, a.y, keep1 * bb.x);
+      if (!PF && i % 8 == 7) asm volatile("" ::: "memory");  // bounds the reads in flight
+    }
+    fft_dif_split<L, +1>(xr, xi, h);  // lane h: L row0[s], L row1[s] at s = 2m + h, position bitrev(m)
     float* d0 = smem + 2 * zo;
 #pragma unroll
     for (int m = 0; m < H2; ++m) {
@@ -373,7 +399,7 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
     __syncthreads();
     const int H = p.H;
     const int wave = tid >> 6, lane = tid & 63, nwave = nthr >> 6;
-    if (p.overlap == 2) {
+    if (MODE == 2) {
       // kept KR x KR of every tile to the scratch, tile after tile
       float* ob = p.tiles + (size_t(ch) * tpc + t0) * KR * KR;
       const SmallDiv div_k(KR);
@@ -385,7 +411,7 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
           ot[e] = lt[2 * rr * RI + cc];
         }
       }
-    } else if (!p.overlap) {
+    } else if (MODE == 0) {
       // kept KR x KR of every tile to its block: a wave per tile (decoded
       // once, wave-uniform), lanes over the block in row order
       const SmallDiv div_k(KR);
@@ -403,27 +429,51 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
     } else {
       // the group is one whole plane: output pixel (i, j) is framed pixel
       // (i + off, j + off), the sum of at most two tiles per side, added in
-      // a fixed order. A wave per output row, lanes over the columns.
+      // a fixed order. A wave per output row, lanes over the columns. Each
+      // lane's column offsets in the (at most two) tiles covering its
+      // columns, with 0/1 weights, are taken once per plane, so that the
+      // reads of a row need no per-lane branch; the tile rows covering a
+      // row are the same for the whole wave.
       const int img = t0 / P, T = p.T, b = p.pitch;
       float* out = p.dst + (size_t(img) * p.n_ch + ch) * H * H;
       const SmallDiv div_b(b);
+      constexpr int MCH = (L * Big<L>::SIDE_MAX + 63) / 64;  // H < T b <= L T
+      int o0[MCH], o1[MCH];
+      float m0[MCH], m1[MCH];
+      int ln = lane;  // opaque: the offsets are not kept across the group loop
+      asm volatile("" : "+v"(ln));
+#pragma unroll
+      for (int k = 0; k < MCH; ++k) {
+        const int jx = ln + 64 * k, c = jx + p.off, Q1 = div_b(c), ca1 = c - Q1 * b;
+        const bool in = jx < H;
+        const bool v1 = in && Q1 < T, v0 = in && Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR;
+        o0[k] = v0 ? (Q1 - 1) * TSZ * 2 + ca1 + b : 0;
+        o1[k] = v1 ? Q1 * TSZ * 2 + ca1 : 0;
+        m0[k] = v0 ? 1.f : 0.f;
+        m1[k] = v1 ? 1.f : 0.f;
+      }
+      const int nch = (H + 63) / 64;
       for (int i = wave; i < H; i += nwave) {
         const int a = i + p.off, P1 = div_b(a), ra1 = a - P1 * b;
         // tile rows covering framed row a: P1 (row ra1) and P1 - 1 (row ra1 + b)
         const bool r1 = P1 < T, r0 = P1 >= 1 && P1 - 1 < T && ra1 + b < KR;
-        const float* l1 = ldf + 2 * (P1 * T * TSZ + ra1 * RI);
-        const float* l0 = ldf + 2 * ((P1 - 1) * T * TSZ + (ra1 + b) * RI);
+        const float* l1 = ldf + (r1 ? 2 * (P1 * T * TSZ + ra1 * RI) : 0);
+        const float* l0 = ldf + (r0 ? 2 * ((P1 - 1) * T * TSZ + (ra1 + b) * RI) : 0);
+        const float w0 = r0 ? 1.f : 0.f, w1 = r1 ? 1.f : 0.f;
         float* orow = out + size_t(i) * H;
-        for (int jx = lane; jx < H; jx += 64) {
-          const int c = jx + p.off, Q1 = div_b(c), ca1 = c - Q1 * b;
-          const bool c1 = Q1 < T, c0 = Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR;
-          const int o1 = Q1 * TSZ * 2 + ca1, o0 = (Q1 - 1) * TSZ * 2 + ca1 + b;
-          float acc = 0.f;
-          if (r0 && c0) acc += l0[o0];
-          if (r0 && c1) acc += l0[o1];
-          if (r1 && c0) acc += l1[o0];
-          if (r1 && c1) acc += l1[o1];
-          orow[jx] = acc;
+        float acc[MCH];
+#pragma unroll
+        for (int k = 0; k < MCH; ++k) {
+          if (k >= nch) break;
+          const float t0v = __builtin_fmaf(m0[k], l0[o0[k]], m1[k] * l0[o1[k]]);
+          const float t1v = __builtin_fmaf(m0[k], l1[o0[k]], m1[k] * l1[o1[k]]);
+          acc[k] = __builtin_fmaf(w0, t0v, w1 * t1v);
+        }
+#pragma unroll
+        for (int k = 0; k < MCH; ++k) {
+          if (k >= nch) break;
+          const int jx = lane + 64 * k;
+          if (jx < H) orow[jx] = acc[k];
         }
       }
     }
@@ -537,18 +587,28 @@ hipError_t launch_big_fwd_L(BigFwdParams p, hipStream_t s) {
   else return launch_big_fwd_LP<L, false>(p, lds, ngroups, s);
 }
 
-template <int L, bool PF>
-hipError_t launch_big_inv_LP(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
+template <int L, bool PF, int MODE>
+hipError_t launch_big_inv_LPM(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
   constexpr int V = Big<L>::V;
   const bool o32 =
       (size_t(L) * V * size_t(p.n_ch) * size_t(p.n_img) * p.T * p.T + size_t(p.nsplit - 1) * p.split_stride) * 8 <
       (size_t(1) << 32);
-  auto kern = o32 ? big_irfft2_kernel<L, true, PF> : big_irfft2_kernel<L, false, PF>;
+  auto kern = o32 ? big_irfft2_kernel<L, true, PF, MODE> : big_irfft2_kernel<L, false, PF, MODE>;
   const hipError_t e = allow_lds(kern, kBigLds);
   if (e != hipSuccess) return e;
   const int nthr = std::min(L * p.TQ, big_inv_threads<L, PF>());
   hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds)), dim3(nthr), lds, s, p);
   return hipGetLastError();
+}
+
+template <int L, bool PF>
+hipError_t launch_big_inv_LP(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
+  switch (p.overlap) {
+    case 0: return launch_big_inv_LPM<L, PF, 0>(p, lds, ngroups, s);
+    case 1: return launch_big_inv_LPM<L, PF, 1>(p, lds, ngroups, s);
+    case 2: return launch_big_inv_LPM<L, PF, 2>(p, lds, ngroups, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <int L>

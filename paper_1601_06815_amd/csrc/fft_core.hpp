@@ -25,7 +25,8 @@ __host__ __device__ constexpr int bitrev(int k, int L) {
   return r;
 }
 
-// (dr + i di) * exp(SIGN * 2 pi i t / L), written to (orr, oi).
+// (dr + i di) * exp(SIGN * 2 pi i t / L), written to (orr, oi); t in [0, L).
+// The quarter turns (t = 0, L/4, L/2, 3L/4) are exchanges and sign flips.
 template <int L, int SIGN>
 __host__ __device__ __forceinline__ void twiddle_mul(int t, float dr, float di, float& orr, float& oi) {
   if (t == 0) {
@@ -34,6 +35,12 @@ __host__ __device__ __forceinline__ void twiddle_mul(int t, float dr, float di, 
   } else if (4 * t == L) {  // exp(SIGN * i pi/2) = SIGN * i
     orr = SIGN > 0 ? -di : di;
     oi = SIGN > 0 ? dr : -dr;
+  } else if (2 * t == L) {  // -1
+    orr = -dr;
+    oi = -di;
+  } else if (4 * t == 3 * L) {  // exp(SIGN * 3 i pi/2) = -SIGN * i
+    orr = SIGN > 0 ? di : -di;
+    oi = SIGN > 0 ? -dr : dr;
   } else {
     const float c = tw::kTable<L>.c[t];
     const float s = SIGN > 0 ? tw::kTable<L>.s[t] : -tw::kTable<L>.s[t];
@@ -42,34 +49,57 @@ __host__ __device__ __forceinline__ void twiddle_mul(int t, float dr, float di, 
   }
 }
 
-// In-place radix-2 decimation-in-frequency FFT. Input in natural order; on
-// return, coefficient k sits at position bitrev(k, L). ZERO_HI states that
-// entries [L/2, L) of the input are zero, which turns the first stage into a
-// twiddle multiplication.
+// In-place decimation-in-frequency FFT. Input in natural order; on return,
+// coefficient k sits at position bitrev(k, L). ZERO_HI states that entries
+// [L/2, L) of the input are zero.
+//
+// Stages go in pairs (radix 2^2): the radix-2 stages of half-sizes h and h/2
+// take the four elements j, j + h/2, j + h, j + 3h/2 of a block of 2h
+// (j < h/2) to the same places as two radix-2 stages would, with
+//   d02 = x0 - x2, d13 = x1 - x3, r = exp(SIGN i pi/2) d13 (a quarter turn),
+//   x0 + x2 + x1 + x3,  (x0 + x2 - x1 - x3) W^(2t),  (d02 + r) W^t,
+//   (d02 - r) W^(3t),  W = exp(SIGN 2 pi i / L), t = j L / (2h),
+// i.e. three twiddle products per four points where the two stages take
+// four (the quarter turn of the second pair is an exchange). With an odd
+// number of stages the last one (h = 1, twiddles 1) is radix 2.
 template <int L, int SIGN, bool ZERO_HI>
 __host__ __device__ __forceinline__ void fft_dif(float (&re)[L], float (&im)[L]) {
 #pragma unroll
-  for (int half = L / 2; half >= 1; half /= 2) {
+  for (int half = L / 2; half >= 2; half /= 4) {
+    const int q = half / 2, s = L / (2 * half);
+    const bool zh = ZERO_HI && half == L / 2;  // x2 = x3 = 0 in the first pair of stages
 #pragma unroll
     for (int base = 0; base < L; base += 2 * half) {
 #pragma unroll
-      for (int j = 0; j < half; ++j) {
-        const int a = base + j;
-        const int b = a + half;
-        const int t = j * (L / (2 * half));
-        float dr, di;
-        if (ZERO_HI && half == L / 2) {
-          dr = re[a];
-          di = im[a];
-        } else {
-          const float ar = re[a], ai = im[a], br = re[b], bi = im[b];
-          re[a] = ar + br;
-          im[a] = ai + bi;
-          dr = ar - br;
-          di = ai - bi;
-        }
-        twiddle_mul<L, SIGN>(t, dr, di, re[b], im[b]);
+      for (int j = 0; j < q; ++j) {
+        const int i0 = base + j, i1 = i0 + q, i2 = i0 + half, i3 = i2 + q;
+        const int t = j * s;
+        const float x0r = re[i0], x0i = im[i0], x1r = re[i1], x1i = im[i1];
+        const float x2r = zh ? 0.f : re[i2], x2i = zh ? 0.f : im[i2];
+        const float x3r = zh ? 0.f : re[i3], x3i = zh ? 0.f : im[i3];
+        const float s02r = x0r + x2r, s02i = x0i + x2i, s13r = x1r + x3r, s13i = x1i + x3i;
+        const float d02r = x0r - x2r, d02i = x0i - x2i, d13r = x1r - x3r, d13i = x1i - x3i;
+        // r = SIGN i d13
+        const float rr = SIGN > 0 ? -d13i : d13i, ri = SIGN > 0 ? d13r : -d13r;
+        re[i0] = s02r + s13r;
+        im[i0] = s02i + s13i;
+        twiddle_mul<L, SIGN>(2 * t, s02r - s13r, s02i - s13i, re[i1], im[i1]);
+        twiddle_mul<L, SIGN>(t, d02r + rr, d02i + ri, re[i2], im[i2]);
+        twiddle_mul<L, SIGN>(3 * t, d02r - rr, d02i - ri, re[i3], im[i3]);
       }
+    }
+  }
+  // log2 L odd: a last radix-2 stage of half-size 1 (twiddle 1); with
+  // L = 2 and ZERO_HI its second input is zero
+  if ((L & 0x55555555) == 0) {
+#pragma unroll
+    for (int a = 0; a < L; a += 2) {
+      const float ar = re[a], ai = im[a];
+      const float br = (ZERO_HI && L == 2) ? 0.f : re[a + 1], bi = (ZERO_HI && L == 2) ? 0.f : im[a + 1];
+      re[a] = ar + br;
+      im[a] = ai + bi;
+      re[a + 1] = ar - br;
+      im[a + 1] = ai - bi;
     }
   }
 }

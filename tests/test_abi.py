@@ -347,3 +347,58 @@ def test_forward_noalloc_validation(lib):
         assert binding.STATUS[lib.oaa_conv_forward_noalloc(None, 256, 256, 256, None)] == "OAA_ERR_INVALID_ARG"
     finally:
         binding.oaa_plan_destroy(h)
+
+
+def test_register_fft_matches_numpy(tmp_path):
+    """The in-register transform of csrc/fft_core.hpp (radix-2^2 stages, a
+    last radix-2 stage for odd log2 L), run on the host: every size L = 2 to
+    64, both signs, with and without the zero upper half, against numpy's
+    FFT in double, coefficient k read at position bitrev(k)."""
+    import shutil
+    import subprocess
+    import numpy as np
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("no hipcc")
+    src = tmp_path / "fft.cpp"
+    src.write_text(r'''#include "fft_core.hpp"
+#include <cstdio>
+template <int L, int SIGN, bool ZH> void run(unsigned seed) {
+  float re[L], im[L];
+  unsigned s = seed;
+  for (int i = 0; i < L; ++i) {
+    s = s * 1664525u + 1013904223u; float a = float(s >> 8) / 16777216.0f - 0.5f;
+    s = s * 1664525u + 1013904223u; float b = float(s >> 8) / 16777216.0f - 0.5f;
+    re[i] = (ZH && i >= L / 2) ? 0.f : a; im[i] = (ZH && i >= L / 2) ? 0.f : b;
+    std::printf("i %d %d %d %d %.9e %.9e\n", L, SIGN, int(ZH), i, re[i], im[i]);
+  }
+  oaa::fft_dif<L, SIGN, ZH>(re, im);
+  for (int i = 0; i < L; ++i) std::printf("o %d %d %d %d %.9e %.9e\n", L, SIGN, int(ZH), i, re[i], im[i]);
+}
+template <int L> void all() { run<L, -1, false>(L); run<L, 1, false>(L + 7); run<L, -1, true>(L + 3); run<L, 1, true>(L + 5); }
+int main() { all<2>(); all<4>(); all<8>(); all<16>(); all<32>(); all<64>(); }
+''')
+    exe = tmp_path / "fft"
+    csrc = os.path.join(os.path.dirname(build.LIB_PATH), "csrc")
+    subprocess.run([hipcc, "-std=c++17", "-O1", "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
+                    "-packed-fp32-ops", "-I", csrc, "-x", "hip", str(src), "-o", str(exe)], check=True,
+                   capture_output=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    data = {}
+    for line in filter(None, out):
+        kind, L, sign, zh, i, a, b = line.split()
+        data.setdefault((int(L), int(sign), int(zh)), {}).setdefault(kind, {})[int(i)] = complex(float(a), float(b))
+
+    def bitrev(k, L):
+        r, b = 0, 1
+        while b < L:
+            r, k, b = (r << 1) | (k & 1), k >> 1, b << 1
+        return r
+
+    assert len(data) == 24
+    for (L, sign, zh), d in data.items():
+        x = np.array([d["i"][i] for i in range(L)])
+        X = np.fft.fft(x) if sign < 0 else L * np.fft.ifft(x)
+        got = np.array([d["o"][bitrev(k, L)] for k in range(L)])
+        err = np.max(np.abs(got - X)) / np.max(np.abs(X))
+        assert err < 2e-6, (L, sign, zh, err)

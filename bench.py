@@ -505,6 +505,8 @@ def main():
                          "(records matrix-core figures in profiles/mfma.json)")
     ap.add_argument("--summarize-stats", metavar="DIR",
                     help="host only: table of a rocprofv3 --kernel-trace --stats run")
+    ap.add_argument("--lib", default=None,
+                    help="run the library built at this path instead of the in-tree one (to compare builds)")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(args.layer, *args.summarize_pmc, method=args.method)
@@ -520,6 +522,9 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(the layer would shard along the batch, with one all-reduce of dw).", file=sys.stderr)
         sys.exit(2)
+    if args.lib:
+        from paper_1601_06815_amd import binding
+        binding.use_library(args.lib)
     if args.report:
         config_report(args)
         return

@@ -73,6 +73,16 @@ def load(path=None):
     return lib
 
 
+def use_library(path):
+    """Load liboaa.so from `path` and make it the library every later call
+    uses (for comparing builds; the default is the in-tree build)."""
+    global _LIB
+    _LIB = None
+    lib = load(path)
+    _LIB = lib
+    return lib
+
+
 class OaaError(RuntimeError):
     def __init__(self, status, detail):
         super().__init__(f"{STATUS.get(status, status)}: {detail}")

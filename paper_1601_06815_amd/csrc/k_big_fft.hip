@@ -100,6 +100,27 @@ __device__ __forceinline__ long first_group() {
   return long(blockIdx.x % 8) * (nwg / 8) + blockIdx.x / 8;
 }
 
+// The groups a workgroup takes: g, g + step, ... below end. Interleaved
+// (consecutive groups on the workgroups of one XCD at about the same time)
+// or, with `contig`, a contiguous range per workgroup (the workgroups of one
+// XCD holding consecutive ranges). The inverse walks contiguous ranges: the
+// runs of a plane's tiles in a bin share 64-byte sectors with the next
+// plane's, which the same workgroup then reads while they are still in L2
+// (measured at the large-kernel layer: forward inverse 0.99 -> 0.93 ms,
+// error-propagation inverse 0.33 -> 0.31 ms; the forward transforms were as
+// fast or slower that way).
+struct GroupWalk {
+  long g, end, step;
+};
+__device__ __forceinline__ GroupWalk group_walk(long ngroups, bool contig) {
+  const long w = first_group();
+  if (contig) {
+    const long nwg = gridDim.x, R = (ngroups + nwg - 1) / nwg;
+    return {w * R, min(ngroups, (w + 1) * R), 1};
+  }
+  return {w, ngroups, long(gridDim.x)};
+}
+
 // ---------------------------------------------------------------------------
 // forward: windows of planes -> half spectra
 //
@@ -122,7 +143,6 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
   const int P = p.T * p.T, tpc = p.n_img * P;
   const size_t bs = p.bs;
   const long ngroups = long(p.n_ch) * p.ngrp;
-  const unsigned nwg = gridDim.x;
   // pass 1: tile q1, columns j and j + L/2, rows [h L/2, h L/2 + L/2); a
   // wave holds one tile (lane = h + 2 (j + (L/2) q1))
   const int j = (tid >> 1) % H2, q1 = (tid >> 1) / H2;
@@ -152,9 +172,10 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
     }
   };
 
-  long g = first_group();
-  if (PF && g < ngroups) load(g);
-  for (; g < ngroups; g += nwg) {
+  const GroupWalk wk = group_walk(ngroups, false);
+  long g = wk.g;
+  if (PF && g < wk.end) load(g);
+  for (; g < wk.end; g += wk.step) {
     const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
     const int nq = min(p.TQ, tpc - t0);
     if (!PF) load(g);
@@ -186,7 +207,7 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
       }
     }
     __syncthreads();
-    if (PF && g + nwg < ngroups) load(g + nwg);  // in flight during pass 2
+    if (PF && g + wk.step < wk.end) load(g + wk.step);  // in flight during pass 2
     if (q2 < nq && u < H2) {
       const float2* row = lds + q2 * TSZ + u * RS + h * (H2 + 1);
       float re[H2], im[H2];
@@ -261,7 +282,6 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
   const int P = p.T * p.T, tpc = p.n_img * P;
   const size_t fstride = size_t(p.n_ch) * tpc;
   const long ngroups = long(p.n_ch) * p.ngrp;
-  const unsigned nwg = gridDim.x;
   const int npair = (KR + 1) / 2;
   const float scale = 1.0f / float(L * L);
   // tasks of passes 1 and 2: h + 2 (q + TQ w), tile q fastest; w is the
@@ -368,12 +388,13 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
   };
 
   const int tq0 = (tid >> 1) % p.TQ, tw0 = (tid >> 1) / p.TQ;  // this thread's first task
-  long g = first_group();
-  if (PF && g < ngroups) {
+  const GroupWalk wk = group_walk(ngroups, true);
+  long g = wk.g;
+  if (PF && g < wk.end) {
     const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
     if (tq0 < min(p.TQ, tpc - t0) && tw0 < H2) load(ch, t0, tq0, tw0);
   }
-  for (; g < ngroups; g += nwg) {
+  for (; g < wk.end; g += wk.step) {
     const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
     const int nq = min(p.TQ, tpc - t0);
     if (PF) {
@@ -387,8 +408,8 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
       }
     }
     __syncthreads();
-    if (PF && g + nwg < ngroups) {  // in flight during passes 2 and 3
-      const long gn = g + nwg;
+    if (PF && g + wk.step < wk.end) {  // in flight during passes 2 and 3
+      const long gn = g + wk.step;
       const int chn = int(gn / p.ngrp), t0n = int(gn % p.ngrp) * p.TQ;
       if (tq0 < min(p.TQ, tpc - t0n) && tw0 < H2) load(chn, t0n, tq0, tw0);
     }

@@ -81,30 +81,6 @@ def stage_work(ly, geo):
     }
 
 
-# fused few-channel passes (L = 64): the spectra of w and x by the tile-group
-# transforms, then one fused kernel per pass (and the tile-group inverse of
-# the weight gradient)
-KERNEL_SOURCE_FUSED = {
-    "w_spectrum": "k_big_fft.hip", "x_spectrum": "k_big_fft.hip", "fwd_inverse": "k_fused.hip",
-    "bwd_data_product": "k_fused.hip", "bwd_filter_product": "k_fused.hip", "bwd_filter_inverse": "k_big_fft.hip",
-}
-KERNEL_SOURCE = {
-    "w_spectrum": "k_tile_fft.hip", "x_spectrum": "k_tile_fft.hip", "g_spectrum": "k_tile_fft.hip",
-    "fwd_inverse": "k_fold_fft.hip", "bwd_data_inverse": "k_tile_fft.hip", "bwd_filter_inverse": "k_tile_fft.hip",
-    "fwd_product": "k_cgemm.hip", "bwd_data_product": "k_cgemm.hip", "bwd_filter_product": "k_cgemm.hip",
-}
-# the output-tiled method crops the forward and overlap-adds the error propagation
-KERNEL_SOURCE_OAS = dict(KERNEL_SOURCE, fwd_inverse="k_tile_fft.hip", bwd_data_inverse="k_fold_fft.hip")
-
-
-def kernel_source(geo, stage):
-    if geo.get("fused"):
-        return KERNEL_SOURCE_FUSED[stage]
-    if geo["L"] >= 64 and stage not in ("fwd_product", "bwd_data_product", "bwd_filter_product"):
-        return "k_big_fft.hip"
-    return (KERNEL_SOURCE_OAS if geo.get("method") else KERNEL_SOURCE)[stage]
-
-
 def traffic_key(workload, geo, stage):
     method = "/oas" if geo.get("method") else ""
     return f"{workload}@{geo['L']}:{geo['b']}{method}/{stage}"
@@ -115,12 +91,29 @@ SHARED_SOURCES = ("oaa_plan.cpp", "oaa_internal.hpp", "tile_common.hpp", "fft_co
 
 
 def source_digest(fname):
-    """Digest of a kernel's source file together with the headers it shares
-    and the plan code that picks its launch shape."""
+    """Digest of a kernel's source file(s) ("a.hip+b.hip" for a stage of two
+    kernels) together with the headers they share and the plan code that
+    picks their launch shape."""
     h = hashlib.sha256()
-    for f in (fname,) + SHARED_SOURCES:
+    for f in tuple(fname.split("+")) + SHARED_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_1601_06815_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
+
+
+KERNEL_FILES = (("big_", "k_big_fft.hip"), ("overlap_gather", "k_big_fft.hip"), ("fused_", "k_fused.hip"),
+                ("cgemm_", "k_cgemm.hip"), ("narrow_", "k_narrow.hip"), ("irfft2_fold", "k_fold_fft.hip"),
+                ("irfft2_overlap", "k_fold_fft.hip"), ("tile_rfft2", "k_tile_fft.hip"),
+                ("window_", "k_tile_fft.hip"), ("irfft2_crop", "k_tile_fft.hip"))
+
+
+def source_for_kernels(kernels):
+    """Source file(s) of a stage's kernel(s), "name" or "name+name"."""
+    files = []
+    for k in kernels.split("+"):
+        f = next((f for prefix, f in KERNEL_FILES if k.startswith(prefix)), None)
+        if f and f not in files:
+            files.append(f)
+    return "+".join(files)
 
 
 def _profile_record(fname, workload, geo, stage):
@@ -133,7 +126,9 @@ def _profile_record(fname, workload, geo, stage):
         rec = json.load(open(path)).get(traffic_key(workload, geo, stage))
     except (ValueError, OSError):
         return None
-    if not rec or rec.get("source_sha256") != source_digest(kernel_source(geo, stage)):
+    if not rec or not rec.get("kernel"):
+        return None
+    if rec.get("source_sha256") != source_digest(source_for_kernels(rec["kernel"])):
         return None
     return rec
 
@@ -185,7 +180,39 @@ def cpu_baseline(ly, x, w, g, budget_s=20.0):
 
 STAGE_ORDER = ["w_spectrum", "x_spectrum", "fwd_product", "fwd_inverse", "g_spectrum", "bwd_data_product",
                "bwd_data_inverse", "bwd_filter_product", "bwd_filter_inverse"]
-LIB_KERNELS = ("tile_rfft2_kernel", "window_rfft2_kernel", "window_rows_rfft2_kernel", "irfft2_", "cgemm_", "narrow_")
+LIB_KERNELS = ("tile_rfft2_kernel", "window_rfft2_kernel", "window_rows_rfft2_kernel", "irfft2_", "cgemm_", "narrow_",
+               "big_rfft2", "big_irfft2", "overlap_gather", "fused_")
+
+
+def stage_sequence(geo):
+    """The stage of each kernel launch of one training step, in launch order
+    (the fused passes launch one kernel per pass; the two-step overlap-add at
+    L = 128, planes of more than two tiles, adds a gather kernel)."""
+    if geo.get("fused"):
+        return ["w_spectrum", "x_spectrum", "fwd_inverse", "bwd_data_product", "bwd_filter_product",
+                "bwd_filter_inverse"]
+    seq = list(STAGE_ORDER)
+    if geo["L"] >= 128 and geo["P"] > 2:
+        twice = "bwd_data_inverse" if geo.get("method") else "fwd_inverse"
+        seq.insert(seq.index(twice), twice)
+    return seq
+
+
+def _per_stage(dispatches, seq, steps):
+    """Group the last `steps` steps' dispatches [(kernel, {counter: value})]
+    by stage: {stage: (kernels, {counter: mean per step})}."""
+    n = len(seq)
+    dispatches = dispatches[-steps * n:]
+    out = {}
+    for j in range(steps):
+        for i, stage in enumerate(seq):
+            k, vals = dispatches[j * n + i]
+            ks, acc = out.setdefault(stage, ([], {}))
+            if k not in ks:
+                ks.append(k)
+            for c, v in vals.items():
+                acc[c] = acc.get(c, 0.0) + v / steps
+    return {st: ("+".join(ks), acc) for st, (ks, acc) in out.items()}
 
 
 def _short_kernel(name):
@@ -228,10 +255,11 @@ def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, ste
     # a plain copy reads and writes copy_bytes; counters are in KiB
     f_factor = copy_bytes / (sorted(cf)[len(cf) // 2] * 1024)
     w_factor = copy_bytes / (sorted(cw)[len(cw) // 2] * 1024)
-    fetch = [(k, v) for k, v in _dispatch_values(fetch_dir, "FETCH_SIZE") if k.startswith(LIB_KERNELS)]
-    write = [(k, v) for k, v in _dispatch_values(write_dir, "WRITE_SIZE") if k.startswith(LIB_KERNELS)]
-    n = len(STAGE_ORDER)
-    fetch, write = fetch[-steps * n:], write[-steps * n:]
+    seq = stage_sequence(geo)
+    fetch = _per_stage([(k, {"v": v}) for k, v in _dispatch_values(fetch_dir, "FETCH_SIZE")
+                        if k.startswith(LIB_KERNELS)], seq, steps)
+    write = _per_stage([(k, {"v": v}) for k, v in _dispatch_values(write_dir, "WRITE_SIZE")
+                        if k.startswith(LIB_KERNELS)], seq, steps)
     work = stage_work(ly, geo)
     path = os.path.join(PROFILE_DIR, "traffic.json")
     db = json.load(open(path)) if os.path.exists(path) else {}
@@ -241,18 +269,16 @@ def summarize_pmc(layer, fetch_dir, write_dir, cal_fetch_dir, cal_write_dir, ste
     name = "overlap-save, h" if geo.get("method") else "b"
     print(f"## {layer}, L={geo['L']} {name}={geo['b']} (mean over the last {steps} steps)")
     print(f"{'stage':20s} {'kernel':48s} {'fetch MB':>9s} {'write MB':>9s} {'total MB':>9s} {'algo MB':>9s} {'ratio':>6s}")
-    for i, stage in enumerate(STAGE_ORDER):
-        fs = [fetch[j * n + i] for j in range(steps)]
-        ws = [write[j * n + i] for j in range(steps)]
-        kern = fs[0][0]
-        fb = sum(v for _, v in fs) / steps * 1024 * f_factor
-        wb = sum(v for _, v in ws) / steps * 1024 * w_factor
+    for stage in [st for st in STAGE_ORDER if st in fetch]:
+        kern = fetch[stage][0]
+        fb = fetch[stage][1]["v"] * 1024 * f_factor
+        wb = write[stage][1]["v"] * 1024 * w_factor
         algo = work[stage]["bytes"]
         print(f"{stage:20s} {kern[:48]:48s} {fb / 1e6:9.1f} {wb / 1e6:9.1f} {(fb + wb) / 1e6:9.1f} "
               f"{algo / 1e6:9.1f} {(fb + wb) / algo:6.2f}")
         db[traffic_key(layer, geo, stage)] = {
             "kernel": kern, "fetch_bytes": int(fb), "write_bytes": int(wb), "bytes_per_launch": int(fb + wb),
-            "source_sha256": source_digest(kernel_source(geo, stage))}
+            "source_sha256": source_digest(source_for_kernels(kern))}
     with open(path, "w") as f:
         json.dump(db, f, indent=1, sort_keys=True)
         f.write("\n")
@@ -286,21 +312,21 @@ def summarize_counters(layer, run_dir, steps=2, method="oaa"):
         e = per.setdefault(d, {"kernel": k})
         e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
     disp = [per[d] for d in sorted(per)]
-    n = len(STAGE_ORDER)
-    disp = disp[-steps * n:]
+    staged = _per_stage([(d["kernel"], {c: v for c, v in d.items() if c != "kernel"}) for d in disp],
+                        stage_sequence(geo), steps)
     work = stage_work(ly, geo)
     name = "overlap-save, h" if geo.get("method") else "b"
     print(f"## {layer}, L={geo['L']} {name}={geo['b']} (mean over the last {steps} steps)")
     print(f"{'stage':20s} {'kernel':44s} " + " ".join(f"{c[:24]:>24s}" for c in names))
     path = os.path.join(PROFILE_DIR, "mfma.json")
     db = json.load(open(path)) if os.path.exists(path) else {}
-    for i, stage in enumerate(STAGE_ORDER):
-        ds = [disp[j * n + i] for j in range(steps)]
-        mean = {c: sum(d.get(c, 0.0) for d in ds) / steps for c in names}
-        print(f"{stage:20s} {ds[0]['kernel'][:44]:44s} " + " ".join(f"{mean[c]:24.4g}" for c in names))
-        if "flops" in work[stage] and "MfmaUtil" in mean:
-            rec = {"kernel": ds[0]["kernel"], "mfma_busy": round(mean["MfmaUtil"] / 100.0, 4),
-                   "source_sha256": source_digest(kernel_source(geo, stage))}
+    for stage in [st for st in STAGE_ORDER if st in staged]:
+        kern, vals = staged[stage]
+        mean = {c: vals.get(c, 0.0) for c in names}
+        print(f"{stage:20s} {kern[:44]:44s} " + " ".join(f"{mean[c]:24.4g}" for c in names))
+        if work[stage].get("bound") == "mfma" and "MfmaUtil" in mean:
+            rec = {"kernel": kern, "mfma_busy": round(mean["MfmaUtil"] / 100.0, 4),
+                   "source_sha256": source_digest(source_for_kernels(kern))}
             if "MfmaFlopsF32" in mean:
                 rec["mfma_f32_flops"] = mean["MfmaFlopsF32"]
             for c, key in (("SQ_INSTS_VALU_MFMA_MOPS_XF32", "mfma_xf32_flops"),

@@ -132,7 +132,8 @@ typedef enum {
                                  that the product spectra (forward) and the
                                  gradient window spectra (both backward passes)
                                  are never stored: overlap-add plans with L = 64,
-                                 C <= 4 and T <= 8 (the library's choice there) */
+                                 C <= 4 and T <= 8 (the library's choice there
+                                 when B T^2 >= 512)                            */
 } oaa_contraction_t;
 
 /* Stages of the three passes, for per-stage timing. */

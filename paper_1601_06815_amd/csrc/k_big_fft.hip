@@ -551,10 +551,16 @@ int cu_count() {
   return cached[dev];
 }
 
+// Waves of these kernels resident on a CU: every instance takes more than 128
+// registers per lane, which leaves two waves on each of the four SIMDs.
+constexpr int kBigWavesPerCu = 8;
+
 // Persistent grid: whole rounds over the 8 XCDs, as many workgroups as are
-// resident (LDS-bound), at most one per group.
-unsigned persistent_grid(long ngroups, size_t lds) {
-  const long per_cu = std::max<long>(1, long(kBigLds / std::max<size_t>(lds, 1)));
+// resident (by LDS and by registers), at most one per group.
+unsigned persistent_grid(long ngroups, size_t lds, int nthr) {
+  const long by_lds = long(kBigLds / std::max<size_t>(lds, 1));
+  const long by_waves = kBigWavesPerCu / std::max(1, (nthr + 63) / 64);
+  const long per_cu = std::max<long>(1, std::min(by_lds, by_waves));
   long nwg = std::min<long>(per_cu * cu_count(), (ngroups + 7) / 8 * 8);
   nwg = std::max<long>(8, nwg / 8 * 8);
   return unsigned(nwg);
@@ -580,7 +586,7 @@ hipError_t launch_big_fwd_LP(const BigFwdParams& p, size_t lds, long ngroups, hi
   auto kern = o32 ? big_rfft2_kernel<L, true, PF> : big_rfft2_kernel<L, false, PF>;
   const hipError_t e = allow_lds(kern, kBigLds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds)), dim3(L * p.TQ), lds, s, p);
+  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds, L * p.TQ)), dim3(L * p.TQ), lds, s, p);
   return hipGetLastError();
 }
 
@@ -618,7 +624,7 @@ hipError_t launch_big_inv_LPM(const BigInvParams& p, size_t lds, long ngroups, h
   const hipError_t e = allow_lds(kern, kBigLds);
   if (e != hipSuccess) return e;
   const int nthr = std::min(L * p.TQ, big_inv_threads<L, PF>());
-  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds)), dim3(nthr), lds, s, p);
+  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds, nthr)), dim3(nthr), lds, s, p);
   return hipGetLastError();
 }
 

@@ -16,6 +16,12 @@
 // wave (96 lane exchanges for C = 3 instead of 576 for a full butterfly). The
 // partial sums of the chunks are added by the inverse-transform kernel, in a
 // fixed order.
+//
+// With few tiles per bin (B P <= 64, e.g. the single images of the paper's
+// sweeps) a lane per tile would leave the workgroup nearly idle and walk all K
+// kernels in one dependent chain; the forward and backward_data variants for
+// that case spread the kernels over the lanes as well (one workgroup per bin),
+// and the backward_filter variant (B P <= 16) gives each lane one kernel.
 #include <algorithm>
 
 #include "oaa_internal.hpp"
@@ -31,6 +37,7 @@ constexpr int kThreads = 256;
 constexpr int kKB = 256;       // kernel spectra staged per LDS block
 constexpr int kIter = 4;       // groups of VEC tiles per lane (forward, backward_data)
 constexpr int kKG = 16;        // kernels per wave (backward_filter)
+constexpr int kFewTiles = 64;  // B P up to which the few-tile variants run
 
 __device__ __forceinline__ float2 cmad_conj(float2 a, float2 b, float2 c) {
   // c + conj(a) * b
@@ -242,6 +249,97 @@ __global__ void __launch_bounds__(kThreads) narrow_bwd_filter_kernel(GemmParams 
   }
 }
 
+// Few tiles per bin: lane t takes tile j = t mod NB (NB = 2^nb_log2 >= B P)
+// and kernels t / NB + i 256 / NB. Forward: each lane writes its own outputs.
+template <int CN>
+__global__ void __launch_bounds__(kThreads) narrow_forward_few_kernel(GemmParams p, int nb_log2) {
+  const int f = unique_bin(blockIdx.x, p.L);
+  const int K = p.M, BP = p.N;
+  const int j = threadIdx.x & ((1 << nb_log2) - 1), nk = kThreads >> nb_log2;
+  if (j >= BP) return;  // no barrier below
+  const float2* A = p.A + size_t(f) * p.a_fstride;
+  const float2* B = p.B + size_t(f) * p.b_fstride;
+  float2* O = p.C + size_t(f) * p.c_fstride;
+  float2 x[CN];
+#pragma unroll
+  for (int c = 0; c < CN; ++c) x[c] = B[c * p.ldb + j];
+#pragma unroll 4
+  for (int k = threadIdx.x >> nb_log2; k < K; k += nk) {
+    float2 y = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int c = 0; c < CN; ++c) y = cmad(y, A[c * p.lda + k], x[c]);
+    O[size_t(k) * p.ldc + j] = y;
+  }
+}
+
+// Few tiles per bin, backward_data: each lane sums its kernels for its tile,
+// then the 256 / NB lanes of a tile are added in LDS in a fixed order.
+template <int CN>
+__global__ void __launch_bounds__(kThreads) narrow_bwd_data_few_kernel(GemmParams p, int nb_log2) {
+  __shared__ float2 red[CN][kThreads];
+  const int f = unique_bin(blockIdx.x, p.L);
+  const int K = p.Kr, BP = p.N;
+  const int t = threadIdx.x, mask = (1 << nb_log2) - 1, j = t & mask, nk = kThreads >> nb_log2;
+  const float2* A = p.A + size_t(f) * p.a_fstride;
+  const float2* B = p.B + size_t(f) * p.b_fstride;
+  float2* O = p.C + size_t(f) * p.c_fstride;
+  float2 acc[CN];
+#pragma unroll
+  for (int c = 0; c < CN; ++c) acc[c] = make_float2(0.f, 0.f);
+  if (j < BP) {
+#pragma unroll 4
+    for (int k = t >> nb_log2; k < K; k += nk) {
+      const float2 g = B[size_t(k) * p.ldb + j];
+#pragma unroll
+      for (int c = 0; c < CN; ++c) acc[c] = cmad_conj(A[c * p.lda + k], g, acc[c]);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CN; ++c) red[c][t] = acc[c];
+  __syncthreads();
+  if (t < (CN << nb_log2) && (t & mask) < BP) {
+    const int c = t >> nb_log2, jj = t & mask;
+    float2 sum = make_float2(0.f, 0.f);
+    for (int q = 0; q < nk; ++q) {
+      const float2 v = red[c][(q << nb_log2) + jj];
+      sum.x += v.x;
+      sum.y += v.y;
+    }
+    O[c * p.ldc + jj] = sum;
+  }
+}
+
+// Few tiles per bin (B P <= 16), backward_filter: a lane per kernel walks
+// the bin's tiles (one partial sum: no split).
+constexpr int kFewTilesFilter = 16;
+
+template <int CN>
+__global__ void __launch_bounds__(kThreads) narrow_bwd_filter_few_kernel(GemmParams p) {
+  const int k = blockIdx.x * kThreads + threadIdx.x;
+  const int K = p.N, BP = p.Kr;
+  if (k >= K) return;
+  const int f = unique_bin(blockIdx.y, p.L);
+  const float2* A = p.A + size_t(f) * p.a_fstride;
+  const float2* g = p.B + size_t(f) * p.b_fstride + size_t(k) * p.ldb;
+  float2 acc[CN];
+#pragma unroll
+  for (int c = 0; c < CN; ++c) acc[c] = make_float2(0.f, 0.f);
+  for (int bp = 0; bp < BP; ++bp) {
+    const float2 gv = g[bp];
+#pragma unroll
+    for (int c = 0; c < CN; ++c) acc[c] = cmad_conj(A[c * p.lda + bp], gv, acc[c]);
+  }
+  float2* out = p.C + size_t(f) * p.c_fstride;
+#pragma unroll
+  for (int c = 0; c < CN; ++c) out[size_t(c) * p.ldc + k] = acc[c];
+}
+
+int few_tiles_log2(long BP) {
+  int l = 0;
+  while ((1L << l) < BP) ++l;
+  return l;
+}
+
 template <int CN, int VEC>
 hipError_t launch_fwd(const GemmParams& p, hipStream_t s) {
   const long per_wg = long(kIter) * kThreads * VEC;
@@ -272,6 +370,22 @@ bool pairs_ok(long ld, long chunk, int nsplit) { return ld % 2 == 0 && (nsplit =
 
 template <int CN>
 hipError_t launch_narrow_c(const GemmParams& p, hipStream_t s) {
+  const bool few = p.N >= 1 && p.N <= kFewTiles && p.nsplit == 1;
+  if (few && p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) {
+    hipLaunchKernelGGL(narrow_forward_few_kernel<CN>, dim3(unsigned(p.F)), dim3(kThreads), 0, s, p,
+                       few_tiles_log2(p.N));
+    return hipGetLastError();
+  }
+  if (few && !p.a_trans && p.a_conj && !p.b_trans && !p.b_conj) {
+    hipLaunchKernelGGL(narrow_bwd_data_few_kernel<CN>, dim3(unsigned(p.F)), dim3(kThreads), 0, s, p,
+                       few_tiles_log2(p.N));
+    return hipGetLastError();
+  }
+  if (p.Kr >= 1 && p.Kr <= kFewTilesFilter && p.nsplit == 1 && !p.a_trans && p.a_conj && p.b_trans && !p.b_conj) {
+    hipLaunchKernelGGL(narrow_bwd_filter_few_kernel<CN>, dim3(unsigned((p.N + kThreads - 1) / kThreads), unsigned(p.F)),
+                       dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+  }
   if (p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) {
     const bool v2 = pairs_ok(p.ldb, 0, 1) && p.ldc % 2 == 0;
     return v2 ? launch_fwd<CN, 2>(p, s) : launch_fwd<CN, 1>(p, s);

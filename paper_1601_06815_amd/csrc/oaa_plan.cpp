@@ -60,6 +60,15 @@
 #define OAA_FUSED_ITEMS 256
 #endif
 
+// Tiles (B T^2) from which the library takes the fused passes by default: the
+// fused error propagation gives a workgroup two tiles and walks all K kernels
+// for them, so fewer than one pair per CU leaves the device mostly idle (a
+// single 64 x 64 image with 100 kernels of 17 x 17: 0.32 ms for the fused
+// error propagation against 0.05 ms for the unfused stages).
+#ifndef OAA_FUSED_MIN_TILES
+#define OAA_FUSED_MIN_TILES 512
+#endif
+
 struct oaa_plan_s {
   int B, C, K, N, n;
   int method;  // oaa_method_t
@@ -78,7 +87,7 @@ struct oaa_plan_s {
   oaa_contraction_t contraction;
   // fused few-channel passes: possible for this tiling, in use, and the
   // ranges of block rows of their weight gradient
-  bool fused_ok, fused;
+  bool fused_ok, fused_auto, fused;
   int fsplit;
   // per-stage timing: event pairs recorded around launches
   bool timing;
@@ -851,7 +860,8 @@ oaa_status_t oaa_plan_create_method(oaa_plan_t* out, int B, int C, int K, int N,
   p->ws_bound = 0;
   p->w_valid = p->x_valid = p->g_valid = false;
   p->contraction = OAA_CONTRACTION_AUTO;
-  p->fused_ok = p->fused = fused_ok;
+  p->fused_ok = fused_ok;
+  p->fused_auto = p->fused = fused_ok && BP >= OAA_FUSED_MIN_TILES;
   p->fsplit = fsplit;
   p->timing = false;
   *out = p;
@@ -950,7 +960,7 @@ oaa_status_t oaa_plan_set_contraction(oaa_plan_t plan, oaa_contraction_t which) 
                 "the fused passes need the overlap-add method, L = 64, C <= %d and at most 8 blocks per side "
                 "(plan: method %d, L=%d, C=%d, T=%d)",
                 oaa::kFusedMaxC, plan->method, plan->L, plan->C, plan->T);
-  const bool fused = which == OAA_CONTRACTION_FUSED || (which == OAA_CONTRACTION_AUTO && plan->fused_ok);
+  const bool fused = which == OAA_CONTRACTION_FUSED || (which == OAA_CONTRACTION_AUTO && plan->fused_auto);
   // the two paths keep their spectra in different layouts
   if (fused != plan->fused) plan->w_valid = plan->x_valid = plan->g_valid = false;
   plan->fused = fused;

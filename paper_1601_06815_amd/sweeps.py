@@ -68,7 +68,7 @@ def time_layer(torch, B, C, K, N, n, tiling, reps):
 
     def bwd():
         plan.backward_data(gd, None, dx)
-        plan.backward_filter(None, None, dw)
+        plan.backward_filter(None, None if plan.caches_grad_spectra else gd, dw)
 
     res = {}
     for name, fn in (("fwd", fwd), ("bwd", bwd)):

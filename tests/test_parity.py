@@ -111,6 +111,25 @@ def test_narrow_contraction(gpu_lib, shape):
         print(f"split {plan.geometry['split']}", flush=True)
 
 
+NARROW_FEW = [  # (B, C, K, N, n, L, b): at most 64 tiles per bin, many kernels (kernels over the lanes too)
+    (1, 1, 300, 32, 5, 16, 5),     # 49 tiles, K > 256
+    (1, 4, 40, 64, 5, 16, 8),      # 64 tiles: the largest few-tile case
+    (2, 1, 33, 20, 3, 16, 14),     # two images of 2 x 2 blocks
+    (1, 2, 257, 60, 5, 64, 60),    # one tile per bin at L = 64 (the unfused passes)
+    (1, 3, 100, 64, 33, 128, 96),  # one tile per bin at L = 128
+]
+
+
+@pytest.mark.parametrize("shape", NARROW_FEW, ids=lambda s: "x".join(map(str, s)))
+def test_narrow_contraction_few_tiles(gpu_lib, shape):
+    """The streaming contraction with few tiles per bin (forward and error
+    propagation spread the kernels over the lanes), forced, against the
+    oracle, compared whole."""
+    B, C, K, N, n, L, b = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=23 + sum(shape))
+    check_whole(x, w, g, binding.CONTRACTION_NARROW, tiling=(L, b))
+
+
 TILED = [  # (B, C, K, N, n, L, b): b = n - 1, b between n and L/2, b = L/2, L twice the paper's
     (1, 3, 4, 32, 5, 16, 4),
     (2, 2, 3, 13, 4, 8, 4),
@@ -172,15 +191,14 @@ def test_transform_side_64(gpu_lib, shape):
 @pytest.mark.parametrize("shape", [sh for sh in BIG64 if sh[7] == "oaa" and sh[1] <= 4],
                          ids=lambda s: "x".join(map(str, s)))
 def test_transform_side_64_unfused(gpu_lib, shape):
-    """The few-channel L = 64 layers above (which take the fused passes by
-    default) through the unfused passes: tile-group transforms and the
-    streaming contraction."""
+    """The few-channel L = 64 layers above through the unfused passes
+    (tile-group transforms and the streaming contraction), forced."""
     B, C, K, N, n, L, b, method = shape
     x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=71 + sum(shape[:7]))
     check_whole(x, w, g, contraction=binding.CONTRACTION_NARROW, tiling=(L, b))
 
 
-FUSED = [  # (B, C, K, N, n, L, b): the fused few-channel passes (L = 64, C <= 4, T <= 8)
+FUSED = [  # (B, C, K, N, n, L, b): the fused few-channel passes (L = 64, C <= 4, T <= 8), forced
     (2, 3, 5, 100, 7, 64, 58),     # the first layer's tiling, reduced: T = 2 (4 planes per item)
     (1, 3, 9, 224, 7, 64, 58),     # the first layer's planes: T = 4, K off a multiple of four
     (2, 1, 3, 60, 5, 64, 60),      # one block per plane, K < 4
@@ -195,13 +213,13 @@ FUSED = [  # (B, C, K, N, n, L, b): the fused few-channel passes (L = 64, C <= 4
 
 @pytest.mark.parametrize("shape", FUSED, ids=lambda s: "x".join(map(str, s)))
 def test_fused_few_channel_passes(gpu_lib, shape):
-    """The fused passes (the library's choice for these layers) against the
-    oracle, compared whole, in the training-step order (cached kernel and
-    input spectra, g given again to the weight gradient) and with explicit
-    inputs; then forced through OAA_CONTRACTION_FUSED."""
+    """The fused passes (taken by default from B T^2 >= 512 tiles; these
+    reduced layers choose them explicitly) against the oracle, compared
+    whole, in the training-step order (cached kernel and input spectra, g
+    given again to the weight gradient) and with explicit inputs."""
     B, C, K, N, n, L, b = shape
     x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=97 + sum(shape))
-    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b), contraction=binding.CONTRACTION_FUSED)
     assert plan.geometry["fused"] == 1 and not plan.caches_grad_spectra
     y, dx, dw = run_training_step(plan, x, w, g)
     refs = (oracle.conv_forward(x, w), oracle.conv_backward_data(g, w, N), oracle.conv_backward_filter(x, g, n))
@@ -218,7 +236,7 @@ def test_fused_spectra_layouts(gpu_lib):
     partial sums in PRODUCT against the oracle's contraction."""
     B, C, K, N, n, L, b = 2, 3, 6, 100, 7, 64, 58
     x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=13)
-    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b), contraction=binding.CONTRACTION_FUSED)
     geo = plan.geometry
     T, F, S = geo["T"], geo["F"], geo["split"]
     V = L // 2 + 1

@@ -312,8 +312,11 @@ def summarize_counters(layer, run_dir, steps=2, method="oaa"):
         e = per.setdefault(d, {"kernel": k})
         e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
     disp = [per[d] for d in sorted(per)]
+    seq = stage_sequence(geo)
+    if not geo.get("fused") and not any(d["kernel"].startswith(("cgemm_", "narrow_")) for d in disp):
+        seq = [st for st in seq if not st.endswith("_product")]  # a run filtered to the transform kernels
     staged = _per_stage([(d["kernel"], {c: v for c, v in d.items() if c != "kernel"}) for d in disp],
-                        stage_sequence(geo), steps)
+                        seq, steps)
     work = stage_work(ly, geo)
     name = "overlap-save, h" if geo.get("method") else "b"
     print(f"## {layer}, L={geo['L']} {name}={geo['b']} (mean over the last {steps} steps)")

@@ -166,10 +166,10 @@ oaa_status_t oaa_plan_create(oaa_plan_t* plan, int B, int C, int K, int N, int n
  * done on the spectra; above, after the inverse). L must be a power of two
  * in [2, 128] (else OAA_ERR_UNSUPPORTED); a b outside that range is
  * OAA_ERR_INVALID_ARG.
- * L = b = 0 lets the library choose: L in {L0, 2 L0} up to 64, or L0 = 128
- * (L0 the paper's side)
- * and b by a work estimate of contraction and transforms. Larger blocks
- * mean fewer tiles: fewer spectra to transform, store and contract. */
+ * L = b = 0 lets the library choose: L from L0 (the paper's side) up to 64,
+ * or L0 = 128, and b, by an estimate of the step time of contractions and
+ * transforms. Larger blocks mean fewer tiles: fewer spectra to transform,
+ * store and contract. */
 oaa_status_t oaa_plan_create_tiled(oaa_plan_t* plan, int B, int C, int K, int N, int n, int L, int b);
 
 /* Same, with a choice of method (oaa_method_t). For OAA_METHOD_OVERLAP_ADD
@@ -237,6 +237,36 @@ oaa_status_t oaa_conv_backward_data(oaa_plan_t plan, const float* g, const float
  * spectra: with them g == NULL is OAA_ERR_NO_CACHE. */
 oaa_status_t oaa_conv_backward_filter(oaa_plan_t plan, const float* x, const float* g, float* dw,
                                       void* hip_stream);
+
+/* Two stacked convolution layers with nothing between them, x -> conv(., w1)
+ * -> conv(., w2), composed in the frequency domain (Conclusion: convolution
+ * layers as products in the frequency domain, with no transform between
+ * them). conv(conv(x, w1), w2) = conv(x, w12), where w12[k][c] = sum_j
+ * w2[k][j] * w1[j][c] (full 2-D convolutions, side n1 + n2 - 1); its
+ * spectrum is, bin by bin, W12[c][k] = sum_j W1[c][j] W2[j][k]. This call
+ * transforms w1 and w2 at the plan's L, forms that product on the device and
+ * stores it as the plan's cached kernel spectra, so that
+ * oaa_conv_forward(plan, x, NULL, y) computes both layers, valid, without
+ * the intermediate activation ever leaving the frequency domain, and
+ * oaa_conv_backward_data(plan, g, NULL, dx) the gradient with respect to x
+ * through both. (backward_filter then gives the gradient of the composite
+ * kernel w12, not of w1 and w2.)
+ *   - plan: bound workspace; C = w1's input channels, K = w2's output
+ *     channels, n = n1 + n2 - 1 (else OAA_ERR_INVALID_ARG); not running the
+ *     fused passes (their kernel spectra have another layout; else
+ *     OAA_ERR_UNSUPPORTED: choose another contraction first).
+ *   - w1: device, [J][C][n1][n1] fp32; w2: device, [K][J][n2][n2] fp32;
+ *     J, n1, n2 >= 1.
+ *   - scratch: device memory of at least oaa_plan_chain_scratch_bytes(plan,
+ *     J) bytes, 256-byte aligned, owned by the caller, for the two layers'
+ *     spectra; free to reuse once the call's work on `stream` is done.
+ *   - stream: as for the passes. Validation happens before any launch.
+ * Later oaa_conv_forward / backward_data calls with w == NULL use the
+ * composed spectra until a call with w != NULL, a contraction switch or a
+ * workspace bind replaces or discards them. */
+size_t oaa_plan_chain_scratch_bytes(oaa_plan_t plan, int J);
+oaa_status_t oaa_plan_set_kernel_chain(oaa_plan_t plan, const float* w1, int J, int n1, const float* w2, int n2,
+                                       void* scratch, size_t scratch_bytes, void* hip_stream);
 
 /* Forward pass without device allocation, for callers that cannot allocate:
  * code being captured into a HIP graph, tight serving loops, harnesses that

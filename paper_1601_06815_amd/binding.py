@@ -47,6 +47,8 @@ SIGNATURES = {
     "oaa_conv_backward_data": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
     "oaa_conv_backward_filter": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
     "oaa_conv_forward_noalloc": (_c_int, [_vp, _vp, _vp, _vp, _vp]),
+    "oaa_plan_chain_scratch_bytes": (_c_size, [_vp, _c_int]),
+    "oaa_plan_set_kernel_chain": (_c_int, [_vp, _vp, _c_int, _c_int, _vp, _c_int, _vp, _c_size, _vp]),
     "oaa_status_string": (ctypes.c_char_p, [_c_int]),
     "oaa_last_error_detail": (ctypes.c_char_p, []),
 }
@@ -174,6 +176,14 @@ def oaa_conv_forward_noalloc(plan, x, w, y, stream):
     return _check(load().oaa_conv_forward_noalloc(plan, x, w, y, stream))
 
 
+def oaa_plan_chain_scratch_bytes(plan, J):
+    return load().oaa_plan_chain_scratch_bytes(plan, J)
+
+
+def oaa_plan_set_kernel_chain(plan, w1, J, n1, w2, n2, scratch, scratch_bytes, stream):
+    return _check(load().oaa_plan_set_kernel_chain(plan, w1, J, n1, w2, n2, scratch, scratch_bytes, stream))
+
+
 def oaa_status_string(status):
     return load().oaa_status_string(status).decode()
 
@@ -298,6 +308,23 @@ class Plan:
                                  self._ptr(dw, (K, C, n, n), "dw"), self._stream())
         self.generation += 1
         return dw
+
+    def set_kernel_chain(self, w1, w2):
+        """oaa_plan_set_kernel_chain: the plan's kernel spectra become those
+        of two stacked layers, w1[J,C,n1,n1] then w2[K,J,n2,n2] with
+        n1 + n2 - 1 = n; forward(x, None) then computes both layers."""
+        import torch
+        g = self.geometry
+        J, n1, n2 = w1.shape[0], w1.shape[-1], w2.shape[-1]
+        p1 = self._ptr(w1, (J, g["C"], n1, n1), "w1")
+        p2 = self._ptr(w2, (g["K"], J, n2, n2), "w2")
+        nbytes = oaa_plan_chain_scratch_bytes(self.handle, J)
+        scratch = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        stream = self._stream()
+        # scratch is allocated on, and used on, the current stream: torch
+        # reuses its memory only for work ordered after these kernels
+        oaa_plan_set_kernel_chain(self.handle, p1, J, n1, p2, n2, scratch.data_ptr(), scratch.numel(), stream)
+        self.generation += 1
 
     def set_timing(self, enable):
         oaa_plan_set_timing(self.handle, enable)

@@ -7,6 +7,8 @@
 //   forward          Yhat[f]  (K x BP) = What[f]^T   (K x C)  * Xhat[f] (C x BP)
 //   backward_data    dXhat[f] (C x BP) = conj What[f] (C x K)  * Ghat[f] (K x BP)
 //   backward_filter  dWhat[f] (C x K)  = conj Xhat[f] (C x BP) * Ghat[f]^T (BP x K)
+// and, to compose two stacked layers in the frequency domain (Conclusion),
+//   W12hat[f] (C x K) = W1hat[f] (C x J) * W2hat[f] (J x K).
 //
 // Two implementations, both staging 16-deep slices of the reduction for one
 // output tile through LDS as separate real and imaginary planes, with the
@@ -522,13 +524,16 @@ hipError_t launch(Kern kern, const GemmParams& p, hipStream_t s) {
 
 hipError_t launch_cgemm_valu(const GemmParams& p, hipStream_t s) {
   if (p.kchunk % kKC != 0 && p.nsplit > 1) return hipErrorInvalidValue;
-  // the three operand orientations the layer uses
+  // the three operand orientations of the layer's passes, and the plain
+  // product that composes two layers' kernel spectra
   if (p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj)
     return launch<kVM, kVN>(cgemm_valu_kernel<true, false, false, false>, p, s);
   if (!p.a_trans && p.a_conj && !p.b_trans && !p.b_conj)
     return launch<kVM, kVN>(cgemm_valu_kernel<false, true, false, false>, p, s);
   if (!p.a_trans && p.a_conj && p.b_trans && !p.b_conj)
     return launch<kVM, kVN>(cgemm_valu_kernel<false, true, true, false>, p, s);
+  if (!p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj)  // kernel spectra of two stacked layers
+    return launch<kVM, kVN>(cgemm_valu_kernel<false, false, false, false>, p, s);
   return hipErrorInvalidValue;
 }
 
@@ -538,6 +543,7 @@ hipError_t launch_cgemm_mfma(const GemmParams& p, hipStream_t s) {
   if (p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<true, false, false, false>(p, s);
   if (!p.a_trans && p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<false, true, false, false>(p, s);
   if (!p.a_trans && p.a_conj && p.b_trans && !p.b_conj) return launch_mfma<false, true, true, false>(p, s);
+  if (!p.a_trans && !p.a_conj && !p.b_trans && !p.b_conj) return launch_mfma<false, false, false, false>(p, s);
   return hipErrorInvalidValue;
 }
 

@@ -244,9 +244,10 @@ oaa_status_t big_inverse(const Ctx& cx, oaa_stage_t stage, const char* what, con
   return timed(cx, stage, what, [&] { return oaa::launch_big_irfft2(cx.p->L, b, cx.s); });
 }
 
+oaa_status_t filter_spectra(const Ctx& cx, const float* w, int K, int C, int n, float2* dst);
+
 oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
   oaa_plan_t p = cx.p;
-  hipStream_t s = cx.s;
   if (p->fused) {
     // kernel by kernel, bins contiguous: (f, c, k) at (k C + c) F + f
     const size_t F = p->F, C = p->C;
@@ -255,26 +256,67 @@ oaa_status_t run_filter_fft(const Ctx& cx, const float* w) {
     if (st == OAA_OK && cx.own) p->w_valid = true;
     return st;
   }
-  if (big_side(p)) {
-    // kernels as single-tile planes w[k][c]: spectra [F][C][K]
-    oaa_status_t st = big_forward(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", w, region(cx, OAA_REGION_W_SPECTRUM),
-                                  p->K, p->C, p->n, p->n, 0, p->n, 1);
-    if (st == OAA_OK && cx.own) p->w_valid = true;
-    return st;
-  }
+  oaa_status_t st = filter_spectra(cx, w, p->K, p->C, p->n, region(cx, OAA_REGION_W_SPECTRUM));
+  if (st == OAA_OK && cx.own) p->w_valid = true;
+  return st;
+}
+
+// Spectra [F][C][K] at the plan's L of K x C kernels w[k][c] of side n
+// (n <= L), zero-padded: the unfused kernel-spectra layout.
+oaa_status_t filter_spectra(const Ctx& cx, const float* w, int K, int C, int n, float2* dst) {
+  oaa_plan_t p = cx.p;
+  hipStream_t s = cx.s;
+  if (big_side(p))  // kernels as single-tile planes w[k][c]
+    return big_forward(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", w, dst, K, C, n, n, 0, n, 1);
   oaa::TileFwdParams t{};
   t.src = w;
-  t.dst = region(cx, OAA_REGION_W_SPECTRUM);
-  t.n_img = p->K;   // w[k][c] plane; spectra [F][C][K]
-  t.n_ch = p->C;
-  t.H = p->n;
-  t.pitch = p->n;
+  t.dst = dst;
+  t.n_img = K;
+  t.n_ch = C;
+  t.H = n;
+  t.pitch = n;
   t.off = 0;
-  t.R = p->n;
+  t.R = n;
   t.T = 1;
   t.gather = 1;
-  oaa_status_t st = timed(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra",
-                          [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+  return timed(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra", [&] { return oaa::launch_tile_rfft2(p->L, t, s); });
+}
+
+// Scratch of the two layers' spectra for kernel_chain: W1hat [F][C][J], then
+// W2hat [F][J][K], each 256-byte aligned.
+size_t chain_scratch_bytes(const oaa_plan_s* p, int J) {
+  return align_up(size_t(p->F) * p->C * J * 8) + align_up(size_t(p->F) * J * p->K * 8);
+}
+
+// Kernel spectra of two stacked layers, x -> conv(., w1) -> conv(., w2) with
+// nothing between them (the Conclusion's convolution layers as products in
+// the frequency domain): w1 [J][C][n1][n1] and w2 [K][J][n2][n2] are
+// transformed at the plan's L, and per bin W12hat[c][k] = sum_j
+// W1hat[c][j] W2hat[j][k] is written as the plan's kernel spectra. W12hat is
+// the spectrum of the full convolution of the two kernels summed over j, a
+// kernel of side n1 + n2 - 1 = n.
+oaa_status_t kernel_chain(const Ctx& cx, const float* w1, int J, int n1, const float* w2, int n2, char* scratch) {
+  oaa_plan_t p = cx.p;
+  float2* w1h = reinterpret_cast<float2*>(scratch);
+  float2* w2h = reinterpret_cast<float2*>(scratch + align_up(size_t(p->F) * p->C * J * 8));
+  if (oaa_status_t st = filter_spectra(cx, w1, J, p->C, n1, w1h)) return st;
+  if (oaa_status_t st = filter_spectra(cx, w2, p->K, J, n2, w2h)) return st;
+  oaa::GemmParams g{};
+  g.A = w1h;
+  g.B = w2h;
+  g.C = region(cx, OAA_REGION_W_SPECTRUM);
+  g.M = p->C; g.N = p->K; g.Kr = J;
+  g.lda = J; g.ldb = p->K; g.ldc = p->K;
+  g.a_fstride = size_t(p->C) * J;
+  g.b_fstride = size_t(J) * p->K;
+  g.c_fstride = size_t(p->C) * p->K;
+  g.nsplit = 1; g.kchunk = J; g.c_sstride = 0;
+  g.F = oaa::unique_bins(p->L);
+  g.L = p->L;
+  g.a_trans = false; g.a_conj = false; g.b_trans = false; g.b_conj = false;
+  oaa_status_t st = timed(cx, OAA_STAGE_W_SPECTRUM, "kernel spectra of two stacked layers", [&] {
+    return oaa::mfma_preferred(g) ? oaa::launch_cgemm_mfma(g, cx.s) : oaa::launch_cgemm_valu(g, cx.s);
+  });
   if (st == OAA_OK && cx.own) p->w_valid = true;
   return st;
 }
@@ -993,6 +1035,35 @@ oaa_status_t oaa_conv_backward_filter(oaa_plan_t p, const float* x, const float*
   if (!g && !p->g_valid) return fail(OAA_ERR_NO_CACHE, "g is NULL and no gradient window spectra are cached");
   (void)hipGetLastError();
   return backward_filter_pass(Ctx{p, p->ws, static_cast<hipStream_t>(stream), true}, x, g, dw);
+}
+
+size_t oaa_plan_chain_scratch_bytes(oaa_plan_t plan, int J) {
+  if (!plan || J < 1) return 0;
+  return chain_scratch_bytes(plan, J);
+}
+
+oaa_status_t oaa_plan_set_kernel_chain(oaa_plan_t p, const float* w1, int J, int n1, const float* w2, int n2,
+                                       void* scratch, size_t scratch_bytes, void* stream) {
+  if (oaa_status_t st = check_plan(p, true)) return st;
+  if (!w1 || !w2 || !scratch) return fail(OAA_ERR_INVALID_ARG, "w1, w2 and scratch must be non-NULL");
+  if (J < 1 || n1 < 1 || n2 < 1) return fail(OAA_ERR_INVALID_ARG, "J=%d, n1=%d, n2=%d must be >= 1", J, n1, n2);
+  if (n1 + n2 - 1 != p->n)
+    return fail(OAA_ERR_INVALID_ARG, "the stacked kernels make a kernel of side n1 + n2 - 1 = %d; the plan has n=%d",
+                n1 + n2 - 1, p->n);
+  if (p->fused)
+    return fail(OAA_ERR_UNSUPPORTED,
+                "the fused passes keep kernel spectra in their own layout: choose another contraction first");
+  if ((long long)J * p->C > kMaxInt || (long long)J * p->K > kMaxInt ||
+      (unsigned long long)p->F * J * (unsigned long long)std::max(p->C, p->K) > kMaxElems)
+    return fail(OAA_ERR_UNSUPPORTED, "J=%d too large", J);
+  if (reinterpret_cast<uintptr_t>(scratch) % kAlign)
+    return fail(OAA_ERR_INVALID_ARG, "scratch pointer is not %zu-byte aligned", kAlign);
+  if (scratch_bytes < chain_scratch_bytes(p, J))
+    return fail(OAA_ERR_INVALID_ARG, "scratch of %zu bytes is smaller than the %zu needed", scratch_bytes,
+                chain_scratch_bytes(p, J));
+  (void)hipGetLastError();
+  return kernel_chain(Ctx{p, p->ws, static_cast<hipStream_t>(stream), true}, w1, J, n1, w2, n2,
+                      static_cast<char*>(scratch));
 }
 
 oaa_status_t oaa_conv_forward_noalloc(oaa_plan_t p, const float* x, const float* w, float* y, void* stream) {

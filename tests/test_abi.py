@@ -402,3 +402,36 @@ int main() { all<2>(); all<4>(); all<8>(); all<16>(); all<32>(); all<64>(); }
         got = np.array([d["o"][bitrev(k, L)] for k in range(L)])
         err = np.max(np.abs(got - X)) / np.max(np.abs(X))
         assert err < 2e-6, (L, sign, zh, err)
+
+
+def test_kernel_chain_validation(lib):
+    """oaa_plan_set_kernel_chain: scratch size, and every argument error
+    before any launch (a fake device pointer is never dereferenced)."""
+    h = binding.oaa_plan_create(2, 3, 4, 20, 6)          # n = 6: n1 + n2 - 1
+    try:
+        g = binding.oaa_plan_geometry(h)
+        F, J = g["F"], 5
+        align = lambda v: (v + 255) // 256 * 256
+        need = align(F * 3 * J * 8) + align(F * J * 4 * 8)
+        assert binding.oaa_plan_chain_scratch_bytes(h, J) == need
+        assert binding.oaa_plan_chain_scratch_bytes(h, 0) == 0
+        fake = 1 << 40
+        assert lib.oaa_plan_set_kernel_chain(h, fake, J, 3, fake, 4, fake, need, None) == 3   # no workspace
+        assert lib.oaa_plan_bind_workspace(h, fake, binding.oaa_plan_workspace_bytes(h)) == 0
+        assert lib.oaa_plan_set_kernel_chain(h, fake, J, 3, fake, 3, fake, need, None) == 1   # 3 + 3 - 1 != 6
+        assert "n1 + n2 - 1" in binding.oaa_last_error_detail()
+        assert lib.oaa_plan_set_kernel_chain(h, None, J, 3, fake, 4, fake, need, None) == 1
+        assert lib.oaa_plan_set_kernel_chain(h, fake, 0, 3, fake, 4, fake, need, None) == 1
+        assert lib.oaa_plan_set_kernel_chain(h, fake, J, 3, fake, 4, fake, need - 1, None) == 1
+        assert lib.oaa_plan_set_kernel_chain(h, fake, J, 3, fake, 4, fake + 8, need, None) == 1  # alignment
+    finally:
+        binding.oaa_plan_destroy(h)
+    h = binding.oaa_plan_create_tiled(64, 3, 64, 224, 7, 64, 58)   # fused passes by default
+    try:
+        fake = 1 << 40
+        assert lib.oaa_plan_bind_workspace(h, fake, binding.oaa_plan_workspace_bytes(h)) == 0
+        need = binding.oaa_plan_chain_scratch_bytes(h, 8)
+        assert lib.oaa_plan_set_kernel_chain(h, fake, 8, 4, fake, 4, fake, need, None) == 2
+        assert "fused" in binding.oaa_last_error_detail()
+    finally:
+        binding.oaa_plan_destroy(h)

@@ -392,3 +392,29 @@ def test_relerr_sees_imaginary_parts():
         relerr(z.real, z)
     with pytest.raises(AssertionError):
         relerr(z, z.real)
+
+
+@pytest.mark.parametrize("shape", [(2, 3, 4, 2, 12, 3, 4), (1, 2, 3, 5, 9, 1, 5), (1, 1, 2, 3, 10, 4, 2)])
+def test_stacked_layers_are_one_layer_of_the_composed_kernel(shape):
+    """Two stacked layers with nothing between them (the reading of the
+    Conclusion's frequency-domain layers that the library composes):
+    conv(conv(x, w1), w2) equals conv(x, w12) with w12[k][c] the sum over j
+    of the full 2-D convolutions of w2[k][j] and w1[j][c] (scipy), and the
+    error propagation through both equals that of w12."""
+    B, C, J, K, N, n1, n2 = shape
+    rng = np.random.default_rng(sum(shape))
+    x = rng.uniform(-1, 1, (B, C, N, N))
+    w1 = rng.standard_normal((J, C, n1, n1))
+    w2 = rng.standard_normal((K, J, n2, n2))
+    n = n1 + n2 - 1
+    w12 = np.zeros((K, C, n, n))
+    for k in range(K):
+        for c in range(C):
+            for j in range(J):
+                w12[k, c] += scipy.signal.convolve2d(w2[k, j], w1[j, c], mode="full")
+    y = oracle.conv_forward(oracle.conv_forward(x, w1), w2)
+    assert relerr(y, oracle.conv_forward(x, w12)) < 1e-12
+    g = rng.uniform(-1, 1, y.shape)
+    N1 = N - n1 + 1
+    dx = oracle.conv_backward_data(oracle.conv_backward_data(g, w2, N1), w1, N)
+    assert relerr(dx, oracle.conv_backward_data(g, w12, N)) < 1e-12

@@ -513,6 +513,43 @@ def test_full_size_layers(gpu_lib, name, tiling):
     check_full_size(name, y, dx, dw, label=f"{name} {tiling} {y.shape}")
 
 
+CHAIN = [  # (B, C, J, K, N, n1, n2, tiling, method): two stacked layers composed in the frequency domain
+    (2, 3, 5, 4, 20, 3, 4, "paper", "oaa"),        # L = 16, vector-ALU composition
+    (2, 40, 36, 48, 24, 3, 3, "paper", "oaa"),     # matrix-core composition and passes
+    (2, 2, 3, 5, 100, 9, 8, (64, 49), "oaa"),      # L = 64 transforms (unfused)
+    (1, 3, 4, 2, 70, 20, 14, (128, 0), "oas"),     # L = 128, overlap-save
+    (3, 1, 1, 1, 9, 1, 1, "paper", "oaa"),         # 1 x 1 kernels: pure channel mixing
+]
+
+
+@pytest.mark.parametrize("shape", CHAIN, ids=lambda s: "x".join(map(str, s[:7])) + f"-{s[8]}")
+def test_kernel_chain_two_stacked_layers(gpu_lib, shape):
+    """oaa_plan_set_kernel_chain: the forward pass gives conv(conv(x, w1), w2)
+    and the error propagation the gradient through both layers, compared
+    whole with the oracle's two layers one after the other."""
+    B, C, J, K, N, n1, n2, tiling, method = shape
+    rng = np.random.default_rng(sum(shape[:7]))
+    x = rng.uniform(-1, 1, (B, C, N, N)).astype(np.float32)
+    w1 = (rng.standard_normal((J, C, n1, n1)) / np.sqrt(C * n1 * n1)).astype(np.float32)
+    w2 = (rng.standard_normal((K, J, n2, n2)) / np.sqrt(J * n2 * n2)).astype(np.float32)
+    n = n1 + n2 - 1
+    M = N - n + 1
+    g = rng.uniform(-1, 1, (B, K, M, M)).astype(np.float32)
+    m = binding.METHOD_OVERLAP_SAVE if method == "oas" else binding.METHOD_OVERLAP_ADD
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=tiling, method=m)
+    assert plan.geometry["fused"] == 0
+    plan.set_kernel_chain(to_dev(w1), to_dev(w2))
+    y = plan.forward(to_dev(x), None)
+    dx = plan.backward_data(to_dev(g), None)
+    torch.cuda.synchronize()
+    x64, w164, w264, g64 = (a.astype(np.float64) for a in (x, w1, w2, g))
+    y_ref = oracle.conv_forward(oracle.conv_forward(x64, w164), w264)
+    dx_ref = oracle.conv_backward_data(oracle.conv_backward_data(g64, w264, N - n1 + 1), w164, N)
+    e = (relerr(y.cpu().numpy(), y_ref), relerr(dx.cpu().numpy(), dx_ref))
+    print(f"chain {shape}: L={plan.geometry['L']} rel err fwd {e[0]:.2e} bwd_data {e[1]:.2e}", flush=True)
+    assert max(e) <= TOL, e
+
+
 def test_stage_spectra_match_oracle_steps(gpu_lib):
     """Workspace spectra (kernel, input blocks, gradient windows, products)
     against the OaA steps of the oracle, in the layouts oaa.h documents."""

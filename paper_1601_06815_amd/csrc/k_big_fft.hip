@@ -150,7 +150,8 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
   const int q2 = (tid >> 1) % p.TQ, u = (tid >> 1) / p.TQ;
   float zr[H2], zi[H2];
 
-  auto load = [&](long gg) {
+  // part 0: columns j (zr), 1: columns j + L/2 (zi), 2: both
+  auto load = [&](long gg, int part) {
     const int ch = int(gg / p.ngrp), t0 = int(gg % p.ngrp) * p.TQ;
     const int nq = min(p.TQ, tpc - t0);
     if (q1 >= nq) return;
@@ -167,18 +168,18 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
     for (int i = 0; i < H2; ++i) {
       const int gr = gr0 + i;
       const bool okr = i < lim && unsigned(gr) < unsigned(p.H);
-      zr[i] = buffer_load_f1(rs, okr && oka ? unsigned(gr * p.H + ca) * 4u : kOutOfRange);
-      zi[i] = buffer_load_f1(rs, okr && okb ? unsigned(gr * p.H + cb) * 4u : kOutOfRange);
+      if (part != 1) zr[i] = buffer_load_f1(rs, okr && oka ? unsigned(gr * p.H + ca) * 4u : kOutOfRange);
+      if (part != 0) zi[i] = buffer_load_f1(rs, okr && okb ? unsigned(gr * p.H + cb) * 4u : kOutOfRange);
     }
   };
 
   const GroupWalk wk = group_walk(ngroups, false);
   long g = wk.g;
-  if (PF && g < wk.end) load(g);
+  if (PF && g < wk.end) load(g, 2);
   for (; g < wk.end; g += wk.step) {
     const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
     const int nq = min(p.TQ, tpc - t0);
-    if (!PF) load(g);
+    if (!PF) load(g, 2);
     if (q1 < nq) {
       fft_dif_split<L, -1>(zr, zi, h);  // lane h: Z[2m + h] at bitrev(m)
       float2* bq = lds + q1 * TSZ;
@@ -206,8 +207,16 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
         bq[H2 + 1 + j] = make_float2(b0, zi[ph]);
       }
     }
+    // The next group's windows load during pass 2, in two halves: a lane's
+    // 64 loads exceed the 63 vector memory instructions a wave can have in
+    // flight, and issued at once they stall the wave (and queue this pass's
+    // stores behind them). Half goes out before the barrier, half after it
+    // (measured at the large-kernel layer, gradient windows: all 64 after
+    // the barrier 0.69 ms, all before it 0.66 ms, split 0.56 ms).
+    const bool nxt = PF && g + wk.step < wk.end;
+    if (nxt) load(g + wk.step, 0);
     __syncthreads();
-    if (PF && g + wk.step < wk.end) load(g + wk.step);  // in flight during pass 2
+    if (nxt) load(g + wk.step, 1);
     if (q2 < nq && u < H2) {
       const float2* row = lds + q2 * TSZ + u * RS + h * (H2 + 1);
       float re[H2], im[H2];

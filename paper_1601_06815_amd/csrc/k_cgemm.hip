@@ -15,11 +15,11 @@
 // next slice loaded into registers while the current one is consumed:
 //  * vector ALU: 64 x 64 complex tile per 256-lane workgroup, 4 x 4 complex
 //    accumulators per lane, four real multiply-adds per complex one;
-//  * fp32 matrix cores (v_mfma_f32_16x16x4f32): 128 x 64 (or 96 x 64)
-//    complex tile per workgroup, persistent workgroups walking the tiles in
-//    XCD-local rounds, operands read through buffer resources, LDS slices
-//    laid out so that one 16-byte read serves four matrix-core steps, and
-//    three real products per complex multiply-add (Gauss's form).
+//  * fp32 matrix cores (v_mfma_f32_16x16x4f32): 128 x 64 (or 96 x 64, or
+//    64 x 96) complex tile per workgroup, persistent workgroups walking the
+//    tiles in XCD-local rounds, operands read through buffer resources, LDS
+//    slices laid out so that one 16-byte read serves four matrix-core steps,
+//    and three real products per complex multiply-add (Gauss's form).
 #include <algorithm>
 
 #include "buffer_io.hpp"
@@ -505,10 +505,18 @@ hipError_t launch_mfma_shape(const GemmParams& p, hipStream_t s) {
 }
 
 // Row tile of 96 when that wastes less than 128 does (e.g. 96 channels).
+// Where the rows are a multiple of 64 and 96-wide column tiles waste less
+// than 64-wide ones, 64 x 96 tiles (e.g. the large-kernel layer's forward
+// product: 288 tiles per bin, the fifth 64-wide column tile half empty;
+// 0.89 -> 0.86 ms). A 96 x 96 tile would need more than the 256 registers
+// of two workgroups per CU.
 template <bool AT, bool AC, bool BT, bool BC>
 hipError_t launch_mfma(const GemmParams& p, hipStream_t s) {
   const long waste128 = (long)((p.M + 127) / 128) * 128 - p.M;
   const long waste96 = (long)((p.M + 95) / 96) * 96 - p.M;
+  const long wasteN64 = (long)((p.N + 63) / 64) * 64 - p.N;
+  const long wasteN96 = (long)((p.N + 95) / 96) * 96 - p.N;
+  if (p.M % 64 == 0 && wasteN96 < wasteN64) return launch_mfma_shape<2, 3, AT, AC, BT, BC>(p, s);
   if (waste96 < waste128) return launch_mfma_shape<3, OAA_GEMM_NB, AT, AC, BT, BC>(p, s);
   return launch_mfma_shape<4, OAA_GEMM_NB, AT, AC, BT, BC>(p, s);
 }

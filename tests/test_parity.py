@@ -86,6 +86,19 @@ def test_contraction_variants(gpu_lib, contraction, shape):
     check_whole(x, w, g, contraction)
 
 
+@pytest.mark.parametrize("shape", [
+    (4, 40, 128, 60, 9, 32, 24),    # forward rows (K = 128) in 128-row tiles
+    (4, 96, 40, 60, 9, 32, 24),     # error-propagation rows (C = 96) in 96-row tiles
+    (10, 32, 64, 100, 16, 64, 49),  # B P = 90 columns: 64 x 96 tiles (forward)
+], ids=lambda s: "x".join(map(str, s)))
+def test_matrix_core_tile_shapes(gpu_lib, shape):
+    """The matrix-core contraction's tile shapes (128 x 64, 96 x 64, 64 x 96),
+    forced, against the oracle, compared whole."""
+    B, C, K, N, n, L, b = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=31 + sum(shape))
+    check_whole(x, w, g, binding.CONTRACTION_MFMA, tiling=(L, b))
+
+
 NARROW = [  # C <= 4: odd and even tile counts, K off multiples of 16, K > 64, K > 256, split reduction
     (1, 1, 1, 9, 3),
     (2, 2, 17, 13, 4),

@@ -404,11 +404,15 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_fwd_kernel(FusedFwdPara
           const int j = min(lane + 64 * ch, M - 1);
           acc[ch] = __builtin_fmaf(cw, crow[j], __builtin_fmaf(m0[ch], lrow[o0[ch]], m1[ch] * lrow[o1[ch]]));
         }
+        // the output is written once and not read here: non-temporal stores
+        // keep it from evicting the spectra the other items of this image
+        // and kernel read (measured at the 224 x 224 RGB layer: 0.78 ->
+        // 0.72 ms)
 #pragma unroll
         for (int ch = 0; ch < MCH; ++ch) {
           if (ch >= nch) break;
           const int j = lane + 64 * ch;
-          if (j < M) orow[j] = acc[ch];
+          if (j < M) __builtin_nontemporal_store(acc[ch], orow + j);
         }
       }
       lds_barrier();  // the carry has been read
@@ -432,7 +436,7 @@ __global__ void __launch_bounds__(Fz<NS>::threads) fused_fwd_kernel(FusedFwdPara
           const int j = lane + 64 * ch;
           if (j < M) {
             if (last)
-              orow[j] = acc[ch];
+              __builtin_nontemporal_store(acc[ch], orow + j);
             else
               crow[j] = acc[ch];
           }

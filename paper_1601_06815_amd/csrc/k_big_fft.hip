@@ -3,25 +3,25 @@
 // block results; Section 3.3 for the transform sides of large kernels), as
 // used for large blocks (b up to L - n + 1) and large kernels.
 //
-// Each L-point transform is split over a pair of neighbouring lanes
-// (fft_dif_split): a lane holds L/2 complex values, about 64 registers at
-// L = 64. A workgroup keeps the intermediate of TQ tiles in LDS (17 KB per
-// tile at L = 64, so one workgroup of up to nine tiles per CU) and walks over
-// groups of TQ consecutive tiles of one channel:
-//  * forward: pass 1 transforms the column pairs (s, s + L/2) of every window
-//    along its rows, lanes over consecutive columns so that the loads of a
-//    row are coalesced, and keeps rows u <= L/2 of the two real columns'
-//    spectra (rows past L/2 are their conjugates); pass 2 transforms each of
-//    those rows along the columns and writes bins (u, v) and (L - u, v) of
-//    the half spectrum with lanes over the group's tiles, so that a store
-//    instruction writes runs of TQ consecutive tiles of a bin;
+// A workgroup keeps the intermediate of TQ tiles in LDS (17 KB per tile at
+// L = 64, so one workgroup of up to nine tiles per CU) and walks over groups
+// of TQ consecutive tiles of one channel:
+//  * forward: each L-point transform is split over a pair of neighbouring
+//    lanes (fft_dif_split, L/2 complex values per lane). Pass 1 transforms
+//    the column pairs (s, s + L/2) of every window along its rows, lanes over
+//    consecutive columns so that the loads of a row are coalesced, and keeps
+//    rows u <= L/2 of the two real columns' spectra (rows past L/2 are their
+//    conjugates); pass 2 transforms each of those rows along the columns and
+//    writes bins (u, v) and (L - u, v) of the half spectrum with lanes over
+//    the group's tiles, so that a store instruction writes runs of TQ
+//    consecutive tiles of a bin. The next group's input is loaded into
+//    registers while the current group's second pass runs.
 //  * inverse: pass 1 inverts the columns v <= L/2 (loads in runs of TQ
 //    tiles), pass 2 inverts row pairs to real rows, pass 3 writes the kept
-//    part of each tile (crop) or the overlap-added plane.
+//    part of each tile (crop) or the overlap-added plane. At L = 64 a lane
+//    holds a whole sequence (big_irfft2_lane_kernel); at L = 128 a lane pair.
 // Consecutive groups run on one XCD at about the same time, so the runs that
-// neighbouring groups write into a bin meet in that XCD's L2. The next
-// group's input is loaded into registers while the current group's second
-// pass runs.
+// neighbouring groups write into a bin meet in that XCD's L2.
 #include <algorithm>
 #include <type_traits>
 
@@ -62,26 +62,9 @@ template <int L, bool PF>
 constexpr int big_threads() {
   return L == 64 && !PF ? 576 : 512;
 }
-// The inverse without the prefetch (planes of nine tiles, overlap-added in
-// one workgroup) also takes eight waves: with nine, a lane's registers are
-// capped at 168 and the passes spill (measured at the large-kernel layer:
-// 0.99 ms with 512 threads, some looping over a second task, against 1.40 ms
-// with 576).
-#ifndef OAA_BIG_INV_PF_BATCH
-#define OAA_BIG_INV_PF_BATCH 0
-#endif
-#ifndef OAA_BIG_INV_PF_THREADS
-#define OAA_BIG_INV_PF_THREADS 512
-#endif
-// the inverse: with the prefetch, nine tiles (a plane of 3 x 3 blocks) at
-// L = 64 take 576 threads
-#ifndef OAA_BIG_INV_THREADS
-#define OAA_BIG_INV_THREADS 512
-#endif
-template <int L, bool PF>
-constexpr int big_inv_threads() {
-  return L == 64 ? (PF ? OAA_BIG_INV_PF_THREADS : OAA_BIG_INV_THREADS) : 512;
-}
+// threads of an inverse workgroup: eight waves (a lane's registers capped
+// at 256)
+constexpr int kBigInvThreads = 512;
 
 // LDS per tile (complex elements, odd)
 template <int L>
@@ -266,6 +249,67 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
   }
 }
 
+// Output of a group that is one whole plane, from its real tiles in LDS (tile
+// q at float offset 2 q TSZ, row r of a tile at 2 r RI): output pixel (i, j)
+// is framed pixel (i + off, j + off), the sum of at most two tiles per side,
+// added in a fixed order. A wave per output row, lanes over the columns. Each
+// lane's column offsets in the (at most two) tiles covering its columns, with
+// 0/1 weights, are taken once per plane, so that the reads of a row need no
+// per-lane branch; the tile rows covering a row are the same for the whole
+// wave. RAW: rows and columns are at their inverse index r, kept index
+// (r + rot) mod L, and hold L^2 times the values; else at kept index, scaled.
+template <int L, bool RAW>
+__device__ __forceinline__ void overlap_plane_out(const BigInvParams& p, const float* ldf, int TSZ, int ch, int t0,
+                                                  int wave, int lane, int nwave) {
+  constexpr int RI = Big<L>::RI;
+  const int H = p.H, KR = p.KR, P = p.T * p.T;
+  // stored index of kept index k
+  auto at = [&](int k) { return RAW ? (k - p.rot) & (L - 1) : k; };
+  const float wt = RAW ? 1.0f / float(L * L) : 1.0f;
+  const int img = t0 / P, T = p.T, b = p.pitch;
+  float* out = p.dst + (size_t(img) * p.n_ch + ch) * H * H;
+  const SmallDiv div_b(b);
+  constexpr int MCH = (L * Big<L>::SIDE_MAX + 63) / 64;  // H < T b <= L T
+  int o0[MCH], o1[MCH];
+  float m0[MCH], m1[MCH];
+  int ln = lane;  // opaque: the offsets are not kept across the group loop
+  asm volatile("" : "+v"(ln));
+#pragma unroll
+  for (int k = 0; k < MCH; ++k) {
+    const int jx = ln + 64 * k, c = jx + p.off, Q1 = div_b(c), ca1 = c - Q1 * b;
+    const bool in = jx < H;
+    const bool v1 = in && Q1 < T, v0 = in && Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR;
+    o0[k] = v0 ? (Q1 - 1) * TSZ * 2 + at(ca1 + b) : 0;
+    o1[k] = v1 ? Q1 * TSZ * 2 + at(ca1) : 0;
+    m0[k] = v0 ? 1.f : 0.f;
+    m1[k] = v1 ? 1.f : 0.f;
+  }
+  const int nch = (H + 63) / 64;
+  for (int i = wave; i < H; i += nwave) {
+    const int a = i + p.off, P1 = div_b(a), ra1 = a - P1 * b;
+    // tile rows covering framed row a: P1 (row ra1) and P1 - 1 (row ra1 + b)
+    const bool r1 = P1 < T, r0 = P1 >= 1 && P1 - 1 < T && ra1 + b < KR;
+    const float* l1 = ldf + (r1 ? 2 * (P1 * T * TSZ + at(ra1) * RI) : 0);
+    const float* l0 = ldf + (r0 ? 2 * ((P1 - 1) * T * TSZ + at(ra1 + b) * RI) : 0);
+    const float w0 = r0 ? wt : 0.f, w1 = r1 ? wt : 0.f;
+    float* orow = out + size_t(i) * H;
+    float acc[MCH];
+#pragma unroll
+    for (int k = 0; k < MCH; ++k) {
+      if (k >= nch) break;
+      const float t0v = __builtin_fmaf(m0[k], l0[o0[k]], m1[k] * l0[o1[k]]);
+      const float t1v = __builtin_fmaf(m0[k], l1[o0[k]], m1[k] * l1[o1[k]]);
+      acc[k] = __builtin_fmaf(w0, t0v, w1 * t1v);
+    }
+#pragma unroll
+    for (int k = 0; k < MCH; ++k) {
+      if (k >= nch) break;
+      const int jx = lane + 64 * k;
+      if (jx < H) orow[jx] = acc[k];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // inverse: half spectra -> kept part of every tile (crop), or the plane the
 // tiles overlap-add to
@@ -279,8 +323,8 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
 // MODE: the kernel's pass 3 (0 crop, 1 overlap-add of one-group planes, 2
 // tiles to the scratch), fixed per instance so that each carries only the
 // registers of its own output code.
-template <int L, bool O32, bool PF, int MODE>
-__global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(BigInvParams p) {
+template <int L, bool O32, int MODE>
+__global__ void __launch_bounds__(kBigInvThreads) big_irfft2_kernel(BigInvParams p) {
   constexpr int H2 = Big<L>::H2, V = Big<L>::V, RI = Big<L>::RI;
   extern __shared__ float smem[];
   float2* lds = reinterpret_cast<float2*>(smem);
@@ -294,8 +338,7 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
   const int npair = (KR + 1) / 2;
   const float scale = 1.0f / float(L * L);
   // tasks of passes 1 and 2: h + 2 (q + TQ w), tile q fastest; w is the
-  // column (pass 1) or the row pair (pass 2). With the prefetch, each thread
-  // has one task per pass (the launcher gives L TQ threads).
+  // column (pass 1) or the row pair (pass 2); threads loop over the tasks
   float zr[H2], zi[H2];
 
   // Column w of tile q, rows [h L/2, h L/2 + L/2), summed over the split
@@ -382,7 +425,7 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
       // lane 0: a.x - b.y, a.y + b.x; lane 1: a.x + b.y, b.x - a.y
       xr[i] = __builtin_fmaf(sg * keep1, bb.y, a.x);
       xi[i] = __builtin_fmaf(-sg, a.y, keep1 * bb.x);
-      if (!PF && i % 8 == 7) asm volatile("" ::: "memory");  // bounds the reads in flight
+      if (i % 8 == 7) asm volatile("" ::: "memory");  // bounds the reads in flight
     }
     fft_dif_split<L, +1>(xr, xi, h);  // lane h: L row0[s], L row1[s] at s = 2m + h, position bitrev(m)
     float* d0 = smem + 2 * zo;
@@ -396,32 +439,17 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
     }
   };
 
-  const int tq0 = (tid >> 1) % p.TQ, tw0 = (tid >> 1) / p.TQ;  // this thread's first task
   const GroupWalk wk = group_walk(ngroups, true);
-  long g = wk.g;
-  if (PF && g < wk.end) {
-    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
-    if (tq0 < min(p.TQ, tpc - t0) && tw0 < H2) load(ch, t0, tq0, tw0);
-  }
-  for (; g < wk.end; g += wk.step) {
+  for (long g = wk.g; g < wk.end; g += wk.step) {
     const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * p.TQ;
     const int nq = min(p.TQ, tpc - t0);
-    if (PF) {
-      if (tq0 < nq && tw0 < H2) column(tq0, tw0);
-    } else {
-      for (int task = tid; task < L * p.TQ; task += nthr) {
-        const int q = (task >> 1) % p.TQ, w = (task >> 1) / p.TQ;
-        if (q >= nq) continue;
-        load(ch, t0, q, w);
-        column(q, w);
-      }
+    for (int task = tid; task < L * p.TQ; task += nthr) {
+      const int q = (task >> 1) % p.TQ, w = (task >> 1) / p.TQ;
+      if (q >= nq) continue;
+      load(ch, t0, q, w);
+      column(q, w);
     }
     __syncthreads();
-    if (PF && g + wk.step < wk.end) {  // in flight during passes 2 and 3
-      const long gn = g + wk.step;
-      const int chn = int(gn / p.ngrp), t0n = int(gn % p.ngrp) * p.TQ;
-      if (tq0 < min(p.TQ, tpc - t0n) && tw0 < H2) load(chn, t0n, tq0, tw0);
-    }
     for (int task = tid; task < 2 * npair * p.TQ; task += nthr) {
       const int q = (task >> 1) % p.TQ, w = (task >> 1) / p.TQ;
       if (q < nq) rows(q, w);
@@ -457,55 +485,188 @@ __global__ void __launch_bounds__((big_inv_threads<L, PF>())) big_irfft2_kernel(
         }
       }
     } else {
-      // the group is one whole plane: output pixel (i, j) is framed pixel
-      // (i + off, j + off), the sum of at most two tiles per side, added in
-      // a fixed order. A wave per output row, lanes over the columns. Each
-      // lane's column offsets in the (at most two) tiles covering its
-      // columns, with 0/1 weights, are taken once per plane, so that the
-      // reads of a row need no per-lane branch; the tile rows covering a
-      // row are the same for the whole wave.
-      const int img = t0 / P, T = p.T, b = p.pitch;
-      float* out = p.dst + (size_t(img) * p.n_ch + ch) * H * H;
-      const SmallDiv div_b(b);
-      constexpr int MCH = (L * Big<L>::SIDE_MAX + 63) / 64;  // H < T b <= L T
-      int o0[MCH], o1[MCH];
-      float m0[MCH], m1[MCH];
-      int ln = lane;  // opaque: the offsets are not kept across the group loop
-      asm volatile("" : "+v"(ln));
+      overlap_plane_out<L, false>(p, ldf, TSZ, ch, t0, wave, lane, nwave);
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// inverse at L = 64 with a whole 64-point sequence per lane: a lane inverts
+// one column of a tile (pass 1), then one pair of rows (pass 2), in 128
+// registers, where the kernel above splits each sequence over a lane pair.
+// No first stage runs across a pair (about 0.7 of the vector instructions
+// per transform), and the 32 tasks per tile and pass of a group take 4 (8
+// tiles) or 4.5 (a nine-tile plane) waves of the eight.
+//
+// Rows and columns stay in LDS at their inverse index r (kept index
+// (r + rot) mod L), in tiles of L x (L/2 + 1) slots, so that every LDS
+// address is a compile-time offset from the task's base; passes 1 and 2
+// write every row and column (skipping the ones nothing reads, under
+// conditions that are uniform, makes the compiler keep more of the
+// transform's values live across the stores, and spill), pass 2 runs on the
+// row pairs that hold kept rows only, and the output pass applies the
+// rotation and the 1/L^2 scale. MODE as for the kernel above; SPLIT: more than one partial
+// spectrum to sum (the weight gradient's split), loaded in batches of 16
+// rows so that the partial sums and the loads in flight fit the registers.
+template <bool O32, int MODE, bool SPLIT>
+__global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
+  constexpr int L = 64, H2 = L / 2, V = L / 2 + 1, RI = Big<L>::RI;
+  extern __shared__ float smem[];
+  float2* lds = reinterpret_cast<float2*>(smem);
+  const float* ldf = smem;
+  const int KR = p.KR, rot = p.rot, TQ = p.TQ;
+  const int TSZ = inv_tile_stride<L>(L);
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int P = p.T * p.T, tpc = p.n_img * P;
+  const size_t fstride = size_t(p.n_ch) * tpc;
+  const long ngroups = long(p.n_ch) * p.ngrp;
+  // the stored rows (k - rot) mod L of kept rows k < KR are a cyclic run
+  // from s0; the row pairs w0, w0 + 1, ... (mod L/2) cover it
+  const int s0 = (L - rot) & (L - 1), w0 = s0 >> 1, npair = min(H2, ((s0 & 1) + KR + 1) >> 1);
+  using off_t = typename std::conditional<O32, unsigned, size_t>::type;
+  auto at = [&](const float2* base, off_t e) { return O32 ? load_at(base, unsigned(e) * 8u) : base[e]; };
+
+  // pass 1: column w of tile q (summed over the partial spectra); column 0
+  // carries the real columns 0 and L/2 together as h0[u] + i h1[u], rows
+  // past L/2 rebuilt as the conjugates of rows L - u (not stored)
+  auto column = [&](int ch, int t0, int q, int w) {
+    float re[L], im[L];
+    const size_t tb = size_t(ch) * tpc + t0 + q;
+    const off_t row = off_t(size_t(V) * fstride);
+    // rows [u0, u0 + NU) of one partial: assigned (first) or added
+    auto gather = [&](const float2* base, int u0c, auto nu, auto first) {
+      constexpr int NU = decltype(nu)::value;
+      constexpr bool FIRST = decltype(first)::value;
+      const int u0 = u0c;
+      if (w > 0) {
+        off_t e = off_t((size_t(u0) * V + w) * fstride + tb);
+        if (O32) asm volatile("" : "+v"(e));
 #pragma unroll
-      for (int k = 0; k < MCH; ++k) {
-        const int jx = ln + 64 * k, c = jx + p.off, Q1 = div_b(c), ca1 = c - Q1 * b;
-        const bool in = jx < H;
-        const bool v1 = in && Q1 < T, v0 = in && Q1 >= 1 && Q1 - 1 < T && ca1 + b < KR;
-        o0[k] = v0 ? (Q1 - 1) * TSZ * 2 + ca1 + b : 0;
-        o1[k] = v1 ? Q1 * TSZ * 2 + ca1 : 0;
-        m0[k] = v0 ? 1.f : 0.f;
-        m1[k] = v1 ? 1.f : 0.f;
-      }
-      const int nch = (H + 63) / 64;
-      for (int i = wave; i < H; i += nwave) {
-        const int a = i + p.off, P1 = div_b(a), ra1 = a - P1 * b;
-        // tile rows covering framed row a: P1 (row ra1) and P1 - 1 (row ra1 + b)
-        const bool r1 = P1 < T, r0 = P1 >= 1 && P1 - 1 < T && ra1 + b < KR;
-        const float* l1 = ldf + (r1 ? 2 * (P1 * T * TSZ + ra1 * RI) : 0);
-        const float* l0 = ldf + (r0 ? 2 * ((P1 - 1) * T * TSZ + (ra1 + b) * RI) : 0);
-        const float w0 = r0 ? 1.f : 0.f, w1 = r1 ? 1.f : 0.f;
-        float* orow = out + size_t(i) * H;
-        float acc[MCH];
-#pragma unroll
-        for (int k = 0; k < MCH; ++k) {
-          if (k >= nch) break;
-          const float t0v = __builtin_fmaf(m0[k], l0[o0[k]], m1[k] * l0[o1[k]]);
-          const float t1v = __builtin_fmaf(m0[k], l1[o0[k]], m1[k] * l1[o1[k]]);
-          acc[k] = __builtin_fmaf(w0, t0v, w1 * t1v);
+        for (int i = 0; i < NU; ++i) {
+          const float2 z = at(base, e);
+          e += row;
+          re[u0 + i] = FIRST ? z.x : re[u0 + i] + z.x;
+          im[u0 + i] = FIRST ? z.y : im[u0 + i] + z.y;
         }
+      } else {
+        // rows u <= L/2 of columns 0 and L/2 give rows u and L - u
+        off_t e = off_t(size_t(u0) * V * fstride + tb);
+        if (O32) asm volatile("" : "+v"(e));
+        const off_t half = off_t(size_t(H2) * fstride);
 #pragma unroll
-        for (int k = 0; k < MCH; ++k) {
-          if (k >= nch) break;
-          const int jx = lane + 64 * k;
-          if (jx < H) orow[jx] = acc[k];
+        for (int i = 0; i < NU; ++i) {
+          const int u = u0 + i;
+          if (u > H2) break;
+          const float2 b0 = at(base, e), b1 = at(base, e + half);
+          e += row;
+          re[u] = FIRST ? b0.x - b1.y : re[u] + (b0.x - b1.y);
+          im[u] = FIRST ? b0.y + b1.x : im[u] + (b0.y + b1.x);
+          if (u > 0 && u < H2) {
+            re[L - u] = FIRST ? b0.x + b1.y : re[L - u] + (b0.x + b1.y);
+            im[L - u] = FIRST ? b1.x - b0.y : im[L - u] + (b1.x - b0.y);
+          }
         }
       }
+    };
+    if (!SPLIT) {
+      gather(p.src, 0, std::integral_constant<int, L>{}, std::true_type{});
+    } else {
+      // column 0 reads rows [0, L/2] only, which the first three batches
+      // cover (the fourth then reads nothing)
+#pragma unroll
+      for (int u0 = 0; u0 < L; u0 += 16) {
+        gather(p.src, u0, std::integral_constant<int, 16>{}, std::true_type{});
+        for (int sp = 1; sp < p.nsplit; ++sp)
+          gather(p.src + size_t(sp) * p.split_stride, u0, std::integral_constant<int, 16>{}, std::false_type{});
+        asm volatile("" ::: "memory");
+      }
+    }
+    fft_dif<L, +1, false>(re, im);  // row r at position bitrev(r)
+    float2* bq = lds + (q * TSZ + w);
+#pragma unroll
+    for (int r = 0; r < L; ++r) bq[r * RI] = make_float2(re[bitrev(r, L)], im[bitrev(r, L)]);
+  };
+  // pass 2: rows 2w, 2w + 1 to L^2 times their real rows, written over their
+  // own storage (slot 0 of a row holds its bins 0 and L/2 as (re, im))
+  auto rows = [&](int q, int w) {
+    float re[L], im[L];
+    float2* za = lds + (q * TSZ + 2 * w * RI);
+    {
+      const float2 a0 = za[0], b0 = za[RI];
+      re[0] = a0.x;
+      im[0] = b0.x;
+      re[H2] = a0.y;
+      im[H2] = b0.y;
+    }
+#pragma unroll
+    for (int v = 1; v < H2; ++v) {
+      const float2 a = za[v], bb = za[RI + v];
+      re[v] = a.x - bb.y;
+      im[v] = a.y + bb.x;
+      re[L - v] = a.x + bb.y;
+      im[L - v] = bb.x - a.y;
+    }
+    fft_dif<L, +1, false>(re, im);  // L^2 row0[s] in re, L^2 row1[s] in im, at position bitrev(s)
+    float* d0 = reinterpret_cast<float*>(za);
+#pragma unroll
+    for (int s = 0; s < L; ++s) {
+      d0[s] = re[bitrev(s, L)];
+      d0[2 * RI + s] = im[bitrev(s, L)];
+    }
+  };
+  // pass 3, MODE 0 and 2: the kept KR x KR of every tile, scaled, to its
+  // block (0) or to the scratch, tile after tile (2); a wave per tile
+  // (decoded once, wave-uniform), lanes over the block in row order
+  auto crop = [&](int ch, int t0, int nq, int wave, int lane, int nwave, auto rotated) {
+    constexpr bool ROT = decltype(rotated)::value;
+    const float scale = 1.0f / float(L * L);
+    const SmallDiv div_k(KR);
+    for (int qq = wave; qq < nq; qq += nwave) {
+      const float* lt = ldf + 2 * qq * TSZ;
+      int nrow = KR, ncol = KR;
+      float* ob;
+      int ostride;
+      if (MODE == 0) {
+        const int t = t0 + qq, img = t / P, pp = t - img * P;
+        const int pr = pp / p.T, qc = pp - pr * p.T;
+        nrow = min(KR, p.H - pr * p.pitch);
+        ncol = min(KR, p.H - qc * p.pitch);
+        ob = p.dst + ((size_t(img) * p.n_ch + ch) * p.H + pr * p.pitch) * p.H + qc * p.pitch;
+        ostride = p.H;
+      } else {
+        ob = p.tiles + ((size_t(ch) * tpc + t0 + qq) * KR) * KR;
+        ostride = KR;
+      }
+      for (int e = lane; e < KR * nrow; e += 64) {
+        const int rr = div_k(e), cc = e - rr * KR;
+        const int sr = ROT ? (rr - rot) & (L - 1) : rr, sc = ROT ? (cc - rot) & (L - 1) : cc;
+        if (cc < ncol) ob[rr * ostride + cc] = lt[2 * sr * RI + sc] * scale;
+      }
+    }
+  };
+
+  const GroupWalk wk = group_walk(ngroups, true);
+  const int wave = tid >> 6, lane = tid & 63, nwave = nthr >> 6;
+  for (long g = wk.g; g < wk.end; g += wk.step) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * TQ;
+    const int nq = min(TQ, tpc - t0);
+    for (int task = tid; task < H2 * TQ; task += nthr) {
+      const int q = task % TQ;
+      if (q < nq) column(ch, t0, q, task / TQ);
+    }
+    __syncthreads();
+    for (int task = tid; task < npair * TQ; task += nthr) {
+      const int q = task % TQ;
+      if (q < nq) rows(q, (w0 + task / TQ) & (H2 - 1));
+    }
+    __syncthreads();
+    if (MODE == 1) {
+      overlap_plane_out<L, true>(p, ldf, TSZ, ch, t0, wave, lane, nwave);
+    } else if (rot == 0) {
+      crop(ch, t0, nq, wave, lane, nwave, std::false_type{});
+    } else {
+      crop(ch, t0, nq, wave, lane, nwave, std::true_type{});
     }
     __syncthreads();
   }
@@ -623,28 +784,54 @@ hipError_t launch_big_fwd_L(BigFwdParams p, hipStream_t s) {
   else return launch_big_fwd_LP<L, false>(p, lds, ngroups, s);
 }
 
-template <int L, bool PF, int MODE>
-hipError_t launch_big_inv_LPM(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
+template <int L, int MODE>
+hipError_t launch_big_inv_LM(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
   constexpr int V = Big<L>::V;
   const bool o32 =
       (size_t(L) * V * size_t(p.n_ch) * size_t(p.n_img) * p.T * p.T + size_t(p.nsplit - 1) * p.split_stride) * 8 <
       (size_t(1) << 32);
-  auto kern = o32 ? big_irfft2_kernel<L, true, PF, MODE> : big_irfft2_kernel<L, false, PF, MODE>;
+  auto kern = o32 ? big_irfft2_kernel<L, true, MODE> : big_irfft2_kernel<L, false, MODE>;
   const hipError_t e = allow_lds(kern, kBigLds);
   if (e != hipSuccess) return e;
-  const int nthr = std::min(L * p.TQ, big_inv_threads<L, PF>());
+  const int nthr = std::min(L * p.TQ, kBigInvThreads);
   hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds, nthr)), dim3(nthr), lds, s, p);
   return hipGetLastError();
 }
 
-template <int L, bool PF>
-hipError_t launch_big_inv_LP(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
+template <int L>
+hipError_t launch_big_inv_LS(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
   switch (p.overlap) {
-    case 0: return launch_big_inv_LPM<L, PF, 0>(p, lds, ngroups, s);
-    case 1: return launch_big_inv_LPM<L, PF, 1>(p, lds, ngroups, s);
-    case 2: return launch_big_inv_LPM<L, PF, 2>(p, lds, ngroups, s);
+    case 0: return launch_big_inv_LM<L, 0>(p, lds, ngroups, s);
+    case 1: return launch_big_inv_LM<L, 1>(p, lds, ngroups, s);
+    case 2: return launch_big_inv_LM<L, 2>(p, lds, ngroups, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+// L = 64: one sequence per lane, tiles of whole L x (L/2 + 1) slots
+template <bool O32>
+hipError_t launch_big_inv_lane_O(const BigInvParams& p, size_t lds, long ngroups, hipStream_t s) {
+  void (*kern)(BigInvParams) = nullptr;
+  if (p.overlap == 0)
+    kern = p.nsplit > 1 ? big_irfft2_lane_kernel<O32, 0, true> : big_irfft2_lane_kernel<O32, 0, false>;
+  else if (p.nsplit == 1)  // the overlap-add of forward spectra: one partial
+    kern = p.overlap == 1 ? big_irfft2_lane_kernel<O32, 1, false> : big_irfft2_lane_kernel<O32, 2, false>;
+  if (!kern) return hipErrorInvalidValue;
+  const hipError_t e = allow_lds(kern, kBigLds);
+  if (e != hipSuccess) return e;
+  constexpr int nthr = 512;
+  hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds, nthr)), dim3(nthr), lds, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_big_inv_lane(const BigInvParams& p, long ngroups, hipStream_t s) {
+  constexpr int L = 64;
+  const size_t lds = size_t(inv_tile_stride<L>(L)) * p.TQ * 8;
+  if (lds > kBigLds || p.TQ > Big<L>::TQ_MAX) return hipErrorInvalidConfiguration;
+  const size_t tpc = size_t(p.n_img) * p.T * p.T;
+  const bool o32 = (size_t(L) * Big<L>::V * size_t(p.n_ch) * tpc + size_t(p.nsplit - 1) * p.split_stride) * 8 <
+                   (size_t(1) << 32);
+  return o32 ? launch_big_inv_lane_O<true>(p, lds, ngroups, s) : launch_big_inv_lane_O<false>(p, lds, ngroups, s);
 }
 
 template <int L>
@@ -676,15 +863,11 @@ hipError_t launch_big_inv_L(BigInvParams p, hipStream_t s) {
   const size_t lds = size_t(inv_tile_stride<L>(p.KR)) * p.TQ * 8;
   if (lds > kBigLds) return hipErrorInvalidConfiguration;
   const long ngroups = long(p.n_ch) * p.ngrp;
-  // the register prefetch needs one task per thread
   hipError_t e = hipSuccess;
   if constexpr (L == 64) {
-    if (L * p.TQ <= big_inv_threads<L, true>())
-      e = launch_big_inv_LP<L, true>(p, lds, ngroups, s);
-    else
-      e = launch_big_inv_LP<L, false>(p, lds, ngroups, s);
+    e = launch_big_inv_lane(p, ngroups, s);
   } else {
-    e = launch_big_inv_LP<L, false>(p, lds, ngroups, s);
+    e = launch_big_inv_LS<L>(p, lds, ngroups, s);
   }
   if (e != hipSuccess || !two_step) return e;
   // second step: about 8 rows per workgroup

@@ -6,7 +6,10 @@
 // A workgroup keeps the intermediate of TQ tiles in LDS (17 KB per tile at
 // L = 64, so one workgroup of up to nine tiles per CU) and walks over groups
 // of TQ consecutive tiles of one channel:
-//  * forward: each L-point transform is split over a pair of neighbouring
+//  * forward: at L = 64 a lane holds a whole sequence and the two halves of
+//    the workgroup alternate between transforming a group and loading the
+//    next (big_rfft2_lane_kernel); at L = 128, and for launches of few
+//    groups, each L-point transform is split over a pair of neighbouring
 //    lanes (fft_dif_split, L/2 complex values per lane). Pass 1 transforms
 //    the column pairs (s, s + L/2) of every window along its rows, lanes over
 //    consecutive columns so that the loads of a row are coalesced, and keeps
@@ -245,6 +248,145 @@ __global__ void __launch_bounds__((big_threads<L, PF>())) big_rfft2_kernel(BigFw
         }
       }
     }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// forward at L = 64 with a whole 64-point sequence per lane: a lane
+// transforms one column pair (j, j + L/2) of a window along its rows (pass
+// 1), then one LDS row along the columns (pass 2). The separations, the LDS
+// layout and the bins written are those of the kernel above; without the
+// first stage across a lane pair a transform takes about 0.7 of the vector
+// instructions. The 32 tasks per tile and pass of a group of eight tiles fill
+// four waves, half the workgroup, and the halves alternate: while one
+// transforms group i, the other loads the windows of group i + 1 into its
+// registers, so the loads have a whole group's passes to arrive. A half's
+// pass 2 works in the registers that held its windows.
+//
+// A wave holds the column pairs of two tiles, possibly of two images, and a
+// buffer resource must be the same for the whole wave: the window rows come
+// through one resource per group, over the planes of channel ch of the
+// group's images. WIDE: spans of the planes or spectra past 32-bit offsets,
+// through 64-bit addresses.
+template <bool WIDE>
+__global__ void __launch_bounds__(512) big_rfft2_lane_kernel(BigFwdParams p) {
+  constexpr int L = 64, H2 = L / 2, V = L / 2 + 1, RS = Big<L>::RS;
+  extern __shared__ float smem[];
+  float2* lds = reinterpret_cast<float2*>(smem);
+  const int TSZ = fwd_tile_stride<L>();
+  const int tid = threadIdx.x, TQ = p.TQ;
+  const int half = tid >> 8, ht = tid & 255;  // half of the workgroup (four waves), thread in it
+  const int P = p.T * p.T, tpc = p.n_img * P;
+  const size_t bs = p.bs;
+  const long ngroups = long(p.n_ch) * p.ngrp;
+  const size_t HH = size_t(p.H) * p.H, istride = size_t(p.n_ch) * HH;  // floats per plane, per image
+  // this thread's tasks: pass 1 tile q1, column pair j (lanes over consecutive
+  // columns: coalesced window rows); pass 2 tile q2, LDS row u (lanes over
+  // the tiles: runs of consecutive tiles of a bin)
+  const int q1 = ht / H2, j = ht % H2, q2 = ht % TQ, u = ht / TQ;
+  float zr[L], zi[L];
+
+  // the windows of group g: columns j and j + L/2 of tile q1 as
+  // z = x[., j] + i x[., j + L/2]
+  auto fetch = [&](long g) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * TQ;
+    const int nq = min(TQ, tpc - t0);
+    if (q1 >= nq) return;
+    const int img0 = t0 / P, img1 = (t0 + nq - 1) / P;
+    const float* base = p.src + (size_t(img0) * p.n_ch + ch) * HH;
+    const __amdgpu_buffer_rsrc_t rs =
+        buffer_resource(base, WIDE ? 0u : unsigned((size_t(img1 - img0) * istride + HH) * 4));
+    const int t = t0 + q1, img = t / P, pp = t - img * P;
+    const int pr = pp / p.T, qc = pp - pr * p.T;
+    const int gr0 = pr * p.pitch - p.off;
+    const int ca = qc * p.pitch - p.off + j, cb = ca + H2;
+    const bool oka = j < p.S && unsigned(ca) < unsigned(p.H);
+    const bool okb = j + H2 < p.S && unsigned(cb) < unsigned(p.H);
+    const unsigned pb = unsigned(size_t(img - img0) * istride);  // this tile's plane in rs (elements)
+    const float* plane = p.src + (size_t(img) * p.n_ch + ch) * HH;
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int gr = gr0 + i;
+      const bool okr = i < p.S && unsigned(gr) < unsigned(p.H);
+      if (WIDE) {
+        zr[i] = okr && oka ? plane[size_t(gr) * p.H + ca] : 0.f;
+        zi[i] = okr && okb ? plane[size_t(gr) * p.H + cb] : 0.f;
+      } else {
+        zr[i] = buffer_load_f1(rs, okr && oka ? (pb + unsigned(gr * p.H + ca)) * 4u : kOutOfRange);
+        zi[i] = buffer_load_f1(rs, okr && okb ? (pb + unsigned(gr * p.H + cb)) * 4u : kOutOfRange);
+      }
+    }
+  };
+  // pass 1 on the fetched windows: the real columns' spectra
+  // C_j[u] = (Z[u] + conj Z[L - u]) / 2, C_{j+L/2}[u] = (Z[u] - conj Z[L - u]) / (2i),
+  // rows u <= L/2; rows 0 and L/2 (real) share LDS row 0 as (re, im)
+  auto columns = [&]() {
+    fft_dif<L, -1, false>(zr, zi);  // Z[k] at position bitrev(k)
+    float2* bq = lds + (q1 * TSZ + j);
+#pragma unroll
+    for (int v = 1; v < H2; ++v) {
+      const float a = zr[bitrev(v, L)], b = zi[bitrev(v, L)];
+      const float c = zr[bitrev(L - v, L)], d = zi[bitrev(L - v, L)];
+      bq[v * RS] = make_float2(0.5f * (a + c), 0.5f * (b - d));
+      bq[v * RS + H2 + 1] = make_float2(0.5f * (b + d), 0.5f * (c - a));
+    }
+    bq[0] = make_float2(zr[0], zr[bitrev(H2, L)]);
+    bq[H2 + 1] = make_float2(zi[0], zi[bitrev(H2, L)]);
+  };
+  // pass 2: LDS row u of tile q2 along the columns; bins (u, v), v <= L/2,
+  // and (L - u, v) = conj X[u][L - v], 0 < v < L/2; the packed row 0 gives
+  // rows 0 and L/2 by the separation of pass 1
+  auto row = [&](int ch, int t0) {
+    const float2* zrow = lds + (q2 * TSZ + u * RS);
+#pragma unroll
+    for (int c = 0; c < H2; ++c) {
+      const float2 a = zrow[c], b = zrow[H2 + 1 + c];
+      zr[c] = a.x;
+      zi[c] = a.y;
+      zr[H2 + c] = b.x;
+      zi[H2 + c] = b.y;
+    }
+    fft_dif<L, -1, false>(zr, zi);  // Y[v] at position bitrev(v)
+    const int t = t0 + q2;
+    const size_t tb = size_t(ch) * p.cs + size_t(t / p.run) * p.rs + size_t(t % p.run);
+    auto put = [&](int r, int v, float2 val) {
+      if (!WIDE) {
+        store_at(p.dst, unsigned((size_t(r) * V * bs + tb) * 8u) + unsigned(v) * unsigned(bs * 8u), val);
+      } else {
+        p.dst[(size_t(r) * V + v) * bs + tb] = val;
+      }
+    };
+    if (u > 0) {
+#pragma unroll
+      for (int v = 0; v <= H2; ++v) put(u, v, make_float2(zr[bitrev(v, L)], zi[bitrev(v, L)]));
+#pragma unroll
+      for (int v = 1; v < H2; ++v) put(L - u, v, make_float2(zr[bitrev(L - v, L)], -zi[bitrev(L - v, L)]));
+    } else {
+#pragma unroll
+      for (int v = 0; v <= H2; ++v) {
+        const float a = zr[bitrev(v, L)], b = zi[bitrev(v, L)];
+        const float c = zr[bitrev((L - v) % L, L)], d = zi[bitrev((L - v) % L, L)];
+        put(0, v, make_float2(0.5f * (a + c), 0.5f * (b - d)));
+        put(H2, v, make_float2(0.5f * (b + d), 0.5f * (c - a)));
+      }
+    }
+  };
+
+  const GroupWalk wk = group_walk(ngroups, false);
+  if (half == 0 && wk.g < wk.end) fetch(wk.g);
+  int turn = 0;  // the half whose windows are in registers for this group
+  for (long g = wk.g; g < wk.end; g += wk.step, turn ^= 1) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * TQ;
+    const int nq = min(TQ, tpc - t0);
+    const bool mine = half == turn;
+    if (mine) {
+      if (q1 < nq) columns();
+    } else if (g + wk.step < wk.end) {
+      fetch(g + wk.step);
+    }
+    __syncthreads();
+    if (mine && q2 < nq && u < H2) row(ch, t0);
     __syncthreads();
   }
 }
@@ -780,8 +922,27 @@ hipError_t launch_big_fwd_L(BigFwdParams p, hipStream_t s) {
   // one task per thread (group_tiles keeps L TQ within a workgroup)
   if (lds > kBigLds || L * p.TQ > big_threads<L, true>()) return hipErrorInvalidConfiguration;
   const long ngroups = long(p.n_ch) * p.ngrp;
-  if constexpr (L == 64) return launch_big_fwd_LP<L, true>(p, lds, ngroups, s);
-  else return launch_big_fwd_LP<L, false>(p, lds, ngroups, s);
+  // at L = 64 the alternating halves need two groups or more per workgroup
+  // (one per CU) to overlap anything; smaller launches take the lane pairs
+  // (measured at the 224 x 224 RGB layer: kernel spectra, 24 groups, 0.017
+  // against 0.025 ms)
+  if constexpr (L == 64) {
+    if (ngroups < 2L * cu_count()) return launch_big_fwd_LP<L, true>(p, lds, ngroups, s);
+    constexpr int V = Big<L>::V;
+    const size_t end = size_t(L * V - 1) * p.bs + size_t(p.n_ch - 1) * p.cs + size_t((tpc - 1) / p.run) * p.rs +
+                       size_t(std::min<long>(p.run, tpc));
+    // the planes one group's windows read: tiles of at most TQ images
+    const size_t span = (size_t(p.TQ - 1) * p.n_ch + 1) * size_t(p.H) * p.H * 4;
+    const bool narrow = end * 8 < (size_t(1) << 32) && span < size_t(kOutOfRange);
+    auto kern = narrow ? big_rfft2_lane_kernel<false> : big_rfft2_lane_kernel<true>;
+    const hipError_t e = allow_lds(kern, kBigLds);
+    if (e != hipSuccess) return e;
+    constexpr int nthr = 512;  // two halves of four waves: 32 TQ <= 256 tasks per pass
+    hipLaunchKernelGGL(kern, dim3(persistent_grid(ngroups, lds, nthr)), dim3(nthr), lds, s, p);
+    return hipGetLastError();
+  } else {
+    return launch_big_fwd_LP<L, false>(p, lds, ngroups, s);
+  }
 }
 
 template <int L, int MODE>

@@ -275,6 +275,34 @@ def test_fused_spectra_layouts(gpu_lib):
     assert relerr(dWh.transpose(3, 2, 0, 1)[..., keep], oaa_oracle.backward_filter_product(Go, Xo)[..., keep]) < TOL
 
 
+def test_forward_transform_alternating_halves(gpu_lib):
+    """The L = 64 forward transform in the form that launches of 512 groups
+    or more take: the two halves of a workgroup alternate between
+    transforming a group and loading the next. The kernel, input-block and
+    gradient-window spectra against the oracle's, with 640 groups of
+    x (a partial group of four tiles per channel) and some workgroups
+    walking an odd number of groups."""
+    B, C, K, N, n, L, b = 9, 128, 128, 64, 16, 64, 49
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=29)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    geo = plan.geometry
+    T, F = geo["T"], geo["F"]
+    V = L // 2 + 1
+    assert geo["fused"] == 0 and T == 2 and C * -(-B * T * T // 8) >= 512
+    plan.forward(to_dev(x), to_dev(w))
+    plan.backward_data(to_dev(g), None)
+    torch.cuda.synchronize()
+    keep = np.ones((L, V), bool)
+    keep[L // 2 + 1:, 0] = keep[L // 2 + 1:, V - 1] = False
+    Wh = plan.region(binding.REGION_W_SPECTRUM).cpu().numpy()[:F * C * K].reshape(L, V, C, K)
+    assert relerr(Wh.transpose(3, 2, 0, 1)[..., keep], oaa_oracle.filter_spectra(w, L)[..., keep]) < TOL
+    Xh = plan.region(binding.REGION_X_SPECTRUM).cpu().numpy()[:F * C * B * T * T].reshape(L, V, C, B, T, T)
+    assert relerr(Xh.transpose(3, 2, 4, 5, 0, 1)[..., keep], oaa_oracle.block_spectra(x, n, L, b)[..., keep]) < TOL
+    Gh = plan.region(binding.REGION_G_SPECTRUM).cpu().numpy()[:F * K * B * T * T].reshape(L, V, K, B, T, T)
+    Go = oaa_oracle.window_spectra(g, n, N, L, side=min(2 * b, L), b=b)
+    assert relerr(Gh.transpose(3, 2, 4, 5, 0, 1)[..., keep], Go[..., keep]) < TOL
+
+
 BIG128 = [  # (B, C, K, N, n, L, b, method): transform side 128 (kernel sides up to 64)
     (1, 2, 3, 64, 33, 128, 33, "oaa"),     # the paper's tiling at n = 33: T = 2, overlap-add in two steps
     (1, 2, 2, 64, 48, 128, 48, "oaa"),     # T = 2

@@ -638,8 +638,13 @@ __global__ void __launch_bounds__(kBigInvThreads) big_irfft2_kernel(BigInvParams
 // one column of a tile (pass 1), then one pair of rows (pass 2), in 128
 // registers, where the kernel above splits each sequence over a lane pair.
 // No first stage runs across a pair (about 0.7 of the vector instructions
-// per transform), and the 32 tasks per tile and pass of a group take 4 (8
-// tiles) or 4.5 (a nine-tile plane) waves of the eight.
+// per transform). The 32 tasks per tile and pass of a group of eight tiles
+// fill four waves, half the workgroup, and the halves alternate: while one
+// transforms group i, the other loads the columns of group i + 1 into its
+// registers, which then have passes 2 and 3 of group i to arrive. A nine-tile
+// plane has 32 tasks per pass past the half's 256; the loading half runs
+// them (loading their columns itself) before it loads the next group.
+// Pass 3, the output, takes all eight waves.
 //
 // Rows and columns stay in LDS at their inverse index r (kept index
 // (r + rot) mod L), in tiles of L x (L/2 + 1) slots, so that every LDS
@@ -648,36 +653,39 @@ __global__ void __launch_bounds__(kBigInvThreads) big_irfft2_kernel(BigInvParams
 // conditions that are uniform, makes the compiler keep more of the
 // transform's values live across the stores, and spill), pass 2 runs on the
 // row pairs that hold kept rows only, and the output pass applies the
-// rotation and the 1/L^2 scale. MODE as for the kernel above; SPLIT: more than one partial
-// spectrum to sum (the weight gradient's split), loaded in batches of 16
-// rows so that the partial sums and the loads in flight fit the registers.
+// rotation and the 1/L^2 scale. MODE as for the kernel above; SPLIT: more
+// than one partial spectrum to sum (the weight gradient's split), loaded in
+// batches of 16 rows so that the partial sums and the loads in flight fit
+// the registers.
 template <bool O32, int MODE, bool SPLIT>
 __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
-  constexpr int L = 64, H2 = L / 2, V = L / 2 + 1, RI = Big<L>::RI;
+  constexpr int L = 64, H2 = L / 2, V = L / 2 + 1, RI = Big<L>::RI, HALF = 256;
   extern __shared__ float smem[];
   float2* lds = reinterpret_cast<float2*>(smem);
   const float* ldf = smem;
   const int KR = p.KR, rot = p.rot, TQ = p.TQ;
   const int TSZ = inv_tile_stride<L>(L);
-  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int tid = threadIdx.x;
+  const int half = tid >> 8, ht = tid & (HALF - 1);  // half of the workgroup (four waves), thread in it
   const int P = p.T * p.T, tpc = p.n_img * P;
   const size_t fstride = size_t(p.n_ch) * tpc;
   const long ngroups = long(p.n_ch) * p.ngrp;
   // the stored rows (k - rot) mod L of kept rows k < KR are a cyclic run
   // from s0; the row pairs w0, w0 + 1, ... (mod L/2) cover it
   const int s0 = (L - rot) & (L - 1), w0 = s0 >> 1, npair = min(H2, ((s0 & 1) + KR + 1) >> 1);
+  const int ntask1 = H2 * TQ, ntask2 = npair * TQ;  // tasks of passes 1 and 2 (tile fastest)
   using off_t = typename std::conditional<O32, unsigned, size_t>::type;
   auto at = [&](const float2* base, off_t e) { return O32 ? load_at(base, unsigned(e) * 8u) : base[e]; };
+  float re[L], im[L];  // a lane's sequence: loaded columns, then the pass's working values
 
-  // pass 1: column w of tile q (summed over the partial spectra); column 0
-  // carries the real columns 0 and L/2 together as h0[u] + i h1[u], rows
+  // column w of tile q into re/im (summed over the partial spectra); column
+  // 0 carries the real columns 0 and L/2 together as h0[u] + i h1[u], rows
   // past L/2 rebuilt as the conjugates of rows L - u (not stored)
-  auto column = [&](int ch, int t0, int q, int w) {
-    float re[L], im[L];
+  auto fetch = [&](int ch, int t0, int q, int w) __attribute__((always_inline)) {
     const size_t tb = size_t(ch) * tpc + t0 + q;
     const off_t row = off_t(size_t(V) * fstride);
     // rows [u0, u0 + NU) of one partial: assigned (first) or added
-    auto gather = [&](const float2* base, int u0c, auto nu, auto first) {
+    auto gather = [&](const float2* base, int u0c, auto nu, auto first) __attribute__((always_inline)) {
       constexpr int NU = decltype(nu)::value;
       constexpr bool FIRST = decltype(first)::value;
       const int u0 = u0c;
@@ -695,12 +703,12 @@ __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
         // rows u <= L/2 of columns 0 and L/2 give rows u and L - u
         off_t e = off_t(size_t(u0) * V * fstride + tb);
         if (O32) asm volatile("" : "+v"(e));
-        const off_t half = off_t(size_t(H2) * fstride);
+        const off_t hoff = off_t(size_t(H2) * fstride);
 #pragma unroll
         for (int i = 0; i < NU; ++i) {
           const int u = u0 + i;
           if (u > H2) break;
-          const float2 b0 = at(base, e), b1 = at(base, e + half);
+          const float2 b0 = at(base, e), b1 = at(base, e + hoff);
           e += row;
           re[u] = FIRST ? b0.x - b1.y : re[u] + (b0.x - b1.y);
           im[u] = FIRST ? b0.y + b1.x : im[u] + (b0.y + b1.x);
@@ -711,7 +719,7 @@ __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
         }
       }
     };
-    if (!SPLIT) {
+    if constexpr (!SPLIT) {
       gather(p.src, 0, std::integral_constant<int, L>{}, std::true_type{});
     } else {
       // column 0 reads rows [0, L/2] only, which the first three batches
@@ -724,6 +732,9 @@ __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
         asm volatile("" ::: "memory");
       }
     }
+  };
+  // pass 1 on the fetched column w of tile q
+  auto column = [&](int q, int w) __attribute__((always_inline)) {
     fft_dif<L, +1, false>(re, im);  // row r at position bitrev(r)
     float2* bq = lds + (q * TSZ + w);
 #pragma unroll
@@ -731,8 +742,7 @@ __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
   };
   // pass 2: rows 2w, 2w + 1 to L^2 times their real rows, written over their
   // own storage (slot 0 of a row holds its bins 0 and L/2 as (re, im))
-  auto rows = [&](int q, int w) {
-    float re[L], im[L];
+  auto rows = [&](int q, int w) __attribute__((always_inline)) {
     float2* za = lds + (q * TSZ + 2 * w * RI);
     {
       const float2 a0 = za[0], b0 = za[RI];
@@ -789,18 +799,34 @@ __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
   };
 
   const GroupWalk wk = group_walk(ngroups, true);
-  const int wave = tid >> 6, lane = tid & 63, nwave = nthr >> 6;
-  for (long g = wk.g; g < wk.end; g += wk.step) {
+  const int wave = tid >> 6, lane = tid & 63, nwave = blockDim.x >> 6;
+  // this half's first task of a group: tile ht % TQ, column ht / TQ
+  auto prefetch = [&](long g) __attribute__((always_inline)) {
+    const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * TQ;
+    if (ht < ntask1 && ht % TQ < min(TQ, tpc - t0)) fetch(ch, t0, ht % TQ, ht / TQ);
+  };
+  if (half == 0 && wk.g < wk.end) prefetch(wk.g);
+  int turn = 0;  // the half whose columns are in registers for this group
+  for (long g = wk.g; g < wk.end; g += wk.step, turn ^= 1) {
     const int ch = int(g / p.ngrp), t0 = int(g % p.ngrp) * TQ;
     const int nq = min(TQ, tpc - t0);
-    for (int task = tid; task < H2 * TQ; task += nthr) {
-      const int q = task % TQ;
-      if (q < nq) column(ch, t0, q, task / TQ);
+    const bool mine = half == turn;
+    if (mine) {
+      if (ht < ntask1 && ht % TQ < nq) column(ht % TQ, ht / TQ);
+    } else {
+      for (int k = HALF + ht; k < ntask1; k += HALF) {
+        if (k % TQ >= nq) continue;
+        fetch(ch, t0, k % TQ, k / TQ);
+        column(k % TQ, k / TQ);
+      }
     }
     __syncthreads();
-    for (int task = tid; task < npair * TQ; task += nthr) {
-      const int q = task % TQ;
-      if (q < nq) rows(q, (w0 + task / TQ) & (H2 - 1));
+    if (mine) {
+      if (ht < ntask2 && ht % TQ < nq) rows(ht % TQ, (w0 + ht / TQ) & (H2 - 1));
+    } else {
+      for (int k = HALF + ht; k < ntask2; k += HALF)
+        if (k % TQ < nq) rows(k % TQ, (w0 + k / TQ) & (H2 - 1));
+      if (g + wk.step < wk.end) prefetch(g + wk.step);
     }
     __syncthreads();
     if (MODE == 1) {

@@ -554,6 +554,34 @@ def test_full_size_layers(gpu_lib, name, tiling):
     check_full_size(name, y, dx, dw, label=f"{name} {tiling} {y.shape}")
 
 
+def test_spectra_past_32_bit_offsets(gpu_lib):
+    """A layer whose gradient-window and forward-product spectra exceed 4 GB
+    (2112 bins x 512 kernels x 576 tiles x 8 bytes = 5.0 GB), so that the
+    L = 64 forward transform, the inverse and the matrix-core contraction take
+    their 64-bit-offset forms; outputs on stratified samples of every image
+    and block of 32 channels, and whole dw planes of kernel-channel pairs
+    spanning every block of 32."""
+    B, C, K, N, n, L, b = 64, 32, 512, 128, 16, 64, 49
+    ly = Layer("wide_spectra", B, C, K, N, n)
+    x, w, g = make_inputs(ly, seed=41)
+    plan = binding.Plan(B, C, K, N, n, device=DEV, tiling=(L, b))
+    geo = plan.geometry
+    assert geo["F"] * K * B * geo["T"] ** 2 * 8 > 2 ** 32
+    y, dx, dw = run_training_step(plan, x, w, g)
+    del plan
+    M = ly.M
+    rng = np.random.default_rng(5)
+    iy, ix = _stratified(rng, B, K, M), _stratified(rng, B, C, N)
+    cs, ks = _one_per_block(rng, C), _one_per_block(rng, K)
+    e = (relerr(y[tuple(iy)], oracle.conv_forward_at(x, w, *iy)),
+         relerr(dx[tuple(ix)], oracle.conv_backward_data_at(g, w, N, *ix)),
+         relerr(dw[np.ix_(ks, cs)], oracle.conv_backward_filter(x[:, cs], g[:, ks], n)))
+    print(f"spectra past 4 GB: {len(iy[0])} y, {len(ix[0])} dx pixels, dw {len(ks)}x{len(cs)} pairs: "
+          f"{e[0]:.2e} {e[1]:.2e} {e[2]:.2e}", flush=True)
+    assert max(e) <= TOL, e
+    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dw).all()
+
+
 CHAIN = [  # (B, C, J, K, N, n1, n2, tiling, method): two stacked layers composed in the frequency domain
     (2, 3, 5, 4, 20, 3, 4, "paper", "oaa"),        # L = 16, vector-ALU composition
     (2, 40, 36, 48, 24, 3, 3, "paper", "oaa"),     # matrix-core composition and passes

@@ -6,25 +6,26 @@
 // A workgroup keeps the intermediate of TQ tiles in LDS (17 KB per tile at
 // L = 64, so one workgroup of up to nine tiles per CU) and walks over groups
 // of TQ consecutive tiles of one channel:
-//  * forward: at L = 64 a lane holds a whole sequence and the two halves of
-//    the workgroup alternate between transforming a group and loading the
-//    next (big_rfft2_lane_kernel); at L = 128, and for launches of few
-//    groups, each L-point transform is split over a pair of neighbouring
-//    lanes (fft_dif_split, L/2 complex values per lane). Pass 1 transforms
-//    the column pairs (s, s + L/2) of every window along its rows, lanes over
-//    consecutive columns so that the loads of a row are coalesced, and keeps
-//    rows u <= L/2 of the two real columns' spectra (rows past L/2 are their
-//    conjugates); pass 2 transforms each of those rows along the columns and
-//    writes bins (u, v) and (L - u, v) of the half spectrum with lanes over
-//    the group's tiles, so that a store instruction writes runs of TQ
-//    consecutive tiles of a bin. The next group's input is loaded into
-//    registers while the current group's second pass runs.
+//  * forward: pass 1 transforms the column pairs (s, s + L/2) of every window
+//    along its rows, lanes over consecutive columns so that the loads of a
+//    row are coalesced, and keeps rows u <= L/2 of the two real columns'
+//    spectra (rows past L/2 are their conjugates); pass 2 transforms each of
+//    those rows along the columns and writes bins (u, v) and (L - u, v) of
+//    the half spectrum with lanes over the group's tiles, so that a store
+//    instruction writes runs of TQ consecutive tiles of a bin. Consecutive
+//    groups run on one XCD at about the same time, so the runs that
+//    neighbouring groups write into a bin meet in that XCD's L2;
 //  * inverse: pass 1 inverts the columns v <= L/2 (loads in runs of TQ
 //    tiles), pass 2 inverts row pairs to real rows, pass 3 writes the kept
-//    part of each tile (crop) or the overlap-added plane. At L = 64 a lane
-//    holds a whole sequence (big_irfft2_lane_kernel); at L = 128 a lane pair.
-// Consecutive groups run on one XCD at about the same time, so the runs that
-// neighbouring groups write into a bin meet in that XCD's L2.
+//    part of each tile (crop) or the overlap-added plane. A workgroup walks a
+//    contiguous range of groups.
+// At L = 64 a lane holds a whole 64-point sequence, and the two halves of the
+// workgroup alternate between transforming a group and loading the next into
+// their registers (big_rfft2_lane_kernel, big_irfft2_lane_kernel). At
+// L = 128, and for forward launches of few groups, each L-point transform is
+// split over a pair of neighbouring lanes (fft_dif_split, L/2 complex values
+// per lane) and the whole workgroup transforms a group; the forward loads the
+// next group into registers while the current group's second pass runs.
 #include <algorithm>
 #include <type_traits>
 

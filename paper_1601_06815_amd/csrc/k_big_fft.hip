@@ -90,12 +90,9 @@ __device__ __forceinline__ long first_group() {
 // The groups a workgroup takes: g, g + step, ... below end. Interleaved
 // (consecutive groups on the workgroups of one XCD at about the same time)
 // or, with `contig`, a contiguous range per workgroup (the workgroups of one
-// XCD holding consecutive ranges). The inverse walks contiguous ranges: the
-// runs of a plane's tiles in a bin share 64-byte sectors with the next
-// plane's, which the same workgroup then reads while they are still in L2
-// (measured at the large-kernel layer: forward inverse 0.99 -> 0.93 ms,
-// error-propagation inverse 0.33 -> 0.31 ms; the forward transforms were as
-// fast or slower that way).
+// XCD holding consecutive ranges). The forward transforms walk interleaved;
+// the L = 128 inverse walks contiguous ranges (at L = 64 that was 0.99 ->
+// 0.93 ms against interleaved for the large-kernel forward inverse).
 struct GroupWalk {
   long g, end, step;
 };
@@ -106,6 +103,27 @@ __device__ __forceinline__ GroupWalk group_walk(long ngroups, bool contig) {
     return {w * R, min(ngroups, (w + 1) * R), 1};
   }
   return {w, ngroups, long(gridDim.x)};
+}
+
+// Teams of S workgroups of one XCD (consecutive first_group numbers; nwg is
+// a multiple of 8 S, else S is 1) take S consecutive groups at a time, and
+// each team walks a contiguous range. The runs of S neighbouring groups in a
+// bin share 128-byte lines, which the first of them to read one brings into
+// the XCD's L2 for the others, read at about the same time. A line shared by
+// groups a workgroup takes one after the other is gone from L2 by the next
+// group (a workgroup's group reads 2050 bins), so a contiguous walk with S = 1
+// reads each such line again. A team of a whole XCD on one channel at a time
+// (S = 32, like the interleaved walk) crowds all XCDs onto a few channels'
+// bins and was slower. Measured at the large-kernel layer (groups of one
+// nine-tile plane in the forward overlap-add, of 8 tiles = 64 bytes in the
+// crops): forward inverse 0.675 / 0.625 / 0.622 / 0.694 ms at S = 1, 4, 8,
+// 16; the crops 0.224 -> 0.217 and 0.151 -> 0.142 ms at S = 2, where a pair
+// of groups covers one line.
+__device__ __forceinline__ GroupWalk group_walk_team(long ngroups, int S0) {
+  const long w = first_group(), nwg = gridDim.x;
+  const long S = nwg % (8 * S0) == 0 ? S0 : 1;
+  const long R = (ngroups + nwg - 1) / nwg, team = w / S, s = w % S;
+  return {team * R * S + s, min(ngroups, (team + 1) * R * S), S};
 }
 
 // ---------------------------------------------------------------------------
@@ -799,7 +817,7 @@ __global__ void __launch_bounds__(512) big_irfft2_lane_kernel(BigInvParams p) {
     }
   };
 
-  const GroupWalk wk = group_walk(ngroups, true);
+  const GroupWalk wk = group_walk_team(ngroups, MODE == 1 ? 8 : 2);
   const int wave = tid >> 6, lane = tid & 63, nwave = blockDim.x >> 6;
   // this half's first task of a group: tile ht % TQ, column ht / TQ
   auto prefetch = [&](long g) __attribute__((always_inline)) {

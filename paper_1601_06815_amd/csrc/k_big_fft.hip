@@ -17,7 +17,10 @@
 //    neighbouring groups write into a bin meet in that XCD's L2;
 //  * inverse: pass 1 inverts the columns v <= L/2 (loads in runs of TQ
 //    tiles), pass 2 inverts row pairs to real rows, pass 3 writes the kept
-//    part of each tile (crop) or the overlap-added plane. A workgroup walks a
+//    part of each tile (crop) or the overlap-added plane. At L = 64 teams of
+//    workgroups of one XCD take neighbouring groups together, each team
+//    walking a contiguous range, so that the 128-byte lines that those
+//    groups' runs share come from HBM once; at L = 128 a workgroup walks a
 //    contiguous range of groups.
 // At L = 64 a lane holds a whole 64-point sequence, and the two halves of the
 // workgroup alternate between transforming a group and loading the next into
@@ -59,12 +62,12 @@ struct Big {
   static constexpr int SIDE_MAX = L == 64 ? 3 : 1;  // blocks per side of a one-group plane
 };
 
-// threads of a workgroup (at most): eight waves, which leaves a lane 256
-// registers; L per tile, one task per thread with the register prefetch,
+// threads of a lane-pair forward workgroup: eight waves, which leaves a lane
+// 256 registers; L per tile, one task per thread with the register prefetch,
 // else threads loop over the tasks
 template <int L, bool PF>
 constexpr int big_threads() {
-  return L == 64 && !PF ? 576 : 512;
+  return 512;
 }
 // threads of an inverse workgroup: eight waves (a lane's registers capped
 // at 256)

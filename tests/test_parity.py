@@ -201,6 +201,32 @@ def test_transform_side_64(gpu_lib, shape):
     check_whole(x, w, g, tiling=(L, b), method=m)
 
 
+# Shapes for the L = 64 inverses' group walk, with groups of one plane in the
+# forward overlap-add (K B groups) and of 8 tiles in the crops (C ceil(B P / 8)
+# for the error propagation, C ceil(K / 8) for the weight gradient), on a grid
+# of min(256, groups rounded up to 8) workgroups. Teams of 8 (forward) or 2
+# (crops) workgroups need a grid that is a multiple of 64 or 16, else each
+# workgroup walks alone.
+TEAM_WALK = [  # (B, C, K, N, n): at (64, 49)
+    (3, 40, 100, 64, 16),   # P = 4: forward 300 groups, teams of 8 with a ragged last range; crops of
+                            # 80 (the last group of each channel 4 tiles) and 520 groups in teams of 2
+    (1, 9, 65, 64, 16),     # forward 65 groups on 72 workgroups: alone; crops 9 groups in teams of 2
+                            # and 81 groups alone
+    (2, 24, 64, 64, 16),    # forward 128 groups, teams of 8 over exact ranges; crops 24 (alone), 192
+    (4, 16, 48, 128, 16),   # P = 9: forward 192 planes in teams of 8; crops of 80 groups spanning
+                            # images and 96 groups, teams of 2
+]
+
+
+@pytest.mark.parametrize("shape", TEAM_WALK, ids=lambda s: "x".join(map(str, s)))
+def test_inverse_team_walk_shapes(gpu_lib, shape):
+    """Every pass at L = 64 against the oracle, compared whole, on grids that
+    take each of the inverses' walks (teams, ragged team ranges, alone)."""
+    B, C, K, N, n = shape
+    x, w, g = make_inputs(Layer("t", B, C, K, N, n), seed=173 + sum(shape))
+    check_whole(x, w, g, tiling=(64, 49))
+
+
 @pytest.mark.parametrize("shape", [sh for sh in BIG64 if sh[7] == "oaa" and sh[1] <= 4],
                          ids=lambda s: "x".join(map(str, s)))
 def test_transform_side_64_unfused(gpu_lib, shape):

@@ -45,8 +45,9 @@
 // has at least this many tiles, a little over two rounds of its 512 resident
 // workgroups. More partial sums balance the rounds better but cost the
 // inverse one more read of the whole weight-gradient spectrum each: measured,
-// 1152 gives the large layer 2 partial sums (1 was slower) and the 56 x 56
-// layer 8 (11 cost 0.03 ms more; overridable at build time for sweeps).
+// 1152 gives the 56 x 56 layer 8 (11 cost 0.03 ms more) and the large-kernel
+// layer at L = 64 one (2 took 0.79 against 0.75 ms for the contraction, and
+// 0.19 ms more per step); overridable at build time for sweeps.
 #ifndef OAA_SPLIT_TILES
 #define OAA_SPLIT_TILES 1152
 #endif

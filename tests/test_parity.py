@@ -247,6 +247,8 @@ FUSED = [  # (B, C, K, N, n, L, b): the fused few-channel passes (L = 64, C <= 4
     (3, 1, 2, 9, 1, 64, 8),        # n = 1: no overlap, nothing carried
     (1, 3, 4, 80, 33, 64, 32),     # n = 33, b = n - 1: 32 carried rows, KR = 64
     (5, 2, 7, 37, 4, 64, 20),      # odd block count per split, B T not a multiple of the splits
+    (2, 2, 64, 100, 7, 64, 58),    # partial sums over block-row ranges, inverted on 16 workgroups in
+                                   # teams of two (2 x 64 kernel-channel pairs, groups of 8)
 ]
 
 
